@@ -1,0 +1,121 @@
+"""The oracle against its pins, and planted mistakes against the same pins.
+
+A mutant replaces one oracle function with a plausible wrong version (a dropped ReLU, an
+off-by-one window, max instead of mean, ...). Each mutant must fail at least one pin, which shows
+that the pins would catch that kind of mistake in the oracle itself.
+"""
+import numpy as np
+import pytest
+
+import oracle.lsa_oracle as orc
+from tests import oracle_pins as pins
+
+
+@pytest.mark.parametrize("pin", pins.ALL_PINS, ids=lambda f: f.__name__)
+def test_oracle_pin(pin):
+    pin(orc)
+
+
+def _no_relu(q_t, w_t, keys):
+    return np.asarray(w_t) @ (np.asarray(q_t) @ np.asarray(keys).T)
+
+
+def _relu_after_sum(q_t, w_t, keys):
+    return np.maximum(np.asarray(w_t) @ (np.asarray(q_t) @ np.asarray(keys).T), 0.0)
+
+
+def _max_pool(k_hat, sub_block):
+    k_hat = np.asarray(k_hat, np.float64)
+    n = k_hat.shape[0] // sub_block
+    m = k_hat[: n * sub_block].reshape(n, sub_block, -1).max(axis=1)
+    return orc.bf16_bits_to_f64(orc.f64_to_bf16_bits(m))
+
+
+def _window_off_by_one(t, prm):
+    sink = np.arange(0, min(prm.k_sink, t + 1))
+    swa = np.arange(max(0, t - prm.k_swa), t + 1)
+    lo, hi = prm.k_sink, t - prm.k_swa - 1
+    return sink, swa, ((lo, hi) if lo <= hi else None)
+
+
+def _no_sink(t, prm):
+    sink = np.arange(0)
+    swa = np.arange(max(0, t - prm.k_swa + 1), t + 1)
+    lo, hi = prm.k_sink, t - prm.k_swa
+    return sink, swa, ((lo, hi) if lo <= hi else None)
+
+
+def _ties_to_later(scores, ids, k):
+    ids = np.asarray(ids, np.int64)
+    if len(ids) <= k:
+        return np.sort(ids)
+    order = np.lexsort((-ids, -np.asarray(scores, np.float64)))
+    return np.sort(ids[order[:k]])
+
+
+def _truncating_bf16(x):
+    x = np.asarray(x, np.float64).astype(np.float32)
+    return (x.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def _e4m3_bias8(codes):
+    c = np.asarray(codes, np.uint8).astype(np.int64)
+    e, m = (c >> 3) & 0xF, (c & 7).astype(np.float64)
+    mag = np.where(e == 0, m * 2.0 ** -10, (1 + m / 8) * np.exp2(e - 8.0))
+    mag = np.where((e == 15) & ((c & 7) == 7), np.nan, mag)
+    return np.where(c & 0x80, -1.0, 1.0) * mag
+
+
+def _cand_with_window(pages, lo, hi, prm):
+    pages = np.asarray(pages, np.int64)
+    pos = (pages[:, None] * prm.page + np.arange(prm.page)[None, :]).reshape(-1)
+    return pos[(pos >= lo) & (pos <= hi + 1)]
+
+
+def _attn_no_scale(q_t, keys, values, scale):
+    return orc.__dict__["_orig_attn"](q_t, keys, values, 1.0)
+
+
+def _attn_log2(q_t, keys, values, scale):
+    o, lse = orc.__dict__["_orig_attn"](q_t, keys, values, scale)
+    return o, lse / np.log(2.0)
+
+
+def _page_score_unweighted(q_t, w_t, k_mean, pages, prm):
+    return orc.__dict__["_orig_page"](q_t, np.ones_like(np.asarray(w_t)), k_mean, pages, prm)
+
+
+def _pages_shifted(lo, hi, prm):
+    return np.arange(lo // prm.page, hi // prm.page)
+
+
+MUTANTS = {
+    "no_relu": ("indexer_scores", _no_relu),
+    "relu_after_head_sum": ("indexer_scores", _relu_after_sum),
+    "max_instead_of_mean": ("sub_block_mean_keys", _max_pool),
+    "window_off_by_one": ("streaming_sets", _window_off_by_one),
+    "sink_excluded": ("streaming_sets", _no_sink),
+    "ties_to_later_position": ("arg_top", _ties_to_later),
+    "bf16_truncation": ("f64_to_bf16_bits", _truncating_bf16),
+    "e4m3_wrong_bias": ("e4m3fn_to_f64", _e4m3_bias8),
+    "candidates_leak_into_window": ("candidates_of_pages", _cand_with_window),
+    "attention_scale_dropped": ("sparse_attention_row", _attn_no_scale),
+    "lse_in_log2": ("sparse_attention_row", _attn_log2),
+    "page_score_ignores_w": ("page_scores", _page_score_unweighted),
+    "last_eligible_page_dropped": ("eligible_pages", _pages_shifted),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    monkeypatch.setitem(orc.__dict__, "_orig_attn", orc.sparse_attention_row)
+    monkeypatch.setitem(orc.__dict__, "_orig_page", orc.page_scores)
+    attr, fn = MUTANTS[name]
+    monkeypatch.setattr(orc, attr, fn)
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(orc)
+        except Exception:  # an assertion or a crash both count as the pin catching the mutant
+            failed.append(pin.__name__)
+    assert failed, f"mutant {name} passed every pin"
