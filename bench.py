@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Benchmark of the LSA hot path on one MI355X.
+
+One step = the whole hot path over one synthetic single-sequence prefill of L = 131072 tokens:
+mean-key cache (lsa_block_means), hierarchical indexer with streaming merge and runs
+(lsa_index_prefill), then sparse attention for the 4 layers of one cross-layer group, all reading
+the same index list (lsa_sparse_attn x 4). Inputs are resident in HBM before timing starts.
+
+Prints one JSON line: tokens/s of the whole step, a roofline entry for the dominant kernel
+(sparse attention: algorithmic bytes per launch over its HIP-event duration against 8 TB/s), the
+indexer's MFMA fraction, and the float64 oracle timed on the host's cores over a bounded sample.
+Diagnostics go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2608_01662_amd import lsa, synth  # noqa: E402
+from paper_2608_01662_amd import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def make_inputs(w, dev):
+    n = w.seq_len
+    H, dqk, dv = w.attn_dims
+    t = {}
+    t["qI"] = synth.device_normal_bf16((n, w.n_heads, w.head_dim), w.seed, synth.T_QI, dev,
+                                       scale=1.0 / math.sqrt(w.head_dim))
+    t["wI"] = synth.device_uniform_f32((n, w.n_heads), w.seed, synth.T_W, dev)
+    if w.fp8:
+        t["kI"], t["ks"] = synth.device_fp8_keys(n, w.head_dim, w.seed, dev)
+    else:
+        t["kI"] = synth.device_normal_bf16((n, w.head_dim), w.seed, synth.T_KI, dev, scale=1.0 / math.sqrt(w.head_dim))
+        t["ks"] = None
+    t["Q"] = [synth.device_normal_bf16((n, H, dqk), w.seed, synth.T_Q + l, dev, rows_per_chunk=2048)
+              for l in range(w.layers)]
+    t["KV"] = [synth.device_normal_bf16((n, dqk), w.seed, synth.T_KV + l, dev) for l in range(w.layers)]
+    t["V"] = [None if w.attn == "mla" else synth.device_normal_bf16((n, dv), w.seed, synth.T_V + l, dev)
+              for l in range(w.layers)]
+    return t
+
+
+def cpu_baseline(w, t, seconds):
+    """The float64 oracle on a bounded sample of query rows of the same workload."""
+    import oracle.lsa_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    n = w.seq_len
+    H, dqk, dv = w.attn_dims
+    g = np.random.default_rng(1234)
+    rows = np.sort(g.choice(np.arange(w.k_cap, n), size=min(512, n - w.k_cap), replace=False))
+    kb = t["kI"].cpu().numpy() if w.fp8 else t["kI"].view(torch.int16).cpu().numpy().view(np.uint16)
+    ks = t["ks"].cpu().numpy() if w.fp8 else None
+    ridx = torch.from_numpy(rows).cuda()
+    qrows = t["qI"].index_select(0, ridx).float().cpu().numpy().astype(np.float64)
+    wrows = t["wI"].index_select(0, ridx).cpu().numpy()
+    Qrows = [q.index_select(0, ridx).view(torch.int16).cpu().numpy().view(np.uint16) for q in t["Q"]]
+    KVb = [kv.view(torch.int16).cpu().numpy().view(np.uint16) for kv in t["KV"]]
+    Vb = [None if v is None else v.view(torch.int16).cpu().numpy().view(np.uint16) for v in t["V"]]
+    prm = orc.IndexParams(page=w.page, sub_block=w.sub_block, keep_pages=w.keep_pages, k_sparse=w.k_sparse,
+                          k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align)
+    t0 = time.perf_counter()
+    k_hat = orc.dequantized_keys(kb, ks)
+    k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block)
+    t_once = time.perf_counter() - t0
+    done = 0
+    t1 = time.perf_counter()
+    for i, tpos in enumerate(rows):
+        r = orc.index_row(int(tpos), qrows[i], wrows[i], k_hat, k_mean, prm)
+        for l in range(w.layers):
+            orc.attention_for_set(Qrows[l][i], KVb[l], Vb[l], r["S"], dv, w.sm_scale)
+        done += 1
+        if time.perf_counter() - t1 > seconds:
+            break
+    per_row = (time.perf_counter() - t1) / done
+    full = t_once + n * per_row
+    return {"value": n / full, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"{done} query rows at random positions in [K_cap, L) through the indexer and "
+                       f"{w.layers} attention layers, plus the one-off key decode and mean keys "
+                       f"({t_once:.2f} s); tokens/s extrapolated to all {n} rows "
+                       f"({per_row * 1e3:.1f} ms per row)")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL if not w.decode and not w.chunk])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
+              "(multi-GPU sharding is a design note, not implemented); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        sys.exit("--steps must be >= 1 and --warmup >= 0")
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.BY_NAME[args.workload]
+    n = w.seq_len
+    H, dqk, dv = w.attn_dims
+    prm, aprm = w.index_params(), w.attn_params()
+    log(f"[bench] {w.name}: generating inputs on {torch.cuda.get_device_name(dev)}")
+    t = make_inputs(w, dev)
+    bk = torch.empty((n // w.sub_block, w.head_dim), dtype=torch.bfloat16, device=dev)
+    out = dict(idx=torch.empty((n, w.k_cap), dtype=torch.int32, device=dev),
+               count=torch.empty((n,), dtype=torch.int32, device=dev),
+               runs=torch.empty((n, w.k_cap, 2), dtype=torch.int32, device=dev),
+               run_count=torch.empty((n,), dtype=torch.int32, device=dev))
+    ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n, n)), dtype=torch.uint8, device=dev)
+    ws_attn_n = lsa.attn_workspace_size(aprm, n, w.k_cap, False)
+    ws_attn = torch.empty(max(1, ws_attn_n), dtype=torch.uint8, device=dev)
+    O = [torch.empty((n, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
+    LSE = [torch.empty((n, H), dtype=torch.float32, device=dev) for _ in range(w.layers)]
+    torch.cuda.synchronize()
+    log(f"[bench] inputs ready; {torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        lsa.block_means(prm, t["kI"], t["ks"], out=bk)
+        if ev is not None:
+            ev[1].record()
+        lsa.index_prefill(prm, t["qI"], t["wI"], t["kI"], t["ks"], bk, 0, n_kv=n, runs=True,
+                          workspace=ws_idx, out=out)
+        if ev is not None:
+            ev[2].record()
+        for l in range(w.layers):
+            lsa.sparse_attn(aprm, t["Q"][l], t["KV"][l], t["V"][l], out["idx"], out["count"], out=O[l],
+                            lse=LSE[l], workspace=ws_attn if ws_attn_n else None)
+            if ev is not None:
+                ev[3 + l].record()
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup step {i + 1}/{args.warmup} done")
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3 + w.layers)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for s in range(args.steps):
+        step(events[s])
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+    bm_ms = np.mean([e[0].elapsed_time(e[1]) for e in events])
+    idx_ms = np.mean([e[1].elapsed_time(e[2]) for e in events])
+    attn_ms = [np.mean([e[2 + l].elapsed_time(e[3 + l]) for e in events]) for l in range(w.layers)]
+    attn_avg = float(np.mean(attn_ms))
+    log(f"[bench] {args.steps} steps: {ms_per_step:.2f} ms/step (block means {bm_ms:.3f}, index {idx_ms:.2f}, "
+        f"attention per layer {attn_avg:.2f} ms)")
+
+    # ---- algorithmic work (per launch / per step)
+    cnt = out["count"].cpu().numpy().astype(np.int64)
+    sum_s = int(cnt.sum())
+    row_kv_bytes = dqk * 2 if w.attn == "mla" else (dqk + dv) * 2
+    attn_bytes = (sum_s * row_kv_bytes + sum_s * 4                       # gathered rows + their indices
+                  + n * H * dqk * 2 + n * H * dv * 2 + n * H * 4 + n * 4)  # Q in, O and lse out, count
+    attn_flops = 2.0 * H * sum_s * (dqk + dv)
+    tpos = np.arange(n)
+    hi = tpos - w.k_swa
+    n_elig_pages = np.where(hi >= w.k_sink, hi // w.page - w.k_sink // w.page + 1, 0)
+    cand = np.where(hi >= w.k_sink, np.minimum(n_elig_pages, w.keep_pages) * w.page, 0)
+    sub_per_page = w.page // w.sub_block
+    idx_flops = 2.0 * w.n_heads * w.head_dim * (float(n_elig_pages.sum()) * sub_per_page + float(cand.sum()))
+    attn_gbs = attn_bytes / (attn_avg * 1e-3) / 1e9
+    res = {
+        "metric": "LSA prefill tokens/s at L=128K (indexer+attn)",
+        "value": n / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "seq_len": n, "layers_sharing_index": w.layers,
+                   "indexer": {"heads": w.n_heads, "head_dim": w.head_dim, "keys": "fp8_e4m3fn" if w.fp8 else "bf16",
+                               "page": w.page, "sub_block": w.sub_block, "keep_pages": w.keep_pages,
+                               "k_sparse": w.k_sparse, "k_sink": w.k_sink, "k_swa": w.k_swa,
+                               "run_align": w.run_align},
+                   "attention": {"kind": w.attn, "heads": H, "d_qk": dqk, "d_v": dv}},
+        "roofline": {"kernel": "mla_attn_kernel", "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_avg},
+        "breakdown": {
+            "block_means_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,
+            "indexer_scoring_tflops": idx_flops / (idx_ms * 1e-3) / 1e12,
+            "indexer_mfma_frac": idx_flops / (idx_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+            "attn_tflops": attn_flops / (attn_avg * 1e-3) / 1e12,
+            "attn_mfma_frac": attn_flops / (attn_avg * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+            "attn_gather_gbs": sum_s * row_kv_bytes / (attn_avg * 1e-3) / 1e9,
+            "attn_tokens_per_s_per_layer": n / (attn_avg * 1e-3),
+            "mean_index_list_len": sum_s / n,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the oracle for ~{args.cpu_seconds:.0f} s on the host")
+        res["cpu_baseline"] = cpu_baseline(w, t, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,600 @@
+// LSA indexer kernels for gfx950: mean-key cache, coarse page scoring, page top-M,
+// fine token scoring, token top-K with the streaming merge, and run encoding.
+//
+// Paper: "LongCat Sparse Attention" (arXiv 2608.01662), Sec. 2.2 Eq. (1)-(2),
+// Sec. 3.1 Eq. (6)-(7), Sec. 3.3 Eq. (9)-(12).
+//
+// Score layout. Both scoring stages are dense contractions Q_I (heads x d_I) times keys
+// (d_I x 32 keys) on v_mfma_f32_32x32x16_bf16: the 32 MFMA rows are the indexer heads (zero-
+// padded when H_I < 32), the 32 columns are keys. In the accumulator layout each lane owns one
+// key column and 16 heads, so ReLU, the head weights and the sum over heads (Eq. 1 / Eq. 9) are
+// 16 in-lane FMAs plus one exchange with the lane 32 apart. fp8 keys are widened to bf16 exactly
+// (e4m3 has 4 significant bits) and the per-token scale is applied after the sum, which is
+// exact algebra since ReLU(s x) = s ReLU(x) for s > 0.
+//
+// The contraction over d_I uses a permuted order of the dimensions: in k-step s the lanes of
+// half h supply dims (d_I/2)*h + 8*s .. +7 of both operands. Any permutation applied to both
+// operands leaves the dot product unchanged, and this one lets every lane read one contiguous
+// run of key bytes.
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace lsa {
+
+// ============================================================================ row geometry
+struct RowInfo {
+  int64_t t;       // query position
+  int valid;       // 0: skip the row (bad context length)
+  int64_t lo, hi;  // eligible range E_t = [lo, hi] (empty if lo > hi)
+  int64_t p_lo, p_hi;
+};
+
+__device__ __forceinline__ RowInfo row_info(const IndexGeom& g, int64_t row) {
+  RowInfo r;
+  if (g.ctx_len) {
+    const int64_t c = g.ctx_len[row];
+    r.valid = (c >= 1 && c <= (int64_t)g.max_pages * g.kv_page);
+    r.t = r.valid ? c - 1 : 0;
+  } else {
+    r.valid = 1;
+    r.t = g.q_start + row;
+  }
+  r.lo = g.k_sink;
+  r.hi = r.t - g.k_swa;
+  r.p_lo = r.lo / g.P;
+  r.p_hi = r.hi >= r.lo ? r.hi / g.P : r.p_lo - 1;
+  return r;
+}
+
+// Physical page of logical page `p` of sequence `seq` (-1 if the entry is out of range).
+__device__ __forceinline__ int64_t phys_page(const IndexGeom& g, int64_t seq, int64_t p) {
+  if (p < 0 || p >= g.max_pages) return -1;
+  const int64_t ph = g.page_table[seq * g.max_pages + p];
+  return (ph >= 0 && ph < g.n_phys) ? ph : -1;
+}
+
+// ============================================================================ mean keys (Stage 1 cache)
+// One thread per (sub-block, group of 4 dims): fp32 sum of s_i * k_i over the B tokens, one
+// multiply by 1/B (B is a power of two, exact), one round-to-nearest-even to bf16.
+template <bool FP8>
+__global__ __launch_bounds__(256) void block_means_kernel(int64_t n_sub, int D, int B, const void* __restrict__ k,
+                                                          const float* __restrict__ ks, uint16_t* __restrict__ out) {
+  const int groups = D / 4;
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= n_sub * groups) return;
+  const int64_t sub = id / groups;
+  const int gq = (int)(id - sub * groups);
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < B; ++i) {
+    const int64_t tok = sub * B + i;
+    if (FP8) {
+      const uint32_t v = reinterpret_cast<const uint32_t*>(k)[tok * groups + gq];
+      const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(v, false);
+      const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(v, true);
+      const float s = ks[tok];
+      acc[0] += s * lo.x; acc[1] += s * lo.y; acc[2] += s * hi.x; acc[3] += s * hi.y;
+    } else {
+      const u32x2 v = reinterpret_cast<const u32x2*>(k)[tok * groups + gq];
+      acc[0] += __uint_as_float(v.x << 16); acc[1] += __uint_as_float(v.x & 0xFFFF0000u);
+      acc[2] += __uint_as_float(v.y << 16); acc[3] += __uint_as_float(v.y & 0xFFFF0000u);
+    }
+  }
+  const float inv = 1.0f / (float)B;
+  u32x2 o;
+  o.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  o.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  reinterpret_cast<u32x2*>(out)[sub * groups + gq] = o;
+}
+
+// ============================================================================ operand loads
+// A operand: 32 (padded) heads of one query row. Lane (head j, half h), k-step s: 8 bf16 at
+// dims (D/2)*h + 8*s.
+template <int D>
+__device__ __forceinline__ void load_query_operand(const uint16_t* __restrict__ q, int H, int64_t row, int lane,
+                                                   u32x4 (&a)[D / 16]) {
+  const int j = lane & 31, h = lane >> 5;
+  if (j < H) {
+    const uint16_t* p = q + (row * H + j) * D + (D / 2) * h;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) a[s] = *reinterpret_cast<const u32x4*>(p + 8 * s);
+  } else {
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) a[s] = u32x4{0, 0, 0, 0};
+  }
+}
+
+// Head weights of the 16 heads this lane holds in the accumulator: 8*(r/4) + 4*h + r%4.
+__device__ __forceinline__ void load_head_weights(const float* __restrict__ w, int H, int64_t row, int lane, float (&wr)[16]) {
+  const int h = lane >> 5;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int head = 8 * (r / 4) + 4 * h + (r % 4);
+    wr[r] = head < H ? w[row * H + head] : 0.f;
+  }
+}
+
+// B operand for one key row: lane half h reads dims [(D/2)*h, (D/2)*h + D/2) of key `krow`.
+template <int D, bool FP8>
+__device__ __forceinline__ void load_key_operand(const void* __restrict__ k, int64_t krow, int lane, u32x4 (&b)[D / 16]) {
+  const int h = lane >> 5;
+  if (FP8) {
+    const u32x4* p = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(k) + krow * D + (D / 2) * h);
+#pragma unroll
+    for (int v = 0; v < D / 32; ++v) {
+      const u32x4 raw = p[v];  // 16 codes = k-steps 2v, 2v+1
+      b[2 * v] = fp8x8_to_bf16x8(raw.x, raw.y);
+      b[2 * v + 1] = fp8x8_to_bf16x8(raw.z, raw.w);
+    }
+  } else {
+    const u32x4* p = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(k) + krow * D + (D / 2) * h);
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) b[s] = p[s];
+  }
+}
+
+// sum_j w_j ReLU(acc_j) over the 32 heads of this lane's key column (Eq. 1 / Eq. 9).
+__device__ __forceinline__ float head_reduce(const f32x16& acc, const float (&wr)[16]) {
+  float v = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) v = fmaf(wr[r], fmaxf(acc[r], 0.f), v);
+  return v + __shfl_xor(v, 32);
+}
+
+// ============================================================================ Stage 1: coarse page scores
+// Eq. (9). Grid: (ceil(n_rows / R), chunks). Each wave takes tiles of 32 mean keys of the
+// chunk; R query rows share each loaded tile (prefill). Output: order keys of the page scores,
+// page_keys[row * ld + p] for eligible pages p.
+template <int D, int R, bool PAGED>
+__global__ __launch_bounds__(256) void coarse_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
+                                                     const float* __restrict__ w, const uint16_t* __restrict__ kmean,
+                                                     uint32_t* __restrict__ page_keys, int64_t ld, int tiles_per_chunk) {
+  constexpr int KS = D / 16;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31;
+  const int64_t row0 = (int64_t)blockIdx.x * R;
+  const int nsub = g.P / g.B;
+
+  RowInfo ri[R];
+  int64_t max_tiles = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = row0 + r;
+    ri[r] = row < n_rows ? row_info(g, row) : RowInfo{0, 0, 1, 0, 0, -1};
+    if (ri[r].valid && ri[r].p_hi >= ri[r].p_lo) {
+      const int64_t nt = ((ri[r].p_hi - ri[r].p_lo + 1) * nsub + 31) / 32;
+      max_tiles = nt > max_tiles ? nt : max_tiles;
+    }
+  }
+  const int64_t tile_beg = (int64_t)blockIdx.y * tiles_per_chunk;
+  const int64_t tile_end = tile_beg + tiles_per_chunk < max_tiles ? tile_beg + tiles_per_chunk : max_tiles;
+  if (tile_beg >= tile_end) return;
+
+  u32x4 a[R][KS];
+  float wr[R][16];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = row0 + r < n_rows ? row0 + r : n_rows - 1;
+    load_query_operand<D>(q, g.H, row, lane, a[r]);
+    load_head_weights(w, g.H, row, lane, wr[r]);
+  }
+  const int64_t p_base = ri[0].p_lo;  // identical for every row (depends on k_sink only)
+
+  for (int64_t tile = tile_beg + wv; tile < tile_end; tile += 4) {
+    const int64_t sb = tile * 32 + j;            // sub-block counted from the first eligible page
+    const int64_t p = p_base + sb / nsub;
+    const int sub_in_page = (int)(sb % nsub);
+    int64_t mrow = 0;
+    bool okp = true;
+    if (PAGED) {
+      const int64_t ph = (R == 1 && p <= ri[0].p_hi) ? phys_page(g, row0, p) : -1;
+      okp = ph >= 0;
+      mrow = okp ? ph * nsub + sub_in_page : 0;
+    } else {
+      okp = p * nsub + sub_in_page < g.n_sub;
+      mrow = okp ? p * nsub + sub_in_page : 0;
+    }
+    u32x4 b[KS];
+    {
+      const u32x4* pk = reinterpret_cast<const u32x4*>(kmean + mrow * D + (D / 2) * (lane >> 5));
+#pragma unroll
+      for (int s = 0; s < KS; ++s) b[s] = pk[s];
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      f32x16 acc = {};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) acc = mfma32(a[r][s], b[s], acc);
+      float v = head_reduce(acc, wr[r]);
+      for (int o = 1; o < nsub; o <<= 1) v += __shfl_xor(v, o);  // sum the sub-blocks of a page
+      const int64_t row = row0 + r;
+      if (lane < 32 && sub_in_page == 0 && row < n_rows && ri[r].valid && p <= ri[r].p_hi)
+        page_keys[row * ld + p] = okp ? score_key(v) : 0u;
+    }
+  }
+}
+
+// ============================================================================ block-wide top-k
+// Threshold T and tie count of the k largest keys among keys[0..n) (LDS), by four 8-bit radix
+// passes: the selection is {i : key_i > T} plus the first `take_eq` indices with key_i == T.
+template <int NT>
+__device__ void radix_threshold(const uint32_t* keys, int n, int k, uint32_t* hist, int* bc, uint32_t& T, int& take_eq) {
+  uint32_t prefix = 0, mask = 0;
+  int rem = k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += NT) {
+      const uint32_t key = keys[i];
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int l = threadIdx.x;
+      const uint32_t c0 = hist[4 * l], c1 = hist[4 * l + 1], c2 = hist[4 * l + 2], c3 = hist[4 * l + 3];
+      const uint32_t tot = c0 + c1 + c2 + c3;
+      uint32_t suf = tot;  // sum of totals of lanes >= l
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_down(suf, o);
+        if (l + o < 64) suf += x;
+      }
+      uint32_t ge = suf - tot;  // keys in bins above this lane's four
+      const uint32_t c[4] = {c0, c1, c2, c3};
+      for (int bq = 3; bq >= 0; --bq) {
+        const uint32_t above = ge;
+        ge += c[bq];
+        if (above < (uint32_t)rem && ge >= (uint32_t)rem) {
+          bc[0] = 4 * l + bq;
+          bc[1] = (int)above;
+        }
+      }
+    }
+    __syncthreads();
+    const uint32_t d = (uint32_t)bc[0];
+    rem -= bc[1];
+    prefix |= d << shift;
+    mask |= 0xFFu << shift;
+    __syncthreads();
+  }
+  T = prefix;
+  take_eq = rem;
+}
+
+// Visits, in index order, every selected index of keys[0..n) (key > T, or key == T among the
+// first take_eq such) and calls emit(rank, i). Returns the number selected.
+template <int NT, typename F>
+__device__ int select_compact(const uint32_t* keys, int n, uint32_t T, int take_eq, int* wsum, F&& emit) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int base_eq = 0, base_out = 0;
+  for (int c = 0; c < n; c += NT) {
+    const int i = c + threadIdx.x;
+    const uint32_t key = i < n ? keys[i] : 0u;
+    const bool eq = i < n && key == T;
+    const uint64_t beq = __ballot(eq);
+    if (lane == 0) wsum[wv] = __popcll(beq);
+    __syncthreads();
+    int eq_prefix = 0, eq_total = 0;
+#pragma unroll
+    for (int x = 0; x < NW; ++x) {
+      const int v = wsum[x];
+      eq_prefix += x < wv ? v : 0;
+      eq_total += v;
+    }
+    const int eq_rank = base_eq + eq_prefix + __popcll(beq & lanemask_lt());
+    const bool sel = i < n && (key > T || (eq && eq_rank < take_eq));
+    const uint64_t bsel = __ballot(sel);
+    if (lane == 0) wsum[NW + wv] = __popcll(bsel);
+    __syncthreads();
+    int sel_prefix = 0, sel_total = 0;
+#pragma unroll
+    for (int x = 0; x < NW; ++x) {
+      const int v = wsum[NW + x];
+      sel_prefix += x < wv ? v : 0;
+      sel_total += v;
+    }
+    if (sel) emit(base_out + sel_prefix + __popcll(bsel & lanemask_lt()), i);
+    base_eq += eq_total;
+    base_out += sel_total;
+    __syncthreads();
+  }
+  return base_out;
+}
+
+__device__ int block_count_nonzero(const uint32_t* keys, int n, int* wsum) {
+  int c = 0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) c += keys[i] != 0u;
+  c = wave_sum(c);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = c;
+  __syncthreads();
+  int tot = 0;
+  for (int x = 0; x < (int)(blockDim.x >> 6); ++x) tot += wsum[x];
+  __syncthreads();
+  return tot;
+}
+
+// ============================================================================ Stage 1: page top-M
+// Eq. (10): P_t = the M eligible pages of largest coarse score (ties to the smaller page),
+// written in ascending page order and padded with -1. All eligible pages when there are <= M.
+template <int NT>
+__global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ page_keys,
+                                                         int64_t ld, int32_t* __restrict__ pages) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t hist[256];
+  __shared__ int wsum[2 * NT / 64 + 2];
+  const int64_t row = blockIdx.x;
+  const RowInfo ri = row_info(g, row);
+  int32_t* out = pages + row * g.M;
+  const int64_t n_elig = (ri.valid && ri.p_hi >= ri.p_lo) ? ri.p_hi - ri.p_lo + 1 : 0;
+  if (n_elig <= g.M) {
+    for (int i = threadIdx.x; i < g.M; i += NT) out[i] = i < n_elig ? (int32_t)(ri.p_lo + i) : -1;
+    return;
+  }
+  const int n = (int)n_elig;
+  uint32_t* keys = smem;
+  for (int i = threadIdx.x; i < n; i += NT) keys[i] = page_keys[row * ld + ri.p_lo + i];
+  __syncthreads();
+  uint32_t T;
+  int take;
+  radix_threshold<NT>(keys, n, g.M, hist, wsum, T, take);
+  const int64_t p_lo = ri.p_lo;
+  select_compact<NT>(keys, n, T, take, wsum, [&](int rank, int i) { out[rank] = (int32_t)(p_lo + i); });
+}
+
+// ============================================================================ Stage 2: fine token scores
+// Eq. (11) over the recalled pages (Eq. 1 over E_t in flat mode). Grid: (n_rows, chunks of
+// pages_per_wg pages); each wave scores whole pages in 32-token MFMA tiles. Output:
+// fine_keys[row * ldf + k * P + offset] = order key of the score of position page_k * P +
+// offset, or 0 for positions outside E_t.
+template <int D, bool FP8, bool PAGED>
+__global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
+                                                   const float* __restrict__ w, const void* __restrict__ k,
+                                                   const float* __restrict__ kscale, const int32_t* __restrict__ pages,
+                                                   uint32_t* __restrict__ fine_keys, int64_t ldf, int pages_per_wg) {
+  constexpr int KS = D / 16;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31;
+  const int64_t row = blockIdx.x;
+  const RowInfo ri = row_info(g, row);
+  if (!ri.valid || ri.p_hi < ri.p_lo) return;
+  const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
+  const bool flat = g.M <= 0;
+  const int64_t n_sel = flat ? n_elig : (n_elig < g.M ? n_elig : g.M);
+  const int64_t k0 = (int64_t)blockIdx.y * pages_per_wg;
+  const int64_t k1 = k0 + pages_per_wg < n_sel ? k0 + pages_per_wg : n_sel;
+  if (k0 >= k1) return;
+
+  u32x4 a[KS];
+  float wr[16];
+  load_query_operand<D>(q, g.H, row, lane, a);
+  load_head_weights(w, g.H, row, lane, wr);
+
+  for (int64_t kk = k0 + wv; kk < k1; kk += 4) {
+    const int64_t page = flat ? ri.p_lo + kk : (int64_t)pages[row * g.M + kk];
+    int64_t kbase = -1;  // key row of the page's first token
+    if (page >= ri.p_lo && page <= ri.p_hi) {
+      if (PAGED) {
+        const int64_t ph = phys_page(g, row, page);
+        kbase = ph >= 0 ? ph * g.kv_page : -1;
+      } else {
+        kbase = page * g.P;  // positions checked below stay <= hi < n_kv
+      }
+    }
+    uint32_t* dst = fine_keys + row * ldf + kk * g.P;
+    for (int tile = 0; tile < g.P / 32; ++tile) {
+      const int64_t pos = page * g.P + tile * 32 + j;
+      const bool ok = kbase >= 0 && pos >= ri.lo && pos <= ri.hi;
+      const int64_t krow = ok ? kbase + tile * 32 + j : 0;
+      u32x4 b[KS];
+      load_key_operand<D, FP8>(k, krow, lane, b);
+      f32x16 acc = {};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) acc = mfma32(a[s], b[s], acc);
+      float v = head_reduce(acc, wr);
+      if (FP8) v *= kscale[krow];
+      if (lane < 32) dst[tile * 32 + j] = ok ? score_key(v) : 0u;
+    }
+  }
+}
+
+// ============================================================================ final top-K_sparse, merge, runs
+// Eq. (12) / Eq. (7) then Eq. (6): S_t = sink ++ (top K_sparse candidates, ascending) ++ window;
+// idx padded with -1; runs re-encode idx, cut at gaps and at multiples of C.
+template <int NT>
+__global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ fine_keys,
+                                                          int64_t ldf, const int32_t* __restrict__ pages,
+                                                          int32_t* __restrict__ idx, int32_t* __restrict__ count,
+                                                          int32_t* __restrict__ runs, int32_t* __restrict__ run_count,
+                                                          int slots_cap) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t hist[256];
+  __shared__ int wsum[2 * NT / 64 + 2];
+  const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
+  uint32_t* keys = smem;                                                  // [max(slots_cap, k_cap)]
+  int32_t* lidx = reinterpret_cast<int32_t*>(smem + (slots_cap > k_cap ? slots_cap : k_cap));   // [k_cap]
+  int32_t* lpages = lidx + k_cap;                                         // [M] (HI only)
+
+  const int64_t row = blockIdx.x;
+  const RowInfo ri = row_info(g, row);
+  int cnt = 0;
+  if (!ri.valid) {
+    cnt = 0;
+  } else if (ri.p_hi < ri.p_lo) {
+    // sink and window cover [0, t]
+    cnt = (int)(ri.t + 1);
+    for (int i = threadIdx.x; i < cnt; i += NT) lidx[i] = i;
+  } else {
+    const bool flat = g.M <= 0;
+    const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
+    const int n_sel = (int)(flat ? n_elig : (n_elig < g.M ? n_elig : g.M));
+    if (!flat)
+      for (int i = threadIdx.x; i < n_sel; i += NT) lpages[i] = pages[row * g.M + i];
+    const int n = n_sel * g.P;
+    for (int i = threadIdx.x; i < n; i += NT) keys[i] = fine_keys[row * ldf + i];
+    __syncthreads();
+    const int n_valid = block_count_nonzero(keys, n, wsum);
+    uint32_t T = 0;
+    int take = 0;
+    if (n_valid > g.k_sparse) radix_threshold<NT>(keys, n, g.k_sparse, hist, wsum, T, take);
+    const int P = g.P;
+    const int64_t p_lo = ri.p_lo;
+    const int ks = g.k_sink;
+    const int n_sp = select_compact<NT>(keys, n, T, take, wsum, [&](int rank, int i) {
+      const int64_t page = flat ? p_lo + i / P : (int64_t)lpages[i / P];
+      lidx[ks + rank] = (int32_t)(page * P + i % P);
+    });
+    for (int i = threadIdx.x; i < g.k_sink; i += NT) lidx[i] = i;
+    for (int i = threadIdx.x; i < g.k_swa; i += NT) lidx[g.k_sink + n_sp + i] = (int32_t)(ri.t - g.k_swa + 1 + i);
+    cnt = g.k_sink + n_sp + g.k_swa;
+  }
+  __syncthreads();
+  int32_t* orow = idx + row * k_cap;
+  for (int i = threadIdx.x; i < k_cap; i += NT) orow[i] = i < cnt ? lidx[i] : -1;
+  if (threadIdx.x == 0) count[row] = cnt;
+  if (!runs) return;
+
+  // runs: a run starts at i = 0, after a gap, or at a position divisible by C
+  int32_t* rstart = reinterpret_cast<int32_t*>(keys);  // keys are dead now
+  const int C = g.C;
+  int base = 0;
+  for (int c = 0; c < cnt; c += NT) {
+    const int i = c + threadIdx.x;
+    bool st = false;
+    if (i < cnt) {
+      const int32_t s = lidx[i];
+      st = i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0;
+    }
+    const uint64_t bs = __ballot(st);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    if (lane == 0) wsum[wv] = __popcll(bs);
+    __syncthreads();
+    int pre = 0, tot = 0;
+    for (int x = 0; x < NT / 64; ++x) {
+      const int v = wsum[x];
+      pre += x < wv ? v : 0;
+      tot += v;
+    }
+    if (st) rstart[base + pre + __popcll(bs & lanemask_lt())] = i;
+    base += tot;
+    __syncthreads();
+  }
+  const int nr = base;
+  int32_t* rrow = runs + row * (int64_t)k_cap * 2;
+  for (int r = threadIdx.x; r < k_cap; r += NT) {
+    if (r < nr) {
+      const int s = rstart[r];
+      const int e = r + 1 < nr ? rstart[r + 1] : cnt;
+      rrow[2 * r] = lidx[s];
+      rrow[2 * r + 1] = e - s;
+    } else {
+      rrow[2 * r] = -1;
+      rrow[2 * r + 1] = 0;
+    }
+  }
+  if (threadIdx.x == 0) run_count[row] = nr;
+}
+
+// ============================================================================ host launchers
+template <bool FP8>
+static hipError_t launch_bm(int64_t n_sub, int D, int B, const void* k, const float* ks, uint16_t* out, hipStream_t st) {
+  const int64_t threads = n_sub * (D / 4);
+  if (threads == 0) return hipSuccess;
+  const int64_t blocks = (threads + 255) / 256;
+  hipLaunchKernelGGL(block_means_kernel<FP8>, dim3((unsigned)blocks), dim3(256), 0, st, n_sub, D, B, k, ks, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_block_means(int64_t n_sub, int D, int B, bool fp8, const void* k, const float* ks, uint16_t* out,
+                              hipStream_t st) {
+  return fp8 ? launch_bm<true>(n_sub, D, B, k, ks, out, st) : launch_bm<false>(n_sub, D, B, k, ks, out, st);
+}
+
+template <int D, int R, bool PAGED>
+static hipError_t launch_coarse_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
+                                  const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
+                                  hipStream_t st) {
+  const int tiles_per_chunk = PAGED ? 8 : (int)(max_tiles > 0 ? max_tiles : 1);
+  const int64_t chunks = (max_tiles + tiles_per_chunk - 1) / tiles_per_chunk;
+  if (chunks == 0 || n_rows == 0) return hipSuccess;
+  const dim3 grid((unsigned)((n_rows + R - 1) / R), (unsigned)chunks);
+  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED>), grid, dim3(256), 0, st, g, n_rows, q, w, kmean, page_keys, ld,
+                     tiles_per_chunk);
+  return hipGetLastError();
+}
+
+hipError_t launch_coarse(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const uint16_t* kmean,
+                         uint32_t* page_keys, int64_t ld, int64_t max_tiles, hipStream_t st) {
+  const bool paged = g.ctx_len != nullptr;
+  if (g.D == 128)
+    return paged ? launch_coarse_t<128, 1, true>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
+                 : launch_coarse_t<128, 4, false>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
+  return paged ? launch_coarse_t<64, 1, true>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
+               : launch_coarse_t<64, 4, false>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
+}
+
+hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t* page_keys, int64_t ld,
+                              int32_t* pages, int64_t max_elig, hipStream_t st) {
+  if (n_rows == 0) return hipSuccess;
+  const size_t lds = (size_t)(max_elig > 0 ? max_elig : 1) * 4;
+  hipLaunchKernelGGL(page_select_kernel<256>, dim3((unsigned)n_rows), dim3(256), lds, st, g, n_rows, page_keys, ld, pages);
+  return hipGetLastError();
+}
+
+template <int D, bool FP8, bool PAGED>
+static hipError_t launch_fine_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
+                                const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf,
+                                int64_t max_sel, hipStream_t st) {
+  const int ppw = PAGED ? 8 : (int)(max_sel > 0 ? max_sel : 1);
+  const int64_t chunks = (max_sel + ppw - 1) / ppw;
+  if (chunks == 0 || n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL((fine_kernel<D, FP8, PAGED>), dim3((unsigned)n_rows, (unsigned)chunks), dim3(256), 0, st, g, n_rows,
+                     q, w, k, ks, pages, fine_keys, ldf, ppw);
+  return hipGetLastError();
+}
+
+hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
+                       const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
+                       hipStream_t st) {
+  const bool paged = g.ctx_len != nullptr, fp8 = g.fp8 != 0;
+#define LSA_FINE(D_, F_, P_) return launch_fine_t<D_, F_, P_>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
+  if (g.D == 128) {
+    if (fp8) { if (paged) LSA_FINE(128, true, true); else LSA_FINE(128, true, false); }
+    else { if (paged) LSA_FINE(128, false, true); else LSA_FINE(128, false, false); }
+  } else {
+    if (fp8) { if (paged) LSA_FINE(64, true, true); else LSA_FINE(64, true, false); }
+    else { if (paged) LSA_FINE(64, false, true); else LSA_FINE(64, false, false); }
+  }
+#undef LSA_FINE
+}
+
+size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M) {
+  const int64_t a = slots_cap > k_cap ? slots_cap : k_cap;
+  return (size_t)(a + k_cap + (M > 0 ? M : 0)) * 4;
+}
+
+hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_t* fine_keys, int64_t ldf,
+                               const int32_t* pages, int32_t* idx, int32_t* count, int32_t* runs, int32_t* run_count,
+                               int64_t slots_cap, hipStream_t st) {
+  if (n_rows == 0) return hipSuccess;
+  const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
+  const size_t lds = token_select_lds_bytes(slots_cap, k_cap, g.M);
+  hipLaunchKernelGGL(token_select_kernel<512>, dim3((unsigned)n_rows), dim3(512), lds, st, g, n_rows, fine_keys, ldf,
+                     pages, idx, count, runs, run_count, (int)slots_cap);
+  return hipGetLastError();
+}
+
+// Lets the two select kernels use up to 156 KB of dynamic LDS (gfx950 has 160 KB per
+// workgroup); done once per device.
+hipError_t prepare_index_kernels() {
+  static bool done[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && done[dev]) return hipSuccess;
+  const int lim = 160 * 1024 - 4096;
+  e = hipFuncSetAttribute((const void*)token_select_kernel<512>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)page_select_kernel<256>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) done[dev] = true;
+  return hipSuccess;
+}
+
+}  // namespace lsa

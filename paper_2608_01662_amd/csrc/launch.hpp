@@ -1,0 +1,64 @@
+// Internal interface between the C-ABI front end (lsa_api.cpp) and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace lsa {
+
+// Everything the indexer kernels need to know about one call, passed by value.
+struct IndexGeom {
+  int H, D, fp8;                 // indexer heads, head dim, fp8 keys
+  int P, B, M;                   // page, sub-block, kept pages (M <= 0: flat)
+  int k_sparse, k_sink, k_swa, C;
+  int64_t q_start;               // prefill: position of row 0
+  int64_t n_kv;                  // prefill: cached tokens
+  int64_t n_sub;                 // mean keys available
+  const int32_t* ctx_len;        // decode: [rows] (nullptr for prefill)
+  const int32_t* page_table;     // decode: [rows, max_pages]
+  int max_pages, kv_page;
+  int64_t n_phys;
+};
+
+hipError_t launch_block_means(int64_t n_sub, int D, int B, bool fp8, const void* k, const float* ks, uint16_t* out,
+                              hipStream_t st);
+hipError_t launch_coarse(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const uint16_t* kmean,
+                         uint32_t* page_keys, int64_t ld, int64_t max_tiles, hipStream_t st);
+hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t* page_keys, int64_t ld,
+                              int32_t* pages, int64_t max_elig, hipStream_t st);
+hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
+                       const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
+                       hipStream_t st);
+size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M);
+hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_t* fine_keys, int64_t ldf,
+                               const int32_t* pages, int32_t* idx, int32_t* count, int32_t* runs, int32_t* run_count,
+                               int64_t slots_cap, hipStream_t st);
+hipError_t prepare_index_kernels();
+
+// Sparse attention over gathered rows.
+struct AttnGeom {
+  const uint16_t* q;       // [n_rows, H, d_qk]
+  const uint16_t* kv;      // latent [n_kv_rows, d_qk] or K
+  const uint16_t* v;       // V [n_kv_rows, d_v] or nullptr
+  int64_t n_kv_rows;
+  const int32_t* rows;     // [n_rows, k_cap] cache rows to attend (positions, or translated rows)
+  const int32_t* count;    // [n_rows]
+  int k_cap;
+  uint16_t* out;           // [n_rows, H, d_v]
+  float* lse;              // [n_rows, H] or nullptr
+  float* part_o;           // split partials [n_rows, n_split, H, d_v]
+  float* part_ml;          // [n_rows, n_split, H, 2]
+  int64_t n_rows;
+  int n_split, split_len;  // slots per split (multiple of the tile)
+  float scale_log2;        // sm_scale * log2(e)
+};
+
+hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st);
+hipError_t launch_mqa_attn(const AttnGeom& a, hipStream_t st);
+hipError_t launch_attn_combine(const AttnGeom& a, int H, int d_v, hipStream_t st);
+hipError_t launch_translate_rows(const int32_t* idx, const int32_t* count, int64_t n_rows, int k_cap,
+                                 const int32_t* page_table, int max_pages, int kv_page, int rows_per_seq,
+                                 int64_t n_kv_rows, int32_t* out_rows, hipStream_t st);
+hipError_t prepare_attn_kernels();
+
+}  // namespace lsa

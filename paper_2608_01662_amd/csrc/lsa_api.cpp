@@ -1,0 +1,392 @@
+// C-ABI front end of the LSA library: argument checks (host only, before any HIP call),
+// workspace layout, kernel selection and error reporting. See include/lsa.h.
+#include "../../include/lsa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "launch.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+constexpr size_t kMaxLds = 160 * 1024;        // gfx950 LDS per workgroup
+constexpr size_t kSelectStaticLds = 4 * 1024;  // static LDS of the select kernels (upper bound)
+
+lsa_status fail(lsa_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+lsa_status hip_fail(hipError_t e, const char* where) {
+  return fail(LSA_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+#define LSA_REQUIRE(cond, st, ...) \
+  do {                             \
+    if (!(cond)) return fail(st, __VA_ARGS__); \
+  } while (0)
+
+lsa_status check_index_params(const lsa_index_params* p) {
+  LSA_REQUIRE(p != nullptr, LSA_ERR_INVALID_ARG, "params is NULL");
+  LSA_REQUIRE(p->n_heads >= 1 && p->n_heads <= 32, LSA_ERR_UNSUPPORTED, "n_heads=%d not in [1, 32]", p->n_heads);
+  LSA_REQUIRE(p->head_dim == 64 || p->head_dim == 128, LSA_ERR_UNSUPPORTED, "head_dim=%d not 64 or 128", p->head_dim);
+  LSA_REQUIRE(p->key_dtype == LSA_KEY_BF16 || p->key_dtype == LSA_KEY_FP8_E4M3FN, LSA_ERR_INVALID_ARG,
+              "key_dtype=%d unknown", p->key_dtype);
+  LSA_REQUIRE(p->page >= 32 && p->page <= 256 && p->page % 32 == 0, LSA_ERR_UNSUPPORTED,
+              "page=%d must be a multiple of 32 in [32, 256]", p->page);
+  LSA_REQUIRE(p->sub_block >= 1 && pow2(p->sub_block) && p->page % p->sub_block == 0 && p->page / p->sub_block <= 32,
+              LSA_ERR_UNSUPPORTED, "sub_block=%d must be a power of two dividing page=%d with page/sub_block <= 32",
+              p->sub_block, p->page);
+  LSA_REQUIRE(p->k_sparse >= 1, LSA_ERR_INVALID_ARG, "k_sparse=%d must be >= 1", p->k_sparse);
+  LSA_REQUIRE(p->k_sink >= 0 && p->k_swa >= 0, LSA_ERR_INVALID_ARG, "k_sink=%d / k_swa=%d must be >= 0", p->k_sink,
+              p->k_swa);
+  LSA_REQUIRE(p->run_align >= 1, LSA_ERR_INVALID_ARG, "run_align=%d must be >= 1", p->run_align);
+  LSA_REQUIRE((int64_t)p->k_sink + p->k_swa + p->k_sparse < (1LL << 30), LSA_ERR_INVALID_ARG, "k_cap too large");
+  if (p->keep_pages > 0)
+    LSA_REQUIRE(p->k_swa >= p->page, LSA_ERR_UNSUPPORTED,
+                "hierarchical mode needs k_swa=%d >= page=%d (scored pages must not reach past the query)", p->k_swa,
+                p->page);
+  return LSA_OK;
+}
+
+// Rows of fine-score slots and page-score entries for a given key range.
+struct IndexPlan {
+  int64_t n_pages;     // pages in [0, max_kv)
+  int64_t slots;       // fine-score slots per row
+  size_t off_page_keys, off_pages, off_fine, total;
+};
+
+IndexPlan plan_index(const lsa_index_params* p, int64_t n_rows, int64_t max_kv) {
+  IndexPlan pl{};
+  pl.n_pages = cdiv(max_kv, p->page);
+  const bool hi = p->keep_pages > 0;
+  pl.slots = (hi ? (int64_t)p->keep_pages : pl.n_pages) * p->page;
+  size_t off = 0;
+  pl.off_page_keys = off;
+  if (hi) off += round_up((size_t)n_rows * pl.n_pages * 4, 256);
+  pl.off_pages = off;
+  if (hi) off += round_up((size_t)n_rows * p->keep_pages * 4, 256);
+  pl.off_fine = off;
+  off += round_up((size_t)n_rows * pl.slots * 4, 256);
+  pl.total = off;
+  return pl;
+}
+
+lsa_status check_lds(const lsa_index_params* p, const IndexPlan& pl) {
+  const int k_cap = p->k_sink + p->k_swa + p->k_sparse;
+  const size_t ts = lsa::token_select_lds_bytes(pl.slots, k_cap, p->keep_pages);
+  LSA_REQUIRE(ts + kSelectStaticLds <= kMaxLds, LSA_ERR_UNSUPPORTED,
+              "candidate slots (%lld) plus k_cap (%d) exceed the LDS of one workgroup; lower keep_pages*page",
+              (long long)pl.slots, k_cap);
+  if (p->keep_pages > 0)
+    LSA_REQUIRE((size_t)pl.n_pages * 4 + kSelectStaticLds <= kMaxLds, LSA_ERR_UNSUPPORTED,
+                "%lld pages per row exceed the LDS of the page selection", (long long)pl.n_pages);
+  return LSA_OK;
+}
+
+lsa::IndexGeom make_geom(const lsa_index_params* p) {
+  lsa::IndexGeom g{};
+  g.H = p->n_heads;
+  g.D = p->head_dim;
+  g.fp8 = p->key_dtype == LSA_KEY_FP8_E4M3FN;
+  g.P = p->page;
+  g.B = p->sub_block;
+  g.M = p->keep_pages > 0 ? p->keep_pages : 0;
+  g.k_sparse = p->k_sparse;
+  g.k_sink = p->k_sink;
+  g.k_swa = p->k_swa;
+  g.C = p->run_align;
+  return g;
+}
+
+lsa_status run_index(const lsa_index_params* p, const lsa::IndexGeom& g, int64_t n_rows, int64_t max_kv,
+                     const void* q, const float* w, const void* k, const float* k_scale, const void* block_keys,
+                     int32_t* idx, int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out,
+                     void* workspace, hipStream_t st) {
+  const IndexPlan pl = plan_index(p, n_rows, max_kv);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint32_t* page_keys = reinterpret_cast<uint32_t*>(ws + pl.off_page_keys);
+  int32_t* pages = pages_out ? pages_out : reinterpret_cast<int32_t*>(ws + pl.off_pages);
+  uint32_t* fine = reinterpret_cast<uint32_t*>(ws + pl.off_fine);
+  const auto* q16 = static_cast<const uint16_t*>(q);
+  hipError_t e = lsa::prepare_index_kernels();
+  if (e != hipSuccess) return hip_fail(e, "prepare");
+  // eligible pages of the last row bound every row's work
+  const int64_t max_elig = pl.n_pages;
+  if (g.M > 0) {
+    const int64_t max_tiles = cdiv(max_elig * (g.P / g.B), 32);
+    e = lsa::launch_coarse(g, n_rows, q16, w, static_cast<const uint16_t*>(block_keys), page_keys, pl.n_pages,
+                           max_tiles, st);
+    if (e != hipSuccess) return hip_fail(e, "coarse page scoring");
+    e = lsa::launch_page_select(g, n_rows, page_keys, pl.n_pages, pages, max_elig, st);
+    if (e != hipSuccess) return hip_fail(e, "page selection");
+  }
+  const int64_t max_sel = g.M > 0 ? (max_elig < g.M ? max_elig : g.M) : max_elig;
+  e = lsa::launch_fine(g, n_rows, q16, w, k, k_scale, pages, fine, pl.slots, max_sel, st);
+  if (e != hipSuccess) return hip_fail(e, "fine token scoring");
+  e = lsa::launch_token_select(g, n_rows, fine, pl.slots, g.M > 0 ? pages : nullptr, idx, count,
+                               reinterpret_cast<int32_t*>(runs), run_count, pl.slots, st);
+  if (e != hipSuccess) return hip_fail(e, "token selection");
+  return LSA_OK;
+}
+
+// ---------------------------------------------------------------- attention planning
+struct AttnPlan {
+  int n_split, split_len;
+  size_t off_rows, off_po, off_ml, total;
+};
+
+AttnPlan plan_attn(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int32_t paged) {
+  AttnPlan pl{};
+  pl.n_split = 1;
+  pl.split_len = k_cap;
+  const bool mla = p->latent != 0;
+  if (mla && n_rows > 0 && n_rows < 2048) {
+    // too few rows to fill 256 CUs: split every row's list into 32-token-aligned pieces
+    int64_t want = cdiv(2048, n_rows);
+    int64_t max_split = cdiv(k_cap, 32);
+    int64_t ns = want < max_split ? want : max_split;
+    if (ns > 1) {
+      int64_t len = round_up((size_t)cdiv(k_cap, ns), 32);
+      pl.split_len = (int)len;
+      pl.n_split = (int)cdiv(k_cap, len);
+    }
+  }
+  size_t off = 0;
+  pl.off_rows = off;
+  if (paged) off += round_up((size_t)n_rows * k_cap * 4, 256);
+  pl.off_po = off;
+  if (pl.n_split > 1) off += round_up((size_t)n_rows * pl.n_split * p->n_heads * p->d_v * 4, 256);
+  pl.off_ml = off;
+  if (pl.n_split > 1) off += round_up((size_t)n_rows * pl.n_split * p->n_heads * 2 * 4, 256);
+  pl.total = off;
+  return pl;
+}
+
+lsa_status check_attn_params(const lsa_attn_params* p) {
+  LSA_REQUIRE(p != nullptr, LSA_ERR_INVALID_ARG, "params is NULL");
+  const bool mla = p->n_heads == 64 && p->d_qk == 576 && p->d_v == 512 && p->latent == 1;
+  const bool mqa = p->n_heads == 16 && p->d_qk == 128 && p->d_v == 128 && p->latent == 0;
+  LSA_REQUIRE(mla || mqa, LSA_ERR_UNSUPPORTED,
+              "attention shape (n_heads=%d, d_qk=%d, d_v=%d, latent=%d) not supported; use (64,576,512,1) or "
+              "(16,128,128,0)",
+              p->n_heads, p->d_qk, p->d_v, p->latent);
+  LSA_REQUIRE(p->sm_scale > 0.f && p->sm_scale < 1e30f, LSA_ERR_INVALID_ARG, "sm_scale must be positive and finite");
+  return LSA_OK;
+}
+
+}  // namespace
+
+namespace lsa {
+hipError_t prepare_index_kernels();
+}
+
+extern "C" {
+
+int32_t lsa_index_k_cap(const lsa_index_params* p) {
+  if (!p) return 0;
+  return p->k_sink + p->k_swa + p->k_sparse;
+}
+
+size_t lsa_index_workspace_size(const lsa_index_params* p, int64_t n_rows, int64_t max_kv) {
+  if (check_index_params(p) != LSA_OK || n_rows < 0 || max_kv < 0) return 0;
+  return plan_index(p, n_rows, max_kv).total;
+}
+
+lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void* k, const float* k_scale,
+                           void* block_keys, void* stream) {
+  g_err[0] = 0;
+  lsa_status s = check_index_params(p);
+  if (s != LSA_OK) return s;
+  const bool fp8 = p->key_dtype == LSA_KEY_FP8_E4M3FN;
+  LSA_REQUIRE(n_tok >= 0, LSA_ERR_INVALID_ARG, "n_tok=%lld < 0", (long long)n_tok);
+  LSA_REQUIRE(k && block_keys, LSA_ERR_INVALID_ARG, "k / block_keys is NULL");
+  LSA_REQUIRE(fp8 == (k_scale != nullptr), LSA_ERR_INVALID_ARG, "k_scale must be given exactly for fp8 keys");
+  LSA_REQUIRE(aligned(k, 16) && aligned(block_keys, 16) && aligned(k_scale, 4), LSA_ERR_INVALID_ARG,
+              "k/block_keys must be 16-byte aligned, k_scale 4-byte aligned");
+  const int64_t n_sub = n_tok / p->sub_block;
+  hipError_t e = lsa::launch_block_means(n_sub, p->head_dim, p->sub_block, fp8, k, k_scale,
+                                         static_cast<uint16_t*>(block_keys), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "block means");
+  return LSA_OK;
+}
+
+static lsa_status check_index_io(const lsa_index_params* p, const void* q, const float* w, const void* k,
+                                 const float* k_scale, const void* block_keys, int32_t* idx, int32_t* count,
+                                 lsa_run* runs, int32_t* run_count, void* workspace, size_t ws_bytes, size_t need) {
+  const bool fp8 = p->key_dtype == LSA_KEY_FP8_E4M3FN;
+  LSA_REQUIRE(q && w && k && idx && count, LSA_ERR_INVALID_ARG, "q, w, k, idx and count must be non-NULL");
+  LSA_REQUIRE(fp8 == (k_scale != nullptr), LSA_ERR_INVALID_ARG, "k_scale must be given exactly for fp8 keys");
+  LSA_REQUIRE(p->keep_pages <= 0 || block_keys != nullptr, LSA_ERR_INVALID_ARG,
+              "block_keys is NULL but keep_pages > 0 (hierarchical mode)");
+  LSA_REQUIRE((runs == nullptr) == (run_count == nullptr), LSA_ERR_INVALID_ARG,
+              "runs and run_count must be both NULL or both non-NULL");
+  LSA_REQUIRE(aligned(q, 16) && aligned(k, 16) && aligned(block_keys, 16), LSA_ERR_INVALID_ARG,
+              "q, k and block_keys must be 16-byte aligned");
+  LSA_REQUIRE(aligned(w, 4) && aligned(k_scale, 4) && aligned(idx, 4) && aligned(count, 4) && aligned(runs, 4) &&
+                  aligned(run_count, 4),
+              LSA_ERR_INVALID_ARG, "w, k_scale, idx, count, runs, run_count must be 4-byte aligned");
+  LSA_REQUIRE(need == 0 || (workspace != nullptr && aligned(workspace, 256)), LSA_ERR_WORKSPACE,
+              "workspace must be non-NULL and 256-byte aligned");
+  LSA_REQUIRE(ws_bytes >= need, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, need);
+  return LSA_OK;
+}
+
+lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t n_q, int64_t n_kv, const void* q,
+                             const float* w, const void* k, const float* k_scale, const void* block_keys, int32_t* idx,
+                             int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out, void* workspace,
+                             size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  lsa_status s = check_index_params(p);
+  if (s != LSA_OK) return s;
+  LSA_REQUIRE(q_start >= 0 && n_q >= 0 && n_kv >= 0, LSA_ERR_INVALID_ARG, "negative q_start / n_q / n_kv");
+  LSA_REQUIRE(q_start + n_q <= n_kv, LSA_ERR_INVALID_ARG, "q_start + n_q = %lld exceeds n_kv = %lld",
+              (long long)(q_start + n_q), (long long)n_kv);
+  LSA_REQUIRE(n_kv < (1LL << 31), LSA_ERR_UNSUPPORTED, "n_kv must be < 2^31 (int32 positions)");
+  LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
+  LSA_REQUIRE(aligned(pages_out, 4), LSA_ERR_INVALID_ARG, "pages_out must be 4-byte aligned");
+  const IndexPlan pl = plan_index(p, n_q, n_kv);
+  s = check_lds(p, pl);
+  if (s != LSA_OK) return s;
+  s = check_index_io(p, q, w, k, k_scale, block_keys, idx, count, runs, run_count, workspace, ws_bytes, pl.total);
+  if (s != LSA_OK) return s;
+  if (n_q == 0) return LSA_OK;
+  lsa::IndexGeom g = make_geom(p);
+  g.q_start = q_start;
+  g.n_kv = n_kv;
+  g.n_sub = n_kv / p->sub_block;
+  return run_index(p, g, n_q, n_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count, pages_out, workspace,
+                   static_cast<hipStream_t>(stream));
+}
+
+lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
+                            const int32_t* page_table, int32_t max_pages, int32_t kv_page_size, int64_t n_phys,
+                            const void* q, const float* w, const void* k, const float* k_scale, const void* block_keys,
+                            int32_t* idx, int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out,
+                            void* workspace, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  lsa_status s = check_index_params(p);
+  if (s != LSA_OK) return s;
+  LSA_REQUIRE(batch >= 0, LSA_ERR_INVALID_ARG, "batch=%d < 0", batch);
+  LSA_REQUIRE(max_pages >= 1 && kv_page_size >= 1 && n_phys >= 1, LSA_ERR_INVALID_ARG,
+              "max_pages, kv_page_size and n_phys must be >= 1");
+  LSA_REQUIRE(kv_page_size == p->page, LSA_ERR_UNSUPPORTED,
+              "paged indexing needs page (%d) == kv_page_size (%d)", p->page, kv_page_size);
+  LSA_REQUIRE((int64_t)max_pages * kv_page_size < (1LL << 31) && n_phys * kv_page_size < (1LL << 31),
+              LSA_ERR_UNSUPPORTED, "positions and cache rows must fit in int32");
+  LSA_REQUIRE(ctx_len && page_table, LSA_ERR_INVALID_ARG, "ctx_len / page_table is NULL");
+  LSA_REQUIRE(aligned(ctx_len, 4) && aligned(page_table, 4) && aligned(pages_out, 4), LSA_ERR_INVALID_ARG,
+              "ctx_len, page_table, pages_out must be 4-byte aligned");
+  LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
+  const int64_t max_kv = (int64_t)max_pages * kv_page_size;
+  const IndexPlan pl = plan_index(p, batch, max_kv);
+  s = check_lds(p, pl);
+  if (s != LSA_OK) return s;
+  s = check_index_io(p, q, w, k, k_scale, block_keys, idx, count, runs, run_count, workspace, ws_bytes, pl.total);
+  if (s != LSA_OK) return s;
+  if (batch == 0) return LSA_OK;
+  lsa::IndexGeom g = make_geom(p);
+  g.ctx_len = ctx_len;
+  g.page_table = page_table;
+  g.max_pages = max_pages;
+  g.kv_page = kv_page_size;
+  g.n_phys = n_phys;
+  g.n_kv = n_phys * kv_page_size;
+  g.n_sub = g.n_kv / p->sub_block;
+  return run_index(p, g, batch, max_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count, pages_out,
+                   workspace, static_cast<hipStream_t>(stream));
+}
+
+size_t lsa_sparse_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int32_t paged) {
+  if (check_attn_params(p) != LSA_OK || n_rows < 0 || k_cap < 1) return 0;
+  return plan_attn(p, n_rows, k_cap, paged).total;
+}
+
+lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv, const void* v,
+                           int64_t n_kv_rows, const int32_t* idx, const int32_t* count, int32_t k_cap,
+                           const int32_t* page_table, int32_t max_pages, int32_t kv_page_size, int32_t rows_per_seq,
+                           void* out, float* lse, void* workspace, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  lsa_status s = check_attn_params(p);
+  if (s != LSA_OK) return s;
+  const bool mla = p->latent != 0;
+  LSA_REQUIRE(n_rows >= 0 && k_cap >= 1, LSA_ERR_INVALID_ARG, "n_rows < 0 or k_cap < 1");
+  LSA_REQUIRE(n_rows < (1LL << 31), LSA_ERR_UNSUPPORTED, "n_rows must be < 2^31");
+  LSA_REQUIRE(n_kv_rows >= 1 && n_kv_rows < (1LL << 31), LSA_ERR_INVALID_ARG, "n_kv_rows=%lld not in [1, 2^31)",
+              (long long)n_kv_rows);
+  LSA_REQUIRE(q && kv && idx && count && out, LSA_ERR_INVALID_ARG, "q, kv, idx, count and out must be non-NULL");
+  LSA_REQUIRE(mla == (v == nullptr), LSA_ERR_INVALID_ARG, mla ? "v must be NULL for a latent cache" : "v is NULL");
+  LSA_REQUIRE(aligned(q, 16) && aligned(kv, 16) && aligned(v, 16) && aligned(out, 16), LSA_ERR_INVALID_ARG,
+              "q, kv, v and out must be 16-byte aligned");
+  LSA_REQUIRE(aligned(idx, 4) && aligned(count, 4) && aligned(lse, 4) && aligned(page_table, 4), LSA_ERR_INVALID_ARG,
+              "idx, count, lse and page_table must be 4-byte aligned");
+  const bool paged = page_table != nullptr;
+  if (paged)
+    LSA_REQUIRE(max_pages >= 1 && kv_page_size >= 1 && rows_per_seq >= 1, LSA_ERR_INVALID_ARG,
+                "paged cache needs max_pages, kv_page_size and rows_per_seq >= 1");
+  const AttnPlan pl = plan_attn(p, n_rows, k_cap, paged);
+  LSA_REQUIRE(pl.total == 0 || (workspace != nullptr && aligned(workspace, 256)), LSA_ERR_WORKSPACE,
+              "workspace must be non-NULL and 256-byte aligned");
+  LSA_REQUIRE(ws_bytes >= pl.total, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, pl.total);
+  if (n_rows == 0) return LSA_OK;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  lsa::AttnGeom a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.kv = static_cast<const uint16_t*>(kv);
+  a.v = static_cast<const uint16_t*>(v);
+  a.n_kv_rows = n_kv_rows;
+  a.rows = idx;
+  a.count = count;
+  a.k_cap = k_cap;
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.n_rows = n_rows;
+  a.n_split = pl.n_split;
+  a.split_len = pl.split_len;
+  a.scale_log2 = p->sm_scale * 1.4426950408889634f;
+  if (paged) {
+    int32_t* rows = reinterpret_cast<int32_t*>(ws + pl.off_rows);
+    hipError_t e = lsa::launch_translate_rows(idx, count, n_rows, k_cap, page_table, max_pages, kv_page_size,
+                                              rows_per_seq, n_kv_rows, rows, st);
+    if (e != hipSuccess) return hip_fail(e, "page-table translation");
+    a.rows = rows;
+  }
+  if (pl.n_split > 1) {
+    a.part_o = reinterpret_cast<float*>(ws + pl.off_po);
+    a.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
+  }
+  hipError_t e = mla ? lsa::launch_mla_attn(a, st) : lsa::launch_mqa_attn(a, st);
+  if (e != hipSuccess) return hip_fail(e, "sparse attention");
+  return LSA_OK;
+}
+
+const char* lsa_status_string(int32_t status) {
+  switch (status) {
+    case LSA_OK: return "LSA_OK";
+    case LSA_ERR_INVALID_ARG: return "LSA_ERR_INVALID_ARG";
+    case LSA_ERR_UNSUPPORTED: return "LSA_ERR_UNSUPPORTED";
+    case LSA_ERR_WORKSPACE: return "LSA_ERR_WORKSPACE";
+    case LSA_ERR_HIP: return "LSA_ERR_HIP";
+    default: return "LSA_ERR_UNKNOWN";
+  }
+}
+
+const char* lsa_last_error(void) { return g_err; }
+
+const char* lsa_version(void) { return "lsa-mi355x 0.1"; }
+
+}  // extern "C"

@@ -1,0 +1,240 @@
+"""Thin Python binding of liblsa.so (the C-ABI in include/lsa.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP library. PyTorch provides
+device memory and the current stream. Importing this module does not load the library; the
+first call does, and raises if liblsa.so has not been built (there is no fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblsa.so")
+
+LSA_KEY_BF16 = 0
+LSA_KEY_FP8_E4M3FN = 1
+
+
+class LSAError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        super().__init__(f"{where}: {message} (status {status})")
+        self.status = status
+
+
+class _IndexParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_heads", "head_dim", "key_dtype", "page", "sub_block", "keep_pages",
+        "k_sparse", "k_sink", "k_swa", "run_align")]
+
+
+class _AttnParams(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int32), ("d_qk", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("latent", ctypes.c_int32), ("sm_scale", ctypes.c_float)]
+
+
+@dataclass(frozen=True)
+class IndexParams:
+    """Indexer hyper-parameters (Sec. 3.1 and 3.3 of the paper); see lsa_index_params."""
+    n_heads: int
+    head_dim: int
+    fp8: bool
+    page: int
+    sub_block: int
+    keep_pages: int
+    k_sparse: int
+    k_sink: int
+    k_swa: int
+    run_align: int
+
+    @property
+    def k_cap(self) -> int:
+        return self.k_sink + self.k_swa + self.k_sparse
+
+    def c(self) -> _IndexParams:
+        return _IndexParams(self.n_heads, self.head_dim, LSA_KEY_FP8_E4M3FN if self.fp8 else LSA_KEY_BF16,
+                            self.page, self.sub_block, self.keep_pages, self.k_sparse, self.k_sink,
+                            self.k_swa, self.run_align)
+
+
+@dataclass(frozen=True)
+class AttnParams:
+    n_heads: int
+    d_qk: int
+    d_v: int
+    latent: bool
+    sm_scale: float
+
+    def c(self) -> _AttnParams:
+        return _AttnParams(self.n_heads, self.d_qk, self.d_v, int(self.latent), self.sm_scale)
+
+
+MLA = dict(n_heads=64, d_qk=576, d_v=512, latent=True)
+MQA = dict(n_heads=16, d_qk=128, d_v=128, latent=False)
+
+_lib = None
+_vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """Load liblsa.so (once). Raises when it is missing: the product path has no fallback."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2608_01662_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER(_IndexParams)
+        A = ctypes.POINTER(_AttnParams)
+        L.lsa_index_k_cap.argtypes = [P]
+        L.lsa_index_k_cap.restype = _i32
+        L.lsa_index_workspace_size.argtypes = [P, _i64, _i64]
+        L.lsa_index_workspace_size.restype = _sz
+        L.lsa_block_means.argtypes = [P, _i64, _vp, _vp, _vp, _vp]
+        L.lsa_block_means.restype = _i32
+        L.lsa_index_prefill.argtypes = [P, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                        _vp, _sz, _vp]
+        L.lsa_index_prefill.restype = _i32
+        L.lsa_index_decode.argtypes = [P, _i32, _vp, _vp, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _vp, _vp, _vp, _vp, _sz, _vp]
+        L.lsa_index_decode.restype = _i32
+        L.lsa_sparse_attn_workspace_size.argtypes = [A, _i64, _i32, _i32]
+        L.lsa_sparse_attn_workspace_size.restype = _sz
+        L.lsa_sparse_attn.argtypes = [A, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _i32, _i32, _i32, _vp,
+                                      _vp, _vp, _sz, _vp]
+        L.lsa_sparse_attn.restype = _i32
+        L.lsa_status_string.argtypes = [_i32]
+        L.lsa_status_string.restype = ctypes.c_char_p
+        L.lsa_last_error.argtypes = []
+        L.lsa_last_error.restype = ctypes.c_char_p
+        L.lsa_version.argtypes = []
+        L.lsa_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        L = lib()
+        raise LSAError(status, where, (L.lsa_last_error() or b"").decode() or
+                       L.lsa_status_string(status).decode())
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _keys_u8_or_bf16(k: torch.Tensor) -> torch.Tensor:
+    if k.dtype == torch.float8_e4m3fn:
+        return k.view(torch.uint8)
+    return k
+
+
+def _workspace(nbytes: int, device, ws):
+    if nbytes == 0:
+        return None, 0
+    if ws is not None:
+        return ws, ws.numel() * ws.element_size()
+    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+
+
+def index_workspace_size(prm: IndexParams, n_rows: int, max_kv: int) -> int:
+    return int(lib().lsa_index_workspace_size(ctypes.byref(prm.c()), n_rows, max_kv))
+
+
+def attn_workspace_size(prm: AttnParams, n_rows: int, k_cap: int, paged: bool) -> int:
+    return int(lib().lsa_sparse_attn_workspace_size(ctypes.byref(prm.c()), n_rows, k_cap, int(paged)))
+
+
+def block_means(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None = None,
+                out: torch.Tensor | None = None) -> torch.Tensor:
+    """Mean-key cache of the coarse stage: [n_tok // sub_block, head_dim] bf16."""
+    k = _keys_u8_or_bf16(k)
+    n_tok = k.shape[0]
+    if out is None:
+        out = torch.empty((n_tok // prm.sub_block, prm.head_dim), dtype=torch.bfloat16, device=k.device)
+    _check(lib().lsa_block_means(ctypes.byref(prm.c()), n_tok, _p(k), _p(k_scale), _p(out), _stream(k.device)),
+           "lsa_block_means")
+    return out
+
+
+def _index_outputs(prm: IndexParams, n_rows: int, device, runs: bool, pages: bool, out: dict | None):
+    out = dict(out or {})
+    kc = prm.k_cap
+    out.setdefault("idx", torch.empty((n_rows, kc), dtype=torch.int32, device=device))
+    out.setdefault("count", torch.empty((n_rows,), dtype=torch.int32, device=device))
+    if runs:
+        out.setdefault("runs", torch.empty((n_rows, kc, 2), dtype=torch.int32, device=device))
+        out.setdefault("run_count", torch.empty((n_rows,), dtype=torch.int32, device=device))
+    if pages and prm.keep_pages > 0:
+        out.setdefault("pages", torch.empty((n_rows, prm.keep_pages), dtype=torch.int32, device=device))
+    return out
+
+
+def index_prefill(prm: IndexParams, q: torch.Tensor, w: torch.Tensor, k: torch.Tensor,
+                  k_scale: torch.Tensor | None, block_keys: torch.Tensor | None, q_start: int,
+                  n_kv: int | None = None, runs: bool = True, pages: bool = False,
+                  workspace: torch.Tensor | None = None, out: dict | None = None) -> dict:
+    """LSA indexer for query rows at positions q_start .. q_start + n_q - 1 (lsa_index_prefill)."""
+    k = _keys_u8_or_bf16(k)
+    n_q = q.shape[0]
+    n_kv = k.shape[0] if n_kv is None else n_kv
+    o = _index_outputs(prm, n_q, q.device, runs, pages, out)
+    ws, wsb = _workspace(index_workspace_size(prm, n_q, n_kv), q.device, workspace)
+    _check(lib().lsa_index_prefill(ctypes.byref(prm.c()), q_start, n_q, n_kv, _p(q), _p(w), _p(k), _p(k_scale),
+                                   _p(block_keys), _p(o["idx"]), _p(o["count"]), _p(o.get("runs")),
+                                   _p(o.get("run_count")), _p(o.get("pages")), _p(ws), wsb, _stream(q.device)),
+           "lsa_index_prefill")
+    return o
+
+
+def index_decode(prm: IndexParams, ctx_len: torch.Tensor, page_table: torch.Tensor, kv_page_size: int,
+                 n_phys: int, q: torch.Tensor, w: torch.Tensor, k: torch.Tensor, k_scale: torch.Tensor | None,
+                 block_keys: torch.Tensor | None, runs: bool = True, pages: bool = False,
+                 workspace: torch.Tensor | None = None, out: dict | None = None) -> dict:
+    """LSA indexer for one new token per sequence over a paged key cache (lsa_index_decode)."""
+    k = _keys_u8_or_bf16(k)
+    batch, max_pages = page_table.shape
+    o = _index_outputs(prm, batch, q.device, runs, pages, out)
+    ws, wsb = _workspace(index_workspace_size(prm, batch, max_pages * kv_page_size), q.device, workspace)
+    _check(lib().lsa_index_decode(ctypes.byref(prm.c()), batch, _p(ctx_len), _p(page_table), max_pages,
+                                  kv_page_size, n_phys, _p(q), _p(w), _p(k), _p(k_scale), _p(block_keys),
+                                  _p(o["idx"]), _p(o["count"]), _p(o.get("runs")), _p(o.get("run_count")),
+                                  _p(o.get("pages")), _p(ws), wsb, _stream(q.device)),
+           "lsa_index_decode")
+    return o
+
+
+def sparse_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, v: torch.Tensor | None,
+                idx: torch.Tensor, count: torch.Tensor, page_table: torch.Tensor | None = None,
+                kv_page_size: int = 0, rows_per_seq: int = 1, out: torch.Tensor | None = None,
+                lse: torch.Tensor | bool | None = True, workspace: torch.Tensor | None = None):
+    """Sparse attention over idx (lsa_sparse_attn). Returns (out [n_rows, H, d_v] bf16, lse or None).
+
+    kv: contiguous [n_kv_rows, d_qk] or paged [n_phys, page, d_qk] (then page_table is required)."""
+    n_rows = q.shape[0]
+    k_cap = idx.shape[1]
+    n_kv_rows = kv.shape[0] * (kv.shape[1] if page_table is not None else 1)
+    if out is None:
+        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=q.device)
+    if lse is True:
+        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=q.device)
+    elif lse is False:
+        lse = None
+    max_pages = page_table.shape[1] if page_table is not None else 0
+    ws, wsb = _workspace(attn_workspace_size(prm, n_rows, k_cap, page_table is not None), q.device, workspace)
+    _check(lib().lsa_sparse_attn(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), _p(v), n_kv_rows, _p(idx),
+                                 _p(count), k_cap, _p(page_table), max_pages, kv_page_size, rows_per_seq,
+                                 _p(out), _p(lse), _p(ws), wsb, _stream(q.device)),
+           "lsa_sparse_attn")
+    return out, lse
+
+
+def version() -> str:
+    return lib().lsa_version().decode()

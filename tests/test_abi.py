@@ -1,0 +1,140 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared entry point, and
+rejects bad arguments on the host before any HIP call (only pointers that fail validation are
+ever passed, so nothing reaches a device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_01662_amd import lsa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lsa.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(lsa.LIB_PATH), reason="liblsa.so not built")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(0x100000)       # aligned, never dereferenced: every call below fails validation
+MISALIGNED = ctypes.c_void_p(0x100001)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]*?\b(lsa_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol():
+    L = lsa.lib()
+    names = declared_functions()
+    assert len(names) >= 10, names
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in lsa.h but not exported"
+
+
+def test_version_and_status_strings():
+    L = lsa.lib()
+    assert lsa.version().startswith("lsa-mi355x")
+    for code, name in [(0, b"LSA_OK"), (1, b"LSA_ERR_INVALID_ARG"), (2, b"LSA_ERR_UNSUPPORTED"),
+                       (3, b"LSA_ERR_WORKSPACE"), (4, b"LSA_ERR_HIP"), (99, b"LSA_ERR_UNKNOWN")]:
+        assert L.lsa_status_string(code) == name
+
+
+def P(**kw):
+    base = dict(n_heads=32, head_dim=128, fp8=True, page=128, sub_block=128, keep_pages=64,
+                k_sparse=2048, k_sink=4, k_swa=1024, run_align=128)
+    base.update(kw)
+    return lsa.IndexParams(**base)
+
+
+def prefill(prm, q_start=0, n_q=16, n_kv=4096, q=FAKE, w=FAKE, k=FAKE, ks=FAKE, bk=FAKE, idx=FAKE, cnt=FAKE,
+            runs=None, rc=None, pages=None, ws=FAKE, wsb=1 << 40):
+    L = lsa.lib()
+    return L.lsa_index_prefill(ctypes.byref(prm.c()), q_start, n_q, n_kv, q, w, k, ks, bk, idx, cnt, runs, rc,
+                               pages, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_heads=0), UNSUPPORTED), (dict(n_heads=33), UNSUPPORTED), (dict(head_dim=96), UNSUPPORTED),
+    (dict(page=48), UNSUPPORTED), (dict(page=512, sub_block=512, k_swa=1024), UNSUPPORTED),
+    (dict(sub_block=3), UNSUPPORTED), (dict(page=128, sub_block=2), UNSUPPORTED),
+    (dict(k_sparse=0), INVALID), (dict(k_sink=-1), INVALID), (dict(run_align=0), INVALID),
+    (dict(keep_pages=8, k_swa=64), UNSUPPORTED),
+])
+def test_bad_index_params(kw, status):
+    assert prefill(P(**kw)) == status
+    assert lsa.lib().lsa_index_workspace_size(ctypes.byref(P(**kw).c()), 16, 4096) == 0
+
+
+def test_bad_index_arguments():
+    prm = P()
+    assert prefill(prm, q_start=4090, n_q=16, n_kv=4096) == INVALID           # rows past the cache
+    assert prefill(prm, n_q=-1) == INVALID
+    assert prefill(prm, q=None) == INVALID
+    assert prefill(prm, ks=None) == INVALID                                   # fp8 needs scales
+    assert prefill(P(fp8=False)) == INVALID                                   # bf16 must not get scales
+    assert prefill(prm, bk=None) == INVALID                                   # HI needs mean keys
+    assert prefill(prm, runs=FAKE, rc=None) == INVALID
+    assert prefill(prm, q=MISALIGNED) == INVALID
+    assert prefill(prm, ws=None) == WORKSPACE
+    assert prefill(prm, wsb=16) == WORKSPACE
+    assert prefill(prm, ws=ctypes.c_void_p(0x100080)) == WORKSPACE             # not 256-byte aligned
+    assert prefill(P(keep_pages=0), pages=FAKE) == INVALID                    # pages need HI mode
+    # candidate slots beyond one workgroup's LDS
+    assert prefill(P(keep_pages=1024, page=128)) == UNSUPPORTED
+    assert b"LDS" in lsa.lib().lsa_last_error()
+    assert prefill(P(keep_pages=0), n_kv=1 << 20, n_q=16) == UNSUPPORTED       # flat over 1M candidates
+
+
+def test_bad_decode_arguments():
+    L = lsa.lib()
+    prm = P(page=64, sub_block=64, keep_pages=128, k_swa=256)
+
+    def dec(batch=4, ctx=FAKE, table=FAKE, max_pages=2048, kv_page=64, n_phys=1000, **kw):
+        return L.lsa_index_decode(ctypes.byref(prm.c()), batch, ctx, table, max_pages, kv_page, n_phys, FAKE,
+                                  FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, kw.get("ws", FAKE),
+                                  kw.get("wsb", 1 << 40), None)
+    assert dec(kv_page=32) == UNSUPPORTED
+    assert dec(ctx=None) == INVALID
+    assert dec(max_pages=0) == INVALID
+    assert dec(batch=-1) == INVALID
+    assert dec(wsb=0) == WORKSPACE
+
+
+def test_bad_attention_arguments():
+    L = lsa.lib()
+    mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+
+    def attn(prm=mla, n_rows=8, q=FAKE, kv=FAKE, v=None, n_kv=100, idx=FAKE, cnt=FAKE, k_cap=64, table=None,
+             max_pages=0, kv_page=0, rps=1, out=FAKE, lse=None, ws=FAKE, wsb=1 << 40):
+        return L.lsa_sparse_attn(ctypes.byref(prm.c()), n_rows, q, kv, v, n_kv, idx, cnt, k_cap, table, max_pages,
+                                 kv_page, rps, out, lse, ws, wsb, None)
+    assert attn(prm=lsa.AttnParams(64, 576, 512, False, 0.07)) == UNSUPPORTED
+    assert attn(prm=lsa.AttnParams(32, 576, 512, True, 0.07)) == UNSUPPORTED
+    assert attn(prm=lsa.AttnParams(64, 576, 512, True, 0.0)) == INVALID
+    assert attn(v=FAKE) == INVALID                                             # latent cache takes no V
+    assert attn(prm=lsa.AttnParams(sm_scale=0.1, **lsa.MQA)) == INVALID        # MQA needs V
+    assert attn(n_kv=0) == INVALID
+    assert attn(k_cap=0) == INVALID
+    assert attn(out=None) == INVALID
+    assert attn(q=MISALIGNED) == INVALID
+    assert attn(table=FAKE, max_pages=0) == INVALID
+    assert attn(n_rows=8, table=FAKE, max_pages=4, kv_page=64, ws=None) == WORKSPACE
+
+
+def test_workspace_sizes():
+    L = lsa.lib()
+    prm = P()
+    n = L.lsa_index_workspace_size(ctypes.byref(prm.c()), 131072, 131072)
+    # page scores (1024 per row) + page lists (64 per row) + fine scores (64*128 per row)
+    assert n == 131072 * 1024 * 4 + 131072 * 64 * 4 + 131072 * 8192 * 4
+    mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+    assert L.lsa_sparse_attn_workspace_size(ctypes.byref(mla.c()), 131072, 3076, 0) == 0
+    assert L.lsa_sparse_attn_workspace_size(ctypes.byref(mla.c()), 64, 2308, 1) > 64 * 2308 * 4
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(lsa, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(lsa, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        lsa.lib()

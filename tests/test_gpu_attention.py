@@ -1,0 +1,189 @@
+"""GPU parity of lsa_sparse_attn (MQA-128 and MLA-576/512, contiguous and paged caches) against the
+oracle's Eq. (3) through the C-ABI. The GPU and the oracle always get the same index list (built
+by the oracle or by the test), so the comparison isolates the attention kernel."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.lsa_oracle as orc
+from paper_2608_01662_amd import lsa, synth
+from paper_2608_01662_amd import workloads as W
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle_index(w, rows_t, n_kv):
+    inp = P.prefill_inputs(w, n_kv)
+    prm = P.oracle_params(w)
+    k_hat = P.oracle_keys(inp)
+    k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block) if w.keep_pages > 0 else None
+    qf = orc.bf16_bits_to_f64(inp["q"])
+    idx = np.full((len(rows_t), w.k_cap), -1, np.int32)
+    cnt = np.zeros(len(rows_t), np.int32)
+    for i, t in enumerate(rows_t):
+        S = orc.index_row(t, qf[t], inp["w"][t], k_hat, k_mean, prm)["S"]
+        idx[i, :S.size] = S
+        cnt[i] = S.size
+    return idx, cnt
+
+
+def _attn_inputs(w, layer, n_q, n_kv):
+    H, dqk, dv = w.attn_dims
+    return synth.attention_inputs(w.seed, layer, n_q, n_kv, H, dqk, dv, latent=(w.attn == "mla"))
+
+
+def _gpu_attn(w, a, rows, idx, cnt, lse=True):
+    q = P.bf16_dev(a["q"][rows])
+    kv = P.bf16_dev(a["kv"])
+    v = P.bf16_dev(a["v"]) if a["v"] is not None else None
+    o, l = lsa.sparse_attn(w.attn_params(), q, kv, v, P.to_dev(idx), P.to_dev(cnt), lse=lse)
+    torch.cuda.synchronize()
+    o = o.float().cpu().numpy()
+    return o, (l.cpu().numpy() if l is not None else None)
+
+
+def _check_rows(w, a, rows, idx, cnt, o, l):
+    H, dqk, dv = w.attn_dims
+    worst = (0.0, 0.0)
+    for i, t in enumerate(rows):
+        S = idx[i][: cnt[i]]
+        S = S[(S >= 0) & (S < a["kv"].shape[0])]
+        oref, lref = orc.attention_for_set(a["q"][t], a["kv"], a["v"], S, dv, w.sm_scale)
+        mx, rel = P.check_attention_row(o[i], None if l is None else l[i], oref, lref, f"row {t}")
+        worst = (max(worst[0], mx), max(worst[1], rel))
+    return worst
+
+
+@pytest.mark.parametrize("w", [W.L2K_MQA, W.SMALL_MLA], ids=lambda w: w.name)
+def test_attention_parity_oracle_index(w):
+    n = w.seq_len
+    rows = list(range(0, n, 3 if w.attn == "mqa" else 13)) + [n - 1, w.k_sink + w.k_swa + 1, 5]
+    idx, cnt = _oracle_index(w, rows, n)
+    a = _attn_inputs(w, 0, n, n)
+    o, l = _gpu_attn(w, a, rows, idx, cnt)
+    print(w.name, "worst (max|d|, rel)", _check_rows(w, a, rows, idx, cnt, o, l))
+
+
+@pytest.mark.parametrize("attn", ["mqa", "mla"])
+def test_dense_causal_equals_sdpa(attn):
+    """K >= t+1: the index list is [0, t] and sparse attention is causal softmax attention
+    (torch's scaled_dot_product_attention in float64 on the CPU)."""
+    from dataclasses import replace
+    w = replace(W.L2K_MQA if attn == "mqa" else W.SMALL_MLA, seq_len=200)
+    T = w.seq_len
+    H, dqk, dv = w.attn_dims
+    a = _attn_inputs(w, 0, T, T)
+    idx = np.full((T, T), -1, np.int32)
+    for t in range(T):
+        idx[t, :t + 1] = np.arange(t + 1)
+    cnt = np.arange(1, T + 1, dtype=np.int32)
+    o, l = _gpu_attn(w, a, list(range(T)), idx, cnt)
+    q = torch.from_numpy(orc.bf16_bits_to_f64(a["q"])).permute(1, 0, 2)[None]
+    kf = torch.from_numpy(orc.bf16_bits_to_f64(a["kv"]))
+    vf = kf[:, :dv] if a["v"] is None else torch.from_numpy(orc.bf16_bits_to_f64(a["v"]))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        q, kf[None, None].expand(1, H, T, dqk), vf.contiguous()[None, None].expand(1, H, T, dv),
+        is_causal=True, scale=w.sm_scale)[0].permute(1, 0, 2).numpy()
+    for t in range(T):
+        P.check_attention_row(o[t], None, ref[t], None, f"t={t}")
+
+
+@pytest.mark.parametrize("attn", ["mqa", "mla"])
+def test_closed_forms_and_edge_lists(attn):
+    from dataclasses import replace
+    w = replace(W.L2K_MQA if attn == "mqa" else W.SMALL_MLA, seq_len=300)
+    H, dqk, dv = w.attn_dims
+    n_kv = w.seq_len
+    a = _attn_inputs(w, 0, 8, n_kv)
+    k_cap = 96
+    g = np.random.default_rng(1)
+    idx = np.full((8, k_cap), -1, np.int32)
+    cnt = np.zeros(8, np.int32)
+    idx[0, 0] = 17; cnt[0] = 1                                       # one token: o = v_17
+    idx[1, :70] = g.choice(n_kv, 70, replace=False); cnt[1] = 70     # unsorted, ragged (70 = 2 tiles + 6)
+    idx[2, :70] = idx[1, :70][::-1]; cnt[2] = 70                     # same set, reversed order
+    cnt[3] = 0                                                       # empty set: o = 0, lse = -inf
+    idx[4, :40] = np.arange(40); idx[4, 10] = -1; idx[4, 20] = n_kv + 5; cnt[4] = 40   # bad entries skipped
+    idx[5, :k_cap] = np.arange(k_cap) * 3; cnt[5] = k_cap            # full capacity
+    idx[6, :33] = np.arange(33); cnt[6] = 33                         # one past a tile
+    idx[7, :5] = [0, 0, 1, 1, 2]; cnt[7] = 5                         # duplicates attend twice
+    rows = list(range(8))
+    a["q"] = a["q"][:8]
+    o, l = _gpu_attn(w, a, rows, idx, cnt)
+    vbits = a["kv"][:, :dv] if a["v"] is None else a["v"]
+    assert np.array_equal(o[0], np.repeat(orc.bf16_bits_to_f64(vbits[17])[None], H, 0))
+    assert np.abs(o[1] - o[2]).max() <= 2e-2 and np.allclose(l[1], l[2], atol=1e-4)
+    assert np.all(o[3] == 0) and np.all(np.isneginf(l[3]))
+    for i in (1, 4, 5, 6, 7):
+        S = idx[i][: cnt[i]]
+        S = S[(S >= 0) & (S < n_kv)]
+        oref, lref = orc.attention_for_set(a["q"][i], a["kv"], a["v"], S, dv, w.sm_scale)
+        P.check_attention_row(o[i], l[i], oref, lref, f"row {i}")
+
+
+def test_cross_layer_reuse():
+    """One index list feeds several layers (Sec. 3.2): each layer's output matches the oracle on
+    its own Q and KV, and the shared list is left byte-identical."""
+    w = W.SMALL_CLI
+    n = w.seq_len
+    rows = list(range(0, n, 41)) + [n - 1]
+    idx, cnt = _oracle_index(w, rows, n)
+    didx, dcnt = P.to_dev(idx), P.to_dev(cnt)
+    before = didx.clone()
+    for layer in range(w.layers):
+        a = _attn_inputs(w, layer, n, n)
+        q = P.bf16_dev(a["q"][rows])
+        o, l = lsa.sparse_attn(w.attn_params(), q, P.bf16_dev(a["kv"]), None, didx, dcnt)
+        torch.cuda.synchronize()
+        _check_rows(w, a, rows, idx, cnt, o.float().cpu().numpy(), l.cpu().numpy())
+    assert torch.equal(before, didx)
+
+
+def test_paged_equals_contiguous_and_oracle():
+    """Decode over a permuted page table equals the same rows attended in a contiguous cache, and
+    matches the oracle on the logical rows."""
+    w = W.SMALL_DECODE
+    H, dqk, dv = w.attn_dims
+    ctx, table, n_phys = synth.decode_layout(w.seed, w.batch, w.ctx_lo, w.ctx_hi, w.kv_page)
+    a = synth.attention_inputs(w.seed, 0, w.batch, n_phys * w.kv_page, H, dqk, dv, latent=True)
+    g = np.random.default_rng(2)
+    idx = np.full((w.batch, w.k_cap), -1, np.int32)
+    cnt = np.zeros(w.batch, np.int32)
+    for b in range(w.batch):
+        t = int(ctx[b]) - 1
+        S = np.unique(np.concatenate([np.arange(w.k_sink), g.choice(t + 1, w.k_sparse, replace=False),
+                                      np.arange(t - w.k_swa + 1, t + 1)]))
+        idx[b, :S.size] = S
+        cnt[b] = S.size
+    kv_paged = P.bf16_dev(a["kv"]).view(n_phys, w.kv_page, dqk)
+    q = P.bf16_dev(a["q"])
+    o_p, l_p = lsa.sparse_attn(w.attn_params(), q, kv_paged, None, P.to_dev(idx), P.to_dev(cnt),
+                               page_table=P.to_dev(table), kv_page_size=w.kv_page)
+    # contiguous equivalent: translate positions to pool rows on the host
+    phys_idx = np.full_like(idx, -1)
+    for b in range(w.batch):
+        S = idx[b, :cnt[b]]
+        phys_idx[b, :cnt[b]] = table[b][S // w.kv_page] * w.kv_page + S % w.kv_page
+    o_c, l_c = lsa.sparse_attn(w.attn_params(), q, P.bf16_dev(a["kv"]), None, P.to_dev(phys_idx), P.to_dev(cnt))
+    torch.cuda.synchronize()
+    assert torch.equal(o_p, o_c) and torch.equal(l_p, l_c)
+    pool = a["kv"].reshape(n_phys, w.kv_page, dqk)
+    for b in range(w.batch):
+        t = int(ctx[b]) - 1
+        kv_log = orc.logical_rows(pool, table[b], t + 1, w.kv_page)
+        oref, lref = orc.attention_for_set(a["q"][b], kv_log, None, idx[b, :cnt[b]], dv, w.sm_scale)
+        P.check_attention_row(o_p[b].float().cpu().numpy(), l_p[b].cpu().numpy(), oref, lref, f"seq {b}")
+
+
+def test_attention_determinism():
+    w = W.SMALL_MLA
+    n = w.seq_len
+    rows = list(range(0, n, 17))
+    idx, cnt = _oracle_index(w, rows, n)
+    a = _attn_inputs(w, 0, n, n)
+    o1, l1 = _gpu_attn(w, a, rows, idx, cnt)
+    o2, l2 = _gpu_attn(w, a, rows, idx, cnt)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)

@@ -1,0 +1,216 @@
+"""GPU parity of the LSA indexer (lsa_block_means, lsa_index_prefill, lsa_index_decode) against
+the oracle, through the C-ABI. Inputs are seeded and synthetic (paper_2608_01662_amd.synth)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.lsa_oracle as orc
+from paper_2608_01662_amd import lsa, synth
+from paper_2608_01662_amd import workloads as W
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def _sample_rows(n, every, extra=()):
+    rows = set(range(0, n, every)) | {n - 1} | {r for r in extra if 0 <= r < n}
+    return sorted(rows)
+
+
+def _run_prefill(w, inp, q_start=0, n_q=None, pages=True):
+    n_kv = inp["k"].shape[0]
+    n_q = n_kv - q_start if n_q is None else n_q
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_means(prm, k, ks) if w.keep_pages > 0 else None
+    out = lsa.index_prefill(prm, q[q_start:q_start + n_q], wt[q_start:q_start + n_q], k, ks, bk, q_start,
+                            n_kv=n_kv, runs=True, pages=pages)
+    torch.cuda.synchronize()
+    return {key: v.cpu().numpy() for key, v in out.items()}, bk
+
+
+def _oracle_rows(w, inp, rows_t):
+    prm = P.oracle_params(w)
+    k_hat = P.oracle_keys(inp)
+    k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block) if w.keep_pages > 0 else None
+    qf = orc.bf16_bits_to_f64(inp["q"])
+    return [orc.index_row(t, qf[t], inp["w"][t], k_hat, k_mean, prm) for t in rows_t]
+
+
+# ----------------------------------------------------------------------------- mean keys
+@pytest.mark.parametrize("fp8,B", [(False, 64), (True, 64), (True, 128), (True, 8), (False, 1)])
+def test_block_means_parity(fp8, B):
+    w = W.L2K_MQA if not fp8 else W.L32K_MLA
+    n = 4096 + 37  # ragged: the trailing partial sub-block is not written
+    inp = synth.indexer_inputs(5, 1, n, 1, w.head_dim, fp8)
+    page = 32 if B == 1 else (128 if B > 64 else 64)
+    prm = lsa.IndexParams(8, w.head_dim, fp8, page, B, 0, 16, 4, 128, 64)
+    _, _, k, ks = P.gpu_index_inputs(inp, w)
+    got = lsa.block_means(prm, k, ks).view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = orc.f64_to_bf16_bits(orc.sub_block_mean_keys(P.oracle_keys(inp), B))
+    assert got.shape == ref.shape
+    # fp32 accumulation vs float64: a value next to a bf16 rounding boundary may land one ulp away
+    diff = np.abs(got.astype(np.int32) - ref.astype(np.int32))
+    assert diff.max() <= 1 and (diff > 0).mean() < 1e-3, (diff.max(), (diff > 0).mean())
+
+
+def test_fp8_decode_all_codes():
+    """Mean keys with B = 1 and unit scales are the decoded codes: all 256 e4m3fn codes, exactly."""
+    codes = np.arange(256, dtype=np.uint32).astype(np.uint8)
+    codes = codes[(codes & 0x7F) != 0x7F]                                   # drop the two NaN codes
+    codes = np.concatenate([codes, codes[:2]]).reshape(-1, 64)             # 4 rows of 64 (d_I = 64)
+    prm = lsa.IndexParams(8, 64, True, 32, 1, 0, 16, 4, 128, 64)
+    out = lsa.block_means(prm, P.to_dev(codes), P.to_dev(np.ones(codes.shape[0], np.float32)))
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = orc.f64_to_bf16_bits(orc.e4m3fn_to_f64(codes))
+    assert np.array_equal(got, ref)
+
+
+# ----------------------------------------------------------------------------- prefill
+@pytest.mark.parametrize("w", [W.L2K_MQA, W.SMALL_FLAT, W.SMALL_MLA, W.SMALL_CLI, W.SMALL_SUBBLOCK],
+                         ids=lambda w: w.name)
+def test_index_prefill_parity(w):
+    inp = P.prefill_inputs(w)
+    out, _ = _run_prefill(w, inp)
+    n = w.seq_len
+    every = 1 if n <= 2048 else 5
+    boundary = [w.k_sink + w.k_swa - 1, w.k_sink + w.k_swa, w.k_sink + w.k_swa + 1,
+                w.k_sink + w.k_swa + w.page, w.keep_pages * w.page + w.k_swa, n - 2]
+    rows = _sample_rows(n, every, boundary)
+    res = _oracle_rows(w, inp, rows)
+    stats = P.check_index_rows(w, rows, out["idx"][rows], out["count"][rows],
+                               out["pages"][rows] if "pages" in out else None, res)
+    P.check_runs(out["runs"][rows], out["run_count"][rows], out["idx"][rows], out["count"][rows], w.run_align)
+    # every row (not only the sampled ones): structure
+    for t in range(0, n, 97):
+        P.check_structure(out["idx"][t][: out["count"][t]], t, w)
+    print(w.name, stats)
+
+
+def test_keep_all_equals_flat_on_gpu():
+    """With M >= #pages the hierarchical kernels must return exactly the flat selection."""
+    w = W.SMALL_MLA
+    inp = P.prefill_inputs(w)
+    from dataclasses import replace
+    flat, _ = _run_prefill(replace(w, keep_pages=0), inp, pages=False)
+    keep, _ = _run_prefill(replace(w, keep_pages=w.seq_len // w.page), inp, pages=False)
+    assert np.array_equal(flat["count"], keep["count"])
+    assert np.array_equal(flat["idx"], keep["idx"])
+
+
+def test_designed_inputs_select_latest():
+    """d-independent designed case: every head's query is +e_0 and key s has component 0 equal to
+    s+1 (all other components 0): every eligible token's score grows with s, so the sparse part is
+    the latest K_sparse eligible positions; with constant keys, ties go to the earliest."""
+    from dataclasses import replace
+    w = replace(W.L2K_MQA, keep_pages=0, seq_len=1024)
+    n, H, d = w.seq_len, w.n_heads, w.head_dim
+    for mode in ("increasing", "constant"):
+        q = np.zeros((n, H, d), np.float32)
+        q[:, :, 0] = 1.0
+        k = np.zeros((n, d), np.float32)
+        k[:, 0] = (np.arange(n) + 1) / 64.0 if mode == "increasing" else 1.0
+        inp = dict(q=synth.to_bf16_bits(q), w=np.ones((n, H), np.float32), k=synth.to_bf16_bits(k), k_scale=None)
+        out, _ = _run_prefill(w, inp, pages=False)
+        for t in range(w.k_sink + w.k_swa, n, 13):
+            elig = np.arange(w.k_sink, t - w.k_swa + 1)
+            want = elig[-w.k_sparse:] if mode == "increasing" else elig[:w.k_sparse]
+            S = out["idx"][t][: out["count"][t]]
+            assert np.array_equal(S[w.k_sink:S.size - w.k_swa], want), (mode, t)
+
+
+def test_chunked_equals_single_call():
+    """Rows of a chunked prefill equal the same rows of one call over the whole sequence."""
+    w = W.SMALL_CHUNKED
+    inp = P.prefill_inputs(w)
+    whole, _ = _run_prefill(w, inp)
+    for q0 in range(0, w.seq_len, w.chunk):
+        nq = min(w.chunk, w.seq_len - q0)
+        part, _ = _run_prefill(w, inp, q_start=q0, n_q=nq)
+        assert np.array_equal(part["idx"], whole["idx"][q0:q0 + nq])
+        assert np.array_equal(part["count"], whole["count"][q0:q0 + nq])
+        assert np.array_equal(part["runs"], whole["runs"][q0:q0 + nq])
+
+
+def test_chunked_parity_sampled():
+    w = W.SMALL_CHUNKED
+    inp = P.prefill_inputs(w)
+    q0 = 9000
+    out, _ = _run_prefill(w, inp, q_start=q0, n_q=w.chunk)
+    rows = list(range(0, w.chunk, 7)) + [w.chunk - 1]
+    res = _oracle_rows(w, inp, [q0 + r for r in rows])
+    P.check_index_rows(w, [q0 + r for r in rows], out["idx"][rows], out["count"][rows], out["pages"][rows], res)
+
+
+def test_determinism():
+    w = W.SMALL_MLA
+    inp = P.prefill_inputs(w)
+    a, _ = _run_prefill(w, inp)
+    b, _ = _run_prefill(w, inp)
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_empty_and_tiny():
+    w = W.L2K_MQA
+    inp = synth.indexer_inputs(9, 40, 40, w.n_heads, w.head_dim, False)
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_means(prm, k, ks)
+    # zero rows: nothing launched, nothing written
+    out = lsa.index_prefill(prm, q[:0], wt[:0], k, ks, bk, 0, n_kv=40)
+    assert out["idx"].shape == (0, w.k_cap)
+    # every row shorter than sink + window: S_t = [0, t]
+    out = lsa.index_prefill(prm, q, wt, k, ks, bk, 0, n_kv=40)
+    torch.cuda.synchronize()
+    for t in range(40):
+        assert out["count"][t].item() == t + 1
+        assert np.array_equal(out["idx"][t, :t + 1].cpu().numpy(), np.arange(t + 1))
+
+
+# ----------------------------------------------------------------------------- decode (paged)
+def _decode_case(w):
+    ctx, table, n_phys = synth.decode_layout(w.seed, w.batch, w.ctx_lo, w.ctx_hi, w.kv_page)
+    inp = synth.indexer_inputs(w.seed, w.batch, n_phys * w.kv_page, w.n_heads, w.head_dim, w.fp8)
+    return ctx, table, n_phys, inp
+
+
+def test_index_decode_parity():
+    w = W.SMALL_DECODE
+    ctx, table, n_phys, inp = _decode_case(w)
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_means(prm, k, ks)
+    out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk, pages=True)
+    torch.cuda.synchronize()
+    out = {key: v.cpu().numpy() for key, v in out.items()}
+    prmo = P.oracle_params(w)
+    k_hat_pool = P.oracle_keys(inp).reshape(n_phys, w.kv_page, -1)
+    qf = orc.bf16_bits_to_f64(inp["q"])
+    rows_t, res = [], []
+    for b in range(w.batch):
+        t = int(ctx[b]) - 1
+        k_log = orc.logical_rows(k_hat_pool, table[b], t + 1, w.kv_page)
+        k_mean = orc.sub_block_mean_keys(k_log, w.sub_block)
+        res.append(orc.index_row(t, qf[b], inp["w"][b], k_log, k_mean, prmo))
+        rows_t.append(t)
+    P.check_index_rows(w, rows_t, out["idx"], out["count"], out["pages"], res)
+    P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
+
+
+def test_decode_bad_rows_are_skipped():
+    """Out-of-range context lengths give count 0 (no fault, nothing selected)."""
+    w = W.SMALL_DECODE
+    ctx, table, n_phys, inp = _decode_case(w)
+    ctx = ctx.copy()
+    ctx[0] = 0
+    ctx[1] = table.shape[1] * w.kv_page + 1
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_means(prm, k, ks)
+    out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk)
+    torch.cuda.synchronize()
+    assert out["count"][0].item() == 0 and out["count"][1].item() == 0
+    assert out["count"][2].item() > 0
