@@ -116,7 +116,7 @@ void mla_attn_kernel(AttnGeom a) {
 
       // ---- partial S^T = K Q^T over this wave's 288 dims; K operand: token j, chunk 2s + h
       f32x16 sacc = {};
-      const uint8_t* kp = tb + (36 * kw) * 1024 + h * 512 + jx * 16;
+      const uint8_t* kp = tb + (36 * kw + h) * 512 + jx * 16;   // chunk 36kw + 2s + h
 #pragma unroll
       for (int s = 0; s < 18; ++s) {
         const u32x4 ka = *reinterpret_cast<const u32x4*>(kp + s * 1024);

@@ -212,11 +212,12 @@ lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void*
   if (s != LSA_OK) return s;
   const bool fp8 = p->key_dtype == LSA_KEY_FP8_E4M3FN;
   LSA_REQUIRE(n_tok >= 0, LSA_ERR_INVALID_ARG, "n_tok=%lld < 0", (long long)n_tok);
+  const int64_t n_sub = n_tok / p->sub_block;
+  if (n_sub == 0) return LSA_OK;  // nothing to read or write
   LSA_REQUIRE(k && block_keys, LSA_ERR_INVALID_ARG, "k / block_keys is NULL");
   LSA_REQUIRE(fp8 == (k_scale != nullptr), LSA_ERR_INVALID_ARG, "k_scale must be given exactly for fp8 keys");
   LSA_REQUIRE(aligned(k, 16) && aligned(block_keys, 16) && aligned(k_scale, 4), LSA_ERR_INVALID_ARG,
               "k/block_keys must be 16-byte aligned, k_scale 4-byte aligned");
-  const int64_t n_sub = n_tok / p->sub_block;
   hipError_t e = lsa::launch_block_means(n_sub, p->head_dim, p->sub_block, fp8, k, k_scale,
                                          static_cast<uint16_t*>(block_keys), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "block means");
@@ -224,12 +225,13 @@ lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void*
 }
 
 static lsa_status check_index_io(const lsa_index_params* p, const void* q, const float* w, const void* k,
-                                 const float* k_scale, const void* block_keys, int32_t* idx, int32_t* count,
-                                 lsa_run* runs, int32_t* run_count, void* workspace, size_t ws_bytes, size_t need) {
+                                 const float* k_scale, const void* block_keys, int64_t n_sub, int32_t* idx,
+                                 int32_t* count, lsa_run* runs, int32_t* run_count, void* workspace,
+                                 size_t ws_bytes, size_t need) {
   const bool fp8 = p->key_dtype == LSA_KEY_FP8_E4M3FN;
   LSA_REQUIRE(q && w && k && idx && count, LSA_ERR_INVALID_ARG, "q, w, k, idx and count must be non-NULL");
   LSA_REQUIRE(fp8 == (k_scale != nullptr), LSA_ERR_INVALID_ARG, "k_scale must be given exactly for fp8 keys");
-  LSA_REQUIRE(p->keep_pages <= 0 || block_keys != nullptr, LSA_ERR_INVALID_ARG,
+  LSA_REQUIRE(p->keep_pages <= 0 || n_sub == 0 || block_keys != nullptr, LSA_ERR_INVALID_ARG,
               "block_keys is NULL but keep_pages > 0 (hierarchical mode)");
   LSA_REQUIRE((runs == nullptr) == (run_count == nullptr), LSA_ERR_INVALID_ARG,
               "runs and run_count must be both NULL or both non-NULL");
@@ -260,9 +262,10 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
   const IndexPlan pl = plan_index(p, n_q, n_kv);
   s = check_lds(p, pl);
   if (s != LSA_OK) return s;
-  s = check_index_io(p, q, w, k, k_scale, block_keys, idx, count, runs, run_count, workspace, ws_bytes, pl.total);
+  if (n_q == 0) return LSA_OK;  // nothing to read or write
+  s = check_index_io(p, q, w, k, k_scale, block_keys, n_kv / p->sub_block, idx, count, runs, run_count, workspace,
+                     ws_bytes, pl.total);
   if (s != LSA_OK) return s;
-  if (n_q == 0) return LSA_OK;
   lsa::IndexGeom g = make_geom(p);
   g.q_start = q_start;
   g.n_kv = n_kv;
@@ -294,9 +297,10 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
   const IndexPlan pl = plan_index(p, batch, max_kv);
   s = check_lds(p, pl);
   if (s != LSA_OK) return s;
-  s = check_index_io(p, q, w, k, k_scale, block_keys, idx, count, runs, run_count, workspace, ws_bytes, pl.total);
+  if (batch == 0) return LSA_OK;  // nothing to read or write
+  s = check_index_io(p, q, w, k, k_scale, block_keys, n_phys * kv_page_size / p->sub_block, idx, count, runs,
+                     run_count, workspace, ws_bytes, pl.total);
   if (s != LSA_OK) return s;
-  if (batch == 0) return LSA_OK;
   lsa::IndexGeom g = make_geom(p);
   g.ctx_len = ctx_len;
   g.page_table = page_table;
@@ -324,6 +328,7 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
   const bool mla = p->latent != 0;
   LSA_REQUIRE(n_rows >= 0 && k_cap >= 1, LSA_ERR_INVALID_ARG, "n_rows < 0 or k_cap < 1");
   LSA_REQUIRE(n_rows < (1LL << 31), LSA_ERR_UNSUPPORTED, "n_rows must be < 2^31");
+  if (n_rows == 0) return LSA_OK;  // nothing to read or write
   LSA_REQUIRE(n_kv_rows >= 1 && n_kv_rows < (1LL << 31), LSA_ERR_INVALID_ARG, "n_kv_rows=%lld not in [1, 2^31)",
               (long long)n_kv_rows);
   LSA_REQUIRE(q && kv && idx && count && out, LSA_ERR_INVALID_ARG, "q, kv, idx, count and out must be non-NULL");

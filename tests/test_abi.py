@@ -138,3 +138,14 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(lsa, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         lsa.lib()
+
+
+def test_zero_sized_calls_accept_null_buffers():
+    """Nothing to read or write: empty tensors (NULL data pointers) are accepted, no launch."""
+    L = lsa.lib()
+    prm = P()
+    assert L.lsa_block_means(ctypes.byref(prm.c()), 64, None, None, None, None) == OK       # 64 < sub_block
+    assert prefill(prm, n_q=0, q=None, w=None, idx=None, cnt=None, ws=None, wsb=0) == OK
+    mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+    assert L.lsa_sparse_attn(ctypes.byref(mla.c()), 0, None, FAKE, None, 10, None, None, 8, None, 0, 0, 1,
+                             None, None, None, 0, None) == OK

@@ -111,7 +111,8 @@ def test_closed_forms_and_edge_lists(attn):
     idx[6, :33] = np.arange(33); cnt[6] = 33                         # one past a tile
     idx[7, :5] = [0, 0, 1, 1, 2]; cnt[7] = 5                         # duplicates attend twice
     rows = list(range(8))
-    a["q"] = a["q"][:8]
+    a["q"] = a["q"][:8].copy()
+    a["q"][2] = a["q"][1]                                            # rows 1 and 2: same query, same set
     o, l = _gpu_attn(w, a, rows, idx, cnt)
     vbits = a["kv"][:, :dv] if a["v"] is None else a["v"]
     assert np.array_equal(o[0], np.repeat(orc.bf16_bits_to_f64(vbits[17])[None], H, 0))

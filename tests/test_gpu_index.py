@@ -63,9 +63,9 @@ def test_fp8_decode_all_codes():
     codes = np.concatenate([codes, codes[:2]]).reshape(-1, 64)             # 4 rows of 64 (d_I = 64)
     prm = lsa.IndexParams(8, 64, True, 32, 1, 0, 16, 4, 128, 64)
     out = lsa.block_means(prm, P.to_dev(codes), P.to_dev(np.ones(codes.shape[0], np.float32)))
-    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
-    ref = orc.f64_to_bf16_bits(orc.e4m3fn_to_f64(codes))
-    assert np.array_equal(got, ref)
+    got = orc.bf16_bits_to_f64(out.view(torch.int16).cpu().numpy().view(np.uint16))
+    ref = orc.e4m3fn_to_f64(codes)                     # every code is exact in bf16
+    assert np.array_equal(got, ref)                    # value equality: the sum of one -0 is +0
 
 
 # ----------------------------------------------------------------------------- prefill
@@ -101,18 +101,19 @@ def test_keep_all_equals_flat_on_gpu():
 
 
 def test_designed_inputs_select_latest():
-    """d-independent designed case: every head's query is +e_0 and key s has component 0 equal to
-    s+1 (all other components 0): every eligible token's score grows with s, so the sparse part is
-    the latest K_sparse eligible positions; with constant keys, ties go to the earliest."""
+    """Designed case: every head's query is +e_0 and key s has component 0 equal to the bf16 value
+    with bit pattern 0x3F80 + s (strictly increasing and exact), all other components 0: every
+    eligible token's score grows with s, so the sparse part is the latest K_sparse eligible
+    positions; with constant keys, ties go to the earliest."""
     from dataclasses import replace
     w = replace(W.L2K_MQA, keep_pages=0, seq_len=1024)
     n, H, d = w.seq_len, w.n_heads, w.head_dim
     for mode in ("increasing", "constant"):
         q = np.zeros((n, H, d), np.float32)
         q[:, :, 0] = 1.0
-        k = np.zeros((n, d), np.float32)
-        k[:, 0] = (np.arange(n) + 1) / 64.0 if mode == "increasing" else 1.0
-        inp = dict(q=synth.to_bf16_bits(q), w=np.ones((n, H), np.float32), k=synth.to_bf16_bits(k), k_scale=None)
+        kb = np.zeros((n, d), np.uint16)
+        kb[:, 0] = (0x3F80 + np.arange(n)) if mode == "increasing" else 0x3F80
+        inp = dict(q=synth.to_bf16_bits(q), w=np.ones((n, H), np.float32), k=kb, k_scale=None)
         out, _ = _run_prefill(w, inp, pages=False)
         for t in range(w.k_sink + w.k_swa, n, 13):
             elig = np.arange(w.k_sink, t - w.k_swa + 1)
