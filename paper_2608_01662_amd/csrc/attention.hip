@@ -22,6 +22,20 @@ constexpr float kLazy = 8.0f;  // rescale when the max grows by more than this (
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// acc *= alpha on an MFMA accumulator kept in AGPRs, element by element through one VGPR. Written
+// as asm so that the accumulators never need VGPR copies outside this (rare) path.
+__device__ __forceinline__ f32x16 scale_acc(f32x16 acc, float alpha) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    float x = acc[r], t;
+    asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                 : "+a"(x), "=&v"(t)
+                 : "v"(alpha));
+    acc[r] = x;
+  }
+  return acc;
+}
+
 __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb) {
   const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pa));
   const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pb));
@@ -40,8 +54,8 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 // KV tiles of 32 gathered latent rows are double-buffered in LDS by direct global->LDS loads
 // (no VGPR staging). LDS tile layout is chunk-major: 16-byte chunk c (dims 8c..8c+7) of token t
 // sits at c*512 + (t ^ 4*(c&1))*16. Each direct load moves chunks (2k, 2k+1) of all 32 tokens,
-// so a lane always reads its own token row at base + 32k; the K-operand reads are 512 contiguous
-// bytes per half-wave, and the XOR on odd chunks keeps the transposed V reads conflict-free.
+// so a lane reads one token row at base + 32k and the lines of a row are fetched by consecutive
+// instructions; the K-operand reads are 512 contiguous bytes per half-wave.
 constexpr int kMlaT = 32;
 constexpr int kMlaLoads = 9;              // direct loads per wave per tile (36 per tile)
 constexpr int kMlaBuf = 36 * 1024;        // 36864 bytes per tile buffer
@@ -64,7 +78,6 @@ void mla_attn_kernel(AttnGeom a) {
   const int32_t* slots = a.rows + row * a.k_cap + s0;
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
   const int head = 32 * hw + j;
-  const int jx = j ^ (4 * h);  // token whose chunks this lane moves (odd chunks are swizzled)
   uint8_t* xch = lds + 2 * kMlaBuf;
 
   // Q^T as the B operand of S^T = K Q^T: column = head, k-step s covers dims 16s + 8h .. +7,
@@ -88,8 +101,10 @@ void mla_attn_kernel(AttnGeom a) {
     const int sl = tile * kMlaT + j;
     return (sl < n && r >= 0 && (int64_t)r < a.n_kv_rows) ? r : -1;
   };
+  // direct load K = 9w + k moves chunks (2K, 2K+1); lane (j, h) fills slot j of chunk 2K + h,
+  // which holds token j ^ 4h ^ 8(K&1).
   auto issue = [&](int prow, int buf) {
-    const int pr = __shfl(prow, jx);
+    const int pr = __shfl(prow, j ^ (4 * h));
     const uint8_t* src = kvb + (pr >= 0 ? (int64_t)pr * 1152 : 0) + 16 * h + 32 * (wv * kMlaLoads);
     uint8_t* dst = lds + buf * kMlaBuf + wv * (kMlaLoads * 1024);
 #pragma unroll
@@ -116,7 +131,8 @@ void mla_attn_kernel(AttnGeom a) {
 
       // ---- partial S^T = K Q^T over this wave's 288 dims; K operand: token j, chunk 2s + h
       f32x16 sacc = {};
-      const uint8_t* kp = tb + (36 * kw + h) * 512 + jx * 16;   // chunk 36kw + 2s + h
+      // K operand: token j, chunk c = 36kw + 2s + h, slot j ^ 4h ^ 8((c>>1)&1), (c>>1)&1 = (18kw+s)&1
+      const uint8_t* kp = tb + (36 * kw + h) * 512 + (j ^ (4 * h)) * 16;
 #pragma unroll
       for (int s = 0; s < 18; ++s) {
         const u32x4 ka = *reinterpret_cast<const u32x4*>(kp + s * 1024);
@@ -138,27 +154,33 @@ void mla_attn_kernel(AttnGeom a) {
       // ---- online softmax (base 2); lane holds tokens 8(r/4) + 4h + r%4 of head `head`.
       // Both waves of a head half see the same sums in the same order, so they agree exactly.
       const uint32_t vmask = (uint32_t)__ballot(r_cur >= 0);
-      float z[16];
-      float mx = -INFINITY;
+      if (vmask != 0xFFFFFFFFu) {  // partial or invalid tokens (last tile of a row): mask them
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int tk = 8 * (r / 4) + 4 * h + (r % 4);
-        z[r] = ((vmask >> tk) & 1u) ? sacc[r] * a.scale_log2 : -INFINITY;
-        mx = fmaxf(mx, z[r]);
+        for (int r = 0; r < 16; ++r) {
+          const int tk = 8 * (r / 4) + 4 * h + (r % 4);
+          sacc[r] = ((vmask >> tk) & 1u) ? sacc[r] : -INFINITY;
+        }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      float smax = sacc[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) smax = fmaxf(smax, sacc[r]);
+      smax = fmaxf(smax, __shfl_xor(smax, 32));
+      const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
       const bool need = mx > m + kLazy;
       if (__ballot(need)) {
+        // Rare after the first tile (the reference max only moves by > 2^8). The asm keeps the
+        // compiler from turning this branch into an every-tile multiply of all accumulators.
         const float alpha = need ? fast_exp2(m - mx) : 1.f;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[c] *= alpha;
+        for (int c = 0; c < 8; ++c) o[c] = scale_acc(o[c], alpha);
         l *= alpha;
         m = need ? mx : m;
       }
+      const float mb = m == -INFINITY ? 0.f : m;  // m = -inf only while every score is -inf
       float p[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        p[r] = z[r] == -INFINITY ? 0.f : fast_exp2(z[r] - m);
+        p[r] = fast_exp2(fmaf(sacc[r], a.scale_log2, -mb));  // -inf -> 0
         l += p[r];
       }
       const u32x4 pb0 = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
@@ -169,7 +191,8 @@ void mla_attn_kernel(AttnGeom a) {
       // token t0 + vq, dims 32c + 16*ch16 + 4gq .. +3, i.e. chunk 4c + 2*ch16 + gq/2.
       const int gi = lane & 15, vq = gi >> 2, gq = gi & 3;
       const int ch16 = (lane >> 4) & 1;
-      const int sw = 4 * (gq >> 1);  // odd chunks are token-swizzled by 4
+      // chunk 32kw + 4c + 2ch16 + gq/2: (c&1) = gq/2, ((c>>1)&1) = ch16
+      const int sw = 4 * (gq >> 1);
       const uint8_t* vb = tb + (32 * kw + 2 * ch16 + (gq >> 1)) * 512 + (gq & 1) * 8;
       const int t0 = 4 * h + vq;
       const int oa = (t0 ^ sw) * 16, ob = ((t0 + 8) ^ sw) * 16, oc = ((t0 + 16) ^ sw) * 16, od = ((t0 + 24) ^ sw) * 16;
