@@ -81,6 +81,8 @@ __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+// Workgroup barrier that the compiler cannot move memory accesses across (no wait implied).
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 // All LDS reads of this wave have returned; then barrier (used before a buffer is refilled).
 __device__ __forceinline__ void lds_done_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
