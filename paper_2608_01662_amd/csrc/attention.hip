@@ -24,9 +24,10 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 // acc *= alpha on an MFMA accumulator kept in AGPRs, element by element through one VGPR. Written
 // as asm so that the accumulators never need VGPR copies outside this (rare) path.
-__device__ __forceinline__ f32x16 scale_acc(f32x16 acc, float alpha) {
+template <typename V, int N>
+__device__ __forceinline__ V scale_acc(V acc, float alpha) {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
+  for (int r = 0; r < N; ++r) {
     float x = acc[r], t;
     asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
                  : "+a"(x), "=&v"(t)
@@ -44,29 +45,45 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 }
 
 // ============================================================================ MLA 64 x 576 / 512
-// One workgroup = 4 waves = one query row (or one split of it). Wave (hw, kw) = (w >> 1, w & 1)
-// owns heads 32hw..32hw+31 and
-//   * computes the partial S^T over dims [288 kw, 288 kw + 288) of the 576 (18 MFMA k-steps);
-//     the two partials of a head half are summed through a 16 KB LDS exchange,
-//   * accumulates O^T for value columns [256 kw, 256 kw + 256) (8 tiles of 32 x 32).
-// Every wave does the same MFMA work and holds 72 Q-operand and 128 accumulator registers.
+// One workgroup = 8 waves = one query row (or one split of its index list), two waves per SIMD
+// so that one wave's softmax and LDS traffic overlap the other's matrix work. Wave
+// (hq, kw) = (w >> 1, w & 1) owns heads 16hq..16hq+15 and
+//   * computes the partial S^T (32 tokens x 16 heads, two 16x16x32 M-tiles) over dims
+//     [288 kw, 288 kw + 288) of the 576; the two partials of a head quarter are summed through a
+//     2 KB-per-wave LDS exchange (a + b == b + a, so both waves see identical scores),
+//   * accumulates O^T for value columns [256 kw, 256 kw + 256): 16 blocks of 16 x 16.
+// Per wave: 36 Q-operand registers and 64 accumulator registers.
 //
-// KV tiles of 32 gathered latent rows are double-buffered in LDS by direct global->LDS loads
-// (no VGPR staging). LDS tile layout is chunk-major: 16-byte chunk c (dims 8c..8c+7) of token t
-// sits at c*512 + (t ^ 4*(c&1))*16. Each direct load moves chunks (2k, 2k+1) of all 32 tokens,
-// so a lane reads one token row at base + 32k and the lines of a row are fetched by consecutive
-// instructions; the K-operand reads are 512 contiguous bytes per half-wave.
+// The row's index list is validated once into LDS (-1 for entries to skip). Tiles of 32 gathered
+// latent rows are moved by direct global->LDS loads into NBUF rotating buffers (NBUF - 1 tiles in
+// flight while one is consumed); waves 0..3 issue them. Tile layout is chunk-major: 16-byte chunk
+// c (dims 8c..8c+7) of token t sits at c*512 + (t ^ kMlaSwz*(c&1))*16, so the K-operand reads are
+// 256 contiguous bytes per 16 lanes and the transposed V reads of two neighbouring chunks land in
+// disjoint bank halves (the LDS bank-conflict counter reads zero for this kernel).
+//
+// Schedules that were measured and not kept: running the two wave groups half a tile apart
+// (ping-pong) is slower here, because the 36 KB of LDS writes a tile refill makes hold up the
+// LDS reads of whichever group computes scores meanwhile; staging the tiles through VGPRs instead
+// of direct loads has the same effect.
 constexpr int kMlaT = 32;
-constexpr int kMlaLoads = 9;              // direct loads per wave per tile (36 per tile)
-constexpr int kMlaBuf = 36 * 1024;        // 36864 bytes per tile buffer
-constexpr int kMlaXch = 4 * 4096;         // partial-score exchange, 4 KB per wave
+constexpr int kMlaTile = 36 * 1024;  // 72 chunks x 32 tokens x 16 bytes
+constexpr int kMlaXch = 8 * 2048;    // partial-score exchange, 2 KB per wave
+constexpr int kMlaLoaders = 4;       // waves that issue the direct loads
+constexpr int kMlaLoads = 9;         // direct loads per loader wave per tile (36 x 1 KB)
+constexpr int kMlaSwz = 12;
+constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
 
-template <bool SPLIT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <bool SPLIT, int NBUF>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void mla_attn_kernel(AttnGeom a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kMlaBuf + kMlaXch];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, h = lane >> 5, j = lane & 31;
-  const int hw = wv >> 1, kw = wv & 1;
+  static_assert(NBUF >= 2 && NBUF <= 3, "two or three tile buffers");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[NBUF * kMlaTile + kMlaXch];
+  __shared__ int32_t ids[kMlaIdCap];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int i16 = lane & 15, g = lane >> 4;
+  const int hq = wv >> 1, kw = wv & 1;
+  const int head = 16 * hq + i16;
+  const bool loader = wv < kMlaLoaders;
   const int64_t row = xcd_band(blockIdx.x, a.n_rows);
   const int split = SPLIT ? (int)blockIdx.y : 0;
   int cnt = a.count[row];
@@ -74,165 +91,178 @@ void mla_attn_kernel(AttnGeom a) {
   const int s0 = split * a.split_len;
   const int s1 = SPLIT ? (cnt < s0 + a.split_len ? cnt : s0 + a.split_len) : cnt;
   const int n = s1 > s0 ? s1 - s0 : 0;
-  const int ntiles = (n + kMlaT - 1) / kMlaT;
   const int32_t* slots = a.rows + row * a.k_cap + s0;
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
-  const int head = 32 * hw + j;
-  uint8_t* xch = lds + 2 * kMlaBuf;
+  uint8_t* xch = lds + NBUF * kMlaTile;
 
-  // Q^T as the B operand of S^T = K Q^T: column = head, k-step s covers dims 16s + 8h .. +7,
-  // s in [18 kw, 18 kw + 18).
-  u32x4 qb[18];
+  // Q^T as the B operand of S^T = K Q^T: column = head, k-step s covers dims 288kw + 32s + 8g .. +7.
+  u32x4 qb[9];
   {
-    const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (row * 64 + head) * 576 + 8 * h) + 36 * kw;
+    const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (row * 64 + head) * 576 + 288 * kw + 8 * g);
 #pragma unroll
-    for (int s = 0; s < 18; ++s) qb[s] = qp[2 * s];
+    for (int s = 0; s < 9; ++s) qb[s] = qp[4 * s];
   }
-  f32x16 o[8];
+  f32x4 o[16];
 #pragma unroll
-  for (int c = 0; c < 8; ++c) o[c] = f32x16{};
+  for (int c = 0; c < 16; ++c) o[c] = f32x4{};
   float m = -INFINITY, l = 0.f;
 
-  auto fetch = [&](int tile) -> int {  // exactly one load per call
-    const int sl = tile * kMlaT + j;
-    return slots[sl < n ? sl : n - 1];
-  };
-  auto checked = [&](int tile, int r) -> int {
-    const int sl = tile * kMlaT + j;
-    return (sl < n && r >= 0 && (int64_t)r < a.n_kv_rows) ? r : -1;
-  };
-  // direct load K = 9w + k moves chunks (2K, 2K+1); lane (j, h) fills slot j of chunk 2K + h,
-  // which holds token j ^ 4h ^ 8(K&1).
-  auto issue = [&](int prow, int buf) {
-    const int pr = __shfl(prow, j ^ (4 * h));
-    const uint8_t* src = kvb + (pr >= 0 ? (int64_t)pr * 1152 : 0) + 16 * h + 32 * (wv * kMlaLoads);
-    uint8_t* dst = lds + buf * kMlaBuf + wv * (kMlaLoads * 1024);
-#pragma unroll
-    for (int k = 0; k < kMlaLoads; ++k)
-      __builtin_amdgcn_global_load_lds(src + 32 * k, LSA_LDS(dst + k * 1024), 16, 0, 0);
+  // K operand (token 16mt + i16, chunk 36kw + 4s + g; chunk parity = g & 1)
+  const int k_off = (36 * kw + g) * 512 + (i16 ^ (kMlaSwz * (g & 1))) * 16;
+  // V^T operand of value block c: source lane (vq, gq) supplies token 4g + vq (and +16), dims
+  // 256kw + 16c + 4gq .. +3, i.e. chunk 32kw + 2c + gq/2 (parity gq/2), byte 8(gq&1).
+  const int vq = i16 >> 2, gq = i16 & 3;
+  const int v_off = (32 * kw + (gq >> 1)) * 512 + ((4 * g + vq) ^ (kMlaSwz * (gq >> 1))) * 16 + (gq & 1) * 8;
+  // Direct load K (= 9 wv + k) moves chunks (2K, 2K+1) of the 32 tokens: lane (j, h) fills slot j
+  // of chunk 2K + h, i.e. token j ^ kMlaSwz*h, from bytes 16h + 32K of that token's row.
+  const int lj = lane & 31, lh = lane >> 5;
+  const int dma_tok = lj ^ (kMlaSwz * lh);
+  const int64_t dma_col = 16 * lh + 32 * (kMlaLoads * wv);
+  auto issue = [&](int tile, int buf) {
+    const int r = ids[tile * kMlaT + dma_tok];
+    const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
+    const uint8_t* const srcs[kMlaLoads] = {src,       src + 32,  src + 64,  src + 96, src + 128,
+                                            src + 160, src + 192, src + 224, src + 256};
+    lds_dma16x9(srcs, lds_addr(lds + buf * kMlaTile + wv * (kMlaLoads * 1024)));
   };
 
-  if (ntiles > 0) {
-    const int raw0 = fetch(0);
-    int raw_next = fetch(ntiles > 1 ? 1 : 0);
-    int r_cur = checked(0, raw0);
-    issue(r_cur, 0);
+  for (int c0 = 0; c0 < n; c0 += kMlaIdCap) {
+    const int nc = n - c0 < kMlaIdCap ? n - c0 : kMlaIdCap;
+    const int ntiles = (nc + kMlaT - 1) / kMlaT;
+    // list entries -> LDS, validated (-1 = skip; the last tile is padded with -1)
+    __syncthreads();  // the previous chunk's readers of `ids` are done
+    {
+      constexpr int U = kMlaIdCap / 512;
+      int v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = (int)threadIdx.x + 512 * u;
+        v[u] = i < nc ? slots[c0 + i] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = (int)threadIdx.x + 512 * u;
+        if (i < ntiles * kMlaT) ids[i] = (v[u] >= 0 && (int64_t)v[u] < a.n_kv_rows) ? v[u] : -1;
+      }
+    }
+    __syncthreads();
+    // the Q operand arrived before the list entries; let the compiler place its wait for Q here,
+    // ahead of the first direct loads, rather than drain those loads before the first tile
+#pragma unroll
+    for (int s = 0; s < 9; ++s) asm volatile("" ::"v"(qb[s]));
+    if (loader)
+      for (int x = 0; x < NBUF - 1 && x < ntiles; ++x) issue(x, x);
+
+    // byte offsets of the buffer being read and of the one refilled next, rotated as wave-uniform
+    // scalars (a modulo by the buffer count would be strength-reduced into per-read address math)
+    uint32_t cur_off = 0, next_off = (NBUF - 1) * kMlaTile;
     for (int it = 0; it < ntiles; ++it) {
-      int r_next = -1;
-      if (it + 1 < ntiles) {
-        r_next = checked(it + 1, raw_next);
-        issue(r_next, (it + 1) & 1);
-        raw_next = fetch(it + 2 < ntiles ? it + 2 : it + 1);
-        vm_wait_barrier<kMlaLoads + 1>();
+      // tile `it` has landed (a loader may keep the loads of later tiles in flight); after this
+      // barrier every wave is also done with tile it - 1, whose buffer is refilled next
+      if (loader) {
+        if (NBUF == 3 && it + 1 < ntiles) vm_wait_barrier<kMlaLoads>();
+        else vm_wait_barrier<0>();
+        if (it + NBUF - 1 < ntiles) issue(it + NBUF - 1, next_off / kMlaTile);
       } else {
-        vm_wait_barrier<0>();
+        barrier_only();
       }
-      const uint8_t* tb = lds + (it & 1) * kMlaBuf;
+      const uint8_t* tb = lds + __builtin_amdgcn_readfirstlane(cur_off);
+      cur_off = cur_off + kMlaTile == NBUF * kMlaTile ? 0 : cur_off + kMlaTile;
+      next_off = next_off + kMlaTile == NBUF * kMlaTile ? 0 : next_off + kMlaTile;
 
-      // ---- partial S^T = K Q^T over this wave's 288 dims; K operand: token j, chunk 2s + h
-      f32x16 sacc = {};
-      // K operand: token j, chunk c = 36kw + 2s + h, slot j ^ 4h ^ 8((c>>1)&1), (c>>1)&1 = (18kw+s)&1
-      const uint8_t* kp = tb + (36 * kw + h) * 512 + (j ^ (4 * h)) * 16;
+      // ---- partial S^T = K Q^T over this wave's 288 dims
+      // all 18 K operands are requested before the first product, so the LDS latency is paid
+      // once per tile rather than once per product
+      u32x4 ka[18];
 #pragma unroll
-      for (int s = 0; s < 18; ++s) {
-        const u32x4 ka = *reinterpret_cast<const u32x4*>(kp + s * 1024);
-        sacc = mfma32(ka, qb[s], sacc);
-      }
-      // ---- sum the two partials of this head half through LDS
+      for (int s = 0; s < 9; ++s)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) ka[2 * s + mt] = *reinterpret_cast<const u32x4*>(tb + k_off + s * 2048 + mt * 256);
+      __builtin_amdgcn_sched_barrier(0);  // keep the scheduler from sinking the reads again
+      f32x4 sacc[2] = {f32x4{}, f32x4{}};
+#pragma unroll
+      for (int s = 0; s < 9; ++s)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) sacc[mt] = mfma16(ka[2 * s + mt], qb[s], sacc[mt]);
+      // ---- sum the two partials of this head quarter
       {
-        f32x4* mine = reinterpret_cast<f32x4*>(xch + wv * 4096) + lane;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) mine[64 * q4] = f32x4{sacc[4 * q4], sacc[4 * q4 + 1], sacc[4 * q4 + 2], sacc[4 * q4 + 3]};
+        f32x4* mine = reinterpret_cast<f32x4*>(xch + wv * 2048) + lane;
+        mine[0] = sacc[0];
+        mine[64] = sacc[1];
         lds_done_barrier();
-        const f32x4* other = reinterpret_cast<const f32x4*>(xch + (wv ^ 1) * 4096) + lane;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const f32x4 v = other[64 * q4];
-          sacc[4 * q4] += v[0]; sacc[4 * q4 + 1] += v[1]; sacc[4 * q4 + 2] += v[2]; sacc[4 * q4 + 3] += v[3];
-        }
+        const f32x4* other = reinterpret_cast<const f32x4*>(xch + (wv ^ 1) * 2048) + lane;
+        sacc[0] += other[0];
+        sacc[1] += other[64];
       }
-      // ---- online softmax (base 2); lane holds tokens 8(r/4) + 4h + r%4 of head `head`.
-      // Both waves of a head half see the same sums in the same order, so they agree exactly.
-      const uint32_t vmask = (uint32_t)__ballot(r_cur >= 0);
-      if (vmask != 0xFFFFFFFFu) {  // partial or invalid tokens (last tile of a row): mask them
+      // ---- online softmax (base 2); lane holds tokens 16mt + 4g + r of head `head`
+      const uint32_t vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
+      if (vmask != 0xFFFFFFFFu) {  // partial or skipped tokens: mask them
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int tk = 8 * (r / 4) + 4 * h + (r % 4);
-          sacc[r] = ((vmask >> tk) & 1u) ? sacc[r] : -INFINITY;
-        }
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int tk = 16 * mt + 4 * g + r;
+            sacc[mt][r] = ((vmask >> tk) & 1u) ? sacc[mt][r] : -INFINITY;
+          }
       }
-      float smax = sacc[0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) smax = fmaxf(smax, sacc[r]);
-      smax = fmaxf(smax, __shfl_xor(smax, 32));
+      float smax = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
+                         fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+      smax = max4_xor16_32(smax);
       const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
       const bool need = mx > m + kLazy;
       if (__ballot(need)) {
-        // Rare after the first tile (the reference max only moves by > 2^8). The asm keeps the
-        // compiler from turning this branch into an every-tile multiply of all accumulators.
+        // Rare after the first tile (the reference max only moves by > 2^8).
         const float alpha = need ? fast_exp2(m - mx) : 1.f;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[c] = scale_acc(o[c], alpha);
+        for (int c = 0; c < 16; ++c) o[c] *= alpha;
         l *= alpha;
         m = need ? mx : m;
       }
       const float mb = m == -INFINITY ? 0.f : m;  // m = -inf only while every score is -inf
-      float p[16];
+      float p[8];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = fast_exp2(fmaf(sacc[r], a.scale_log2, -mb));  // -inf -> 0
-        l += p[r];
-      }
-      const u32x4 pb0 = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
-      const u32x4 pb1 = {pack_bf16x2(p[8], p[9]), pack_bf16x2(p[10], p[11]), pack_bf16x2(p[12], p[13]),
-                         pack_bf16x2(p[14], p[15])};
-      // ---- O^T += V^T P^T over this wave's 256 value columns; V^T via transposed LDS reads.
-      // 16-lane group (column half ch16 = (lane>>4)&1, token half h); source lane (vq, gq) reads
-      // token t0 + vq, dims 32c + 16*ch16 + 4gq .. +3, i.e. chunk 4c + 2*ch16 + gq/2.
-      const int gi = lane & 15, vq = gi >> 2, gq = gi & 3;
-      const int ch16 = (lane >> 4) & 1;
-      // chunk 32kw + 4c + 2ch16 + gq/2: (c&1) = gq/2, ((c>>1)&1) = ch16
-      const int sw = 4 * (gq >> 1);
-      const uint8_t* vb = tb + (32 * kw + 2 * ch16 + (gq >> 1)) * 512 + (gq & 1) * 8;
-      const int t0 = 4 * h + vq;
-      const int oa = (t0 ^ sw) * 16, ob = ((t0 + 8) ^ sw) * 16, oc = ((t0 + 16) ^ sw) * 16, od = ((t0 + 24) ^ sw) * 16;
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const uint8_t* pc = vb + c * 2048;
-        o[c] = mfma32(tr16_pair(pc + oa, pc + ob), pb0, o[c]);
-        o[c] = mfma32(tr16_pair(pc + oc, pc + od), pb1, o[c]);
+        for (int r = 0; r < 4; ++r) {
+          p[4 * mt + r] = fast_exp2(fmaf(sacc[mt][r], a.scale_log2, -mb));  // -inf -> 0
+          l += p[4 * mt + r];
+        }
+      // B operand P^T: k index 8g + v <-> token (v < 4 ? 4g + v : 16 + 4g + v - 4)
+      const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                        pack_bf16x2(p[6], p[7])};
+      // ---- O^T += V^T P^T over this wave's 256 value columns; V^T via transposed LDS reads
+      // (V operands requested in two batches of eight, again to pay the LDS latency rarely)
+      const uint8_t* vb = tb + v_off;
+#pragma unroll
+      for (int c8 = 0; c8 < 16; c8 += 8) {
+        u32x4 va[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) va[c] = tr16_pair(vb + (c8 + c) * 1024, vb + (c8 + c) * 1024 + 256);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) o[c8 + c] = mfma16(va[c], pb, o[c8 + c]);
       }
-      lds_done_barrier();  // tile buffer and exchange slots are free again
-      r_cur = r_next;
     }
   }
 
-  const float lt = l + __shfl_xor(l, 32);
-  const int dv0 = 256 * kw + 4 * h;
+  const float lt = sum4_xor16_32(l);
+  // accumulator layout: lane holds value columns 256kw + 16c + 4g + r of head `head`
+  const int dv0 = 256 * kw + 4 * g;
   if (!SPLIT) {
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     uint16_t* orow = a.out + (row * 64 + head) * 512 + dv0;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const u32x2 v = {pack_bf16x2(o[c][4 * rr] * inv, o[c][4 * rr + 1] * inv),
-                         pack_bf16x2(o[c][4 * rr + 2] * inv, o[c][4 * rr + 3] * inv)};
-        *reinterpret_cast<u32x2*>(orow + 32 * c + 8 * rr) = v;
-      }
+    for (int c = 0; c < 16; ++c) {
+      const u32x2 v = {pack_bf16x2(o[c][0] * inv, o[c][1] * inv), pack_bf16x2(o[c][2] * inv, o[c][3] * inv)};
+      *reinterpret_cast<u32x2*>(orow + 16 * c) = v;
     }
-    if (a.lse && h == 0 && kw == 0) a.lse[row * 64 + head] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
+    if (a.lse && g == 0 && kw == 0) a.lse[row * 64 + head] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
   } else {
     const int64_t pi = (row * a.n_split + split) * 64 + head;
     float* po = a.part_o + pi * 512 + dv0;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-        *reinterpret_cast<f32x4*>(po + 32 * c + 8 * rr) =
-            f32x4{o[c][4 * rr], o[c][4 * rr + 1], o[c][4 * rr + 2], o[c][4 * rr + 3]};
-    }
-    if (h == 0 && kw == 0) {
+    for (int c = 0; c < 16; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = o[c];
+    if (g == 0 && kw == 0) {
       a.part_ml[pi * 2] = m;
       a.part_ml[pi * 2 + 1] = lt;
     }
@@ -403,15 +433,19 @@ __global__ __launch_bounds__(256) void translate_rows_kernel(const int32_t* __re
 }
 
 // ============================================================================ host launchers
+// Two tile buffers: one tile in flight while one is consumed. A third buffer (two in flight)
+// measured no faster at the L = 128K shape.
+constexpr int kMlaBufs = 2;
+
 hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st) {
   if (a.n_rows == 0) return hipSuccess;
   if (a.n_split > 1) {
-    hipLaunchKernelGGL(mla_attn_kernel<true>, dim3((unsigned)a.n_rows, (unsigned)a.n_split), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((mla_attn_kernel<true, kMlaBufs>), dim3((unsigned)a.n_rows, (unsigned)a.n_split), dim3(512), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_attn_combine(a, 64, 512, st);
   }
-  hipLaunchKernelGGL(mla_attn_kernel<false>, dim3((unsigned)a.n_rows), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((mla_attn_kernel<false, kMlaBufs>), dim3((unsigned)a.n_rows), dim3(512), 0, st, a);
   return hipGetLastError();
 }
 

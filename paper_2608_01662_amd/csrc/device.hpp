@@ -81,6 +81,14 @@ __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+// Wait until at most N vector-memory operations are outstanding and every LDS access of this
+// wave has completed (so its LDS writes are visible), then join the workgroup barrier.
+// N = 63 leaves the vector-memory count alone.
+template <int N>
+__device__ __forceinline__ void vm_lds_wait_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
 // Workgroup barrier that the compiler cannot move memory accesses across (no wait implied).
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 // All LDS reads of this wave have returned; then barrier (used before a buffer is refilled).
@@ -90,6 +98,45 @@ __device__ __forceinline__ void lds_done_barrier() {
 // Full workgroup barrier with LDS visibility (ordinary ds_write -> ds_read hand-off).
 __device__ __forceinline__ void block_sync() { __syncthreads(); }
 
+// ---------------------------------------------------------------- direct global -> LDS loads
+// Nine loads of 16 bytes per lane: load k reads 16 bytes at src[k] and writes LDS bytes
+// [lds + 1024k + 16 lane, +16). Written as one asm block so that the compiler does not see LDS
+// being written by vector-memory loads: it would otherwise drain every such load in flight before
+// any later LDS read it cannot prove disjoint. Callers order these loads with explicit vmcnt
+// waits and barriers. M0, which holds the LDS base of the loads, is saved and restored.
+__device__ __forceinline__ void lds_dma16x9(const uint8_t* const (&src)[9], uint32_t lds) {
+  uint32_t save;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %10\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %3, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %4, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %5, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %6, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %7, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %8, off\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "global_load_lds_dwordx4 %9, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(save)
+      : "v"(src[0]), "v"(src[1]), "v"(src[2]), "v"(src[3]), "v"(src[4]), "v"(src[5]), "v"(src[6]), "v"(src[7]),
+        "v"(src[8]), "s"(lds)
+      : "memory", "scc");
+}
+// LDS byte address of a pointer into __shared__ memory (the low 32 bits of its generic address).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+
 // ---------------------------------------------------------------- wave reductions
 __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
@@ -98,6 +145,22 @@ __device__ __forceinline__ float wave_max(float v) {
 __device__ __forceinline__ int wave_sum(int v) {
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
   return v;
+}
+// Reductions over the four lanes l, l^16, l^32, l^48 with gfx950's row swaps: after
+// v_permlane16_swap(x, x) a lane holds {x[l], x[l^16]} in its two results, after
+// v_permlane32_swap the same for l^32. VALU only; since a + b == b + a, all four lanes end with
+// bit-identical results.
+__device__ __forceinline__ float max4_xor16_32(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum4_xor16_32(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 __device__ __forceinline__ uint64_t lanemask_lt() {
   int l = threadIdx.x & 63;
