@@ -14,6 +14,7 @@ Diagnostics go to stderr.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -33,8 +34,50 @@ HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mla_attn_kernel_L131072_hbm_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_01662_amd", "csrc", f) for f in ("attention.hip", "device.hpp")]
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
+    or None when that summary is missing or was taken on different kernel sources."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as fh:
+            for line in fh:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("kernel_sources_sha256") != kernel_source_hash():
+            return None
+        return int(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_probe(nbytes: int):
+    """A plain device copy of known size, run under rocprofv3 --pmc to calibrate FETCH_SIZE and
+    WRITE_SIZE (each copy reads and writes exactly nbytes)."""
+    dev = torch.device("cuda:0")
+    src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "copies": 3}), flush=True)
 
 
 def make_inputs(w, dev):
@@ -109,6 +152,8 @@ def main():
     ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL if not w.decode and not w.chunk])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
@@ -116,6 +161,9 @@ def main():
         sys.exit(2)
     if args.steps < 1 or args.warmup < 0:
         sys.exit("--steps must be >= 1 and --warmup >= 0")
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -209,7 +257,7 @@ def main():
                                "run_align": w.run_align},
                    "attention": {"kind": w.attn, "heads": H, "d_qk": dqk, "d_v": dv}},
         "roofline": {"kernel": "mla_attn_kernel", "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_avg},
         "breakdown": {
             "block_means_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,

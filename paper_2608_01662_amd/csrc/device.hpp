@@ -81,14 +81,6 @@ __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-// Wait until at most N vector-memory operations are outstanding and every LDS access of this
-// wave has completed (so its LDS writes are visible), then join the workgroup barrier.
-// N = 63 leaves the vector-memory count alone.
-template <int N>
-__device__ __forceinline__ void vm_lds_wait_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
-}
 // Workgroup barrier that the compiler cannot move memory accesses across (no wait implied).
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 // All LDS reads of this wave have returned; then barrier (used before a buffer is refilled).
