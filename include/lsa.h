@@ -95,7 +95,8 @@ lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void*
 
 /*
  * Indexer for prefill (Eq. 6-7, 9-12): query rows i = 0..n_q-1 at positions t = q_start + i of
- * one sequence whose first n_kv tokens are cached (requires q_start + n_q <= n_kv).
+ * one sequence whose first n_kv tokens are cached (requires q_start + n_q <= n_kv, n_kv < 2^31
+ * and n_q < 2^28; longer prefills are issued in chunks through q_start).
  *   q          [n_q, H^I, d_I] bf16 indexer queries
  *   w          [n_q, H^I] fp32 head weights (any sign)
  *   k, k_scale [n_kv, d_I] keys (+ [n_kv] fp32 scales for fp8, NULL for bf16)

@@ -21,6 +21,15 @@
 
 namespace lsa {
 
+// 8 e4m3fn codes (two dwords) -> one bf16x8 MFMA operand with gfx950's packed converter: two
+// codes per instruction (scale 1.0, so the exact values come out as bf16).
+__device__ __forceinline__ u32x4 fp8x8_to_bf16x8_pk(uint32_t a, uint32_t b) {
+  return u32x4{__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(a, 1.0f, false)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(a, 1.0f, true)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(b, 1.0f, false)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(b, 1.0f, true))};
+}
+
 // ============================================================================ row geometry
 struct RowInfo {
   int64_t t;       // query position
@@ -132,11 +141,18 @@ __device__ __forceinline__ void load_key_operand(const void* __restrict__ k, int
   }
 }
 
-// sum_j w_j ReLU(acc_j) over the 32 heads of this lane's key column (Eq. 1 / Eq. 9).
+// max(x, 0) as one integer max on the bit pattern: negative floats (sign bit set) are negative
+// integers and become +0, non-negative floats are unchanged. fmaxf would first quiet signalling
+// NaNs with an extra v_max x, x, since an MFMA result is not known to be canonical.
+__device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
+
+// sum_j w_j ReLU(acc_j) over the 32 heads of this lane's key column (Eq. 1 / Eq. 9), as four
+// interleaved partial sums (a fixed order, so every tile and row rounds the same way).
 __device__ __forceinline__ float head_reduce(const f32x16& acc, const float (&wr)[16]) {
-  float v = 0.f;
+  float p[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int r = 0; r < 16; ++r) v = fmaf(wr[r], fmaxf(acc[r], 0.f), v);
+  for (int r = 0; r < 16; ++r) p[r & 3] = fmaf(wr[r], relu(acc[r]), p[r & 3]);
+  const float v = (p[0] + p[1]) + (p[2] + p[3]);
   return v + __shfl_xor(v, 32);
 }
 
@@ -394,9 +410,167 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
   }
 }
 
+// Prefill variant (contiguous keys): one wave per (row, XCD). Workgroup b runs on XCD b mod 8,
+// and the wave of XCD x scores only the recalled pages p with p mod 8 == x, so each XCD's L2
+// holds one eighth of the keys instead of streaming all of them. A page's keys are one contiguous
+// block of P rows, copied into LDS 64 rows at a time by direct loads in which the 16-byte granules
+// of one key row go to consecutive lanes (a few cache lines per load instead of one line per
+// lane); granule c of row t is stored at slot c ^ swz(t) so that the operand reads are
+// conflict-free. The two 32-key tiles of a chunk run as two independent MFMA chains.
+// Output layout as fine_kernel.
+template <int D, bool FP8>
+__device__ __forceinline__ int fine_swz(int t) {
+  constexpr int RB = FP8 ? D : 2 * D;  // key row bytes
+  constexpr int GR = RB / 16;          // 16-byte granules per row
+  return RB >= 128 ? (t & 7) : ((t >> (7 - __builtin_ctz(RB))) & (GR - 1));
+}
+
+constexpr int kFineChunk = 64;  // key rows staged in LDS at a time
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 64 ? 4 : 3, 8))) void fine_xcd_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
+                                                      const float* __restrict__ w, const void* __restrict__ k,
+                                                      const float* __restrict__ kscale, const int32_t* __restrict__ pages,
+                                                      uint32_t* __restrict__ fine_keys, int64_t ldf) {
+  constexpr int KS = D / 16;          // MFMA k-steps
+  constexpr int RB = FP8 ? D : 2 * D;
+  constexpr int GR = RB / 16;
+  constexpr int LG = FP8 ? D / 32 : D / 16;  // 16-byte granules per lane per tile
+  __shared__ __attribute__((aligned(16))) uint8_t fsm[kFineChunk * RB];
+  __shared__ float lsc[kFineChunk];
+  const int lane = threadIdx.x, j = lane & 31, h = lane >> 5;
+  const int x = (int)(blockIdx.x & 7);
+  const int64_t row = (int64_t)(blockIdx.x >> 3);
+  if (row >= n_rows) return;
+  const RowInfo ri = row_info(g, row);
+  if (!ri.valid || ri.p_hi < ri.p_lo) return;
+  const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
+  const bool flat = g.M <= 0;
+  const int n_sel = (int)(flat ? n_elig : (n_elig < g.M ? n_elig : g.M));
+  const int P = g.P;
+
+  u32x4 a[KS];
+  float wr[16];
+  load_query_operand<D>(q, g.H, row, lane, a);
+  load_head_weights(w, g.H, row, lane, wr);
+  const uint8_t* kb = reinterpret_cast<const uint8_t*>(k);
+
+  auto widen = [&](const u32x4 (&raw)[LG], int s) -> u32x4 {
+    if (FP8) {
+      const u32x4 r = raw[s >> 1];
+      return (s & 1) ? fp8x8_to_bf16x8_pk(r.z, r.w) : fp8x8_to_bf16x8_pk(r.x, r.y);
+    }
+    return raw[s];
+  };
+
+  for (int base = 0; base < n_sel; base += 64) {
+    const int kk = base + lane;
+    const int64_t page = kk < n_sel ? (flat ? ri.p_lo + kk : (int64_t)pages[row * g.M + kk]) : -1;
+    uint64_t mine = __ballot(page >= 0 && (page & 7) == x);
+    while (mine) {
+      const int bit = __builtin_ctzll(mine);
+      mine &= mine - 1;
+      const int64_t pg = (int64_t)__shfl((int)page, bit);  // page ids fit in 31 bits (n_kv < 2^31)
+      if (pg < ri.p_lo || pg > ri.p_hi) continue;          // (recalled pages are always eligible)
+      uint32_t* dst = fine_keys + row * ldf + (int64_t)(base + bit) * P;
+      for (int c0 = 0; c0 < P; c0 += kFineChunk) {
+        const int nt = P - c0 < kFineChunk ? (P - c0) / 32 : kFineChunk / 32;  // 1 or 2 tiles
+        const int64_t r0 = pg * P + c0;
+        // ---- rows r0 .. r0 + 32 nt - 1 -> LDS (rows past the last cached key, possible in flat
+        // mode when K_swa < P, re-read the last key; their positions get no score)
+        for (int p0 = 0; p0 < 32 * nt * GR; p0 += 64) {
+          const int p = p0 + lane, t = p / GR, c = (p % GR) ^ fine_swz<D, FP8>(t);
+          const int64_t srow = r0 + t < g.n_kv ? r0 + t : g.n_kv - 1;
+          __builtin_amdgcn_global_load_lds(kb + srow * RB + c * 16, LSA_LDS(fsm + p0 * 16), 16, 0, 0);
+        }
+        if (FP8) {
+          const int64_t srow = r0 + lane < g.n_kv ? r0 + lane : g.n_kv - 1;
+          if (lane < 32 * nt) __builtin_amdgcn_global_load_lds(kscale + srow, LSA_LDS(lsc), 4, 0, 0);
+        }
+        vm_wait<0>();
+        // ---- both tiles' operands, then two independent MFMA chains
+        u32x4 raw0[LG], raw1[LG];
+        const int t0 = j, t1 = 32 + j;
+#pragma unroll
+        for (int v = 0; v < LG; ++v) {
+          raw0[v] = *reinterpret_cast<const u32x4*>(fsm + t0 * RB + (((LG * h + v) ^ fine_swz<D, FP8>(t0)) * 16));
+          raw1[v] = *reinterpret_cast<const u32x4*>(fsm + t1 * RB + (((LG * h + v) ^ fine_swz<D, FP8>(t1)) * 16));
+        }
+        const float sc0 = FP8 ? lsc[t0] : 1.f, sc1 = FP8 ? lsc[t1] : 1.f;
+        f32x16 acc0 = {}, acc1 = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          acc0 = mfma32(a[s], widen(raw0, s), acc0);
+          acc1 = mfma32(a[s], widen(raw1, s), acc1);
+        }
+        const int64_t pos0 = r0 + t0, pos1 = r0 + t1;
+        const float v0 = head_reduce(acc0, wr) * sc0;
+        const float v1 = head_reduce(acc1, wr) * sc1;
+        if (lane < 32) {
+          dst[c0 + t0] = (pos0 >= ri.lo && pos0 <= ri.hi) ? score_key(v0) : 0u;
+          if (nt == 2) dst[c0 + t1] = (pos1 >= ri.lo && pos1 <= ri.hi) ? score_key(v1) : 0u;
+        }
+        lds_done_barrier();  // this wave's reads are done before the next chunk overwrites the buffer
+      }
+    }
+  }
+}
+
 // ============================================================================ final top-K_sparse, merge, runs
+// Writes idx/count of one row from lidx[0..cnt) and, if requested, its runs: maximal stretches of
+// consecutive positions, also cut at multiples of C. rstart is LDS scratch of >= cnt entries.
+template <int NT>
+__device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, int cnt, int32_t* rstart, int* wsum,
+                         int32_t* __restrict__ idx, int32_t* __restrict__ count, int32_t* __restrict__ runs,
+                         int32_t* __restrict__ run_count) {
+  const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
+  int32_t* orow = idx + row * k_cap;
+  for (int i = threadIdx.x; i < k_cap; i += NT) orow[i] = i < cnt ? lidx[i] : -1;
+  if (threadIdx.x == 0) count[row] = cnt;
+  if (!runs) return;
+  // a run starts at i = 0, after a gap, or at a position divisible by C
+  const int C = g.C;
+  int base = 0;
+  for (int c = 0; c < cnt; c += NT) {
+    const int i = c + threadIdx.x;
+    bool st = false;
+    if (i < cnt) {
+      const int32_t s = lidx[i];
+      st = i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0;
+    }
+    const uint64_t bs = __ballot(st);
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    if (lane == 0) wsum[wv] = __popcll(bs);
+    __syncthreads();
+    int pre = 0, tot = 0;
+    for (int x = 0; x < NT / 64; ++x) {
+      const int v = wsum[x];
+      pre += x < wv ? v : 0;
+      tot += v;
+    }
+    if (st) rstart[base + pre + __popcll(bs & lanemask_lt())] = i;
+    base += tot;
+    __syncthreads();
+  }
+  const int nr = base;
+  int32_t* rrow = runs + row * (int64_t)k_cap * 2;
+  for (int r = threadIdx.x; r < k_cap; r += NT) {
+    if (r < nr) {
+      const int s = rstart[r];
+      const int e = r + 1 < nr ? rstart[r + 1] : cnt;
+      rrow[2 * r] = lidx[s];
+      rrow[2 * r + 1] = e - s;
+    } else {
+      rrow[2 * r] = -1;
+      rrow[2 * r + 1] = 0;
+    }
+  }
+  if (threadIdx.x == 0) run_count[row] = nr;
+}
+
 // Eq. (12) / Eq. (7) then Eq. (6): S_t = sink ++ (top K_sparse candidates, ascending) ++ window;
-// idx padded with -1; runs re-encode idx, cut at gaps and at multiples of C.
+// idx padded with -1; runs re-encode idx, cut at gaps and at multiples of C. General version:
+// the candidate keys are staged in LDS (any number that fits).
 template <int NT>
 __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ fine_keys,
                                                           int64_t ldf, const int32_t* __restrict__ pages,
@@ -445,50 +619,183 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
     cnt = g.k_sink + n_sp + g.k_swa;
   }
   __syncthreads();
-  int32_t* orow = idx + row * k_cap;
-  for (int i = threadIdx.x; i < k_cap; i += NT) orow[i] = i < cnt ? lidx[i] : -1;
-  if (threadIdx.x == 0) count[row] = cnt;
-  if (!runs) return;
+  emit_row<NT>(g, row, lidx, cnt, reinterpret_cast<int32_t*>(keys), wsum, idx, count, runs, run_count);
+}
 
-  // runs: a run starts at i = 0, after a gap, or at a position divisible by C
-  int32_t* rstart = reinterpret_cast<int32_t*>(keys);  // keys are dead now
-  const int C = g.C;
-  int base = 0;
-  for (int c = 0; c < cnt; c += NT) {
-    const int i = c + threadIdx.x;
-    bool st = false;
-    if (i < cnt) {
-      const int32_t s = lidx[i];
-      st = i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0;
-    }
-    const uint64_t bs = __ballot(st);
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    if (lane == 0) wsum[wv] = __popcll(bs);
-    __syncthreads();
-    int pre = 0, tot = 0;
-    for (int x = 0; x < NT / 64; ++x) {
-      const int v = wsum[x];
-      pre += x < wv ? v : 0;
-      tot += v;
-    }
-    if (st) rstart[base + pre + __popcll(bs & lanemask_lt())] = i;
-    base += tot;
-    __syncthreads();
+// Block-wide scans over NT threads of one 32-bit value each.
+// Exclusive prefix (sum over threads < t) and suffix (sum over threads > t); wtot is LDS [NT/64].
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t* wtot) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
   }
-  const int nr = base;
-  int32_t* rrow = runs + row * (int64_t)k_cap * 2;
-  for (int r = threadIdx.x; r < k_cap; r += NT) {
-    if (r < nr) {
-      const int s = rstart[r];
-      const int e = r + 1 < nr ? rstart[r + 1] : cnt;
-      rrow[2 * r] = lidx[s];
-      rrow[2 * r + 1] = e - s;
-    } else {
-      rrow[2 * r] = -1;
-      rrow[2 * r + 1] = 0;
-    }
+  if (lane == 63) wtot[wv] = inc;
+  __syncthreads();
+  uint32_t base = 0;
+#pragma unroll
+  for (int x = 0; x < NT / 64; ++x) base += x < wv ? wtot[x] : 0u;
+  __syncthreads();
+  return base + inc - v;
+}
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_suffix(uint32_t v, uint32_t* wtot) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_down(inc, o);
+    if (lane + o < 64) inc += t;
   }
-  if (threadIdx.x == 0) run_count[row] = nr;
+  if (lane == 0) wtot[wv] = inc;
+  __syncthreads();
+  uint32_t base = 0;
+#pragma unroll
+  for (int x = 0; x < NT / 64; ++x) base += x > wv ? wtot[x] : 0u;
+  __syncthreads();
+  return base + inc - v;
+}
+
+// One radix step over register-held keys: among keys with (key & mask) == prefix, find the digit
+// value d (BITS bits at SHIFT) such that fewer than rem keys have a larger digit and at least rem
+// have a digit >= d; then narrow prefix/mask to d and take the keys above it off rem.
+template <int NT, int KPT, int SHIFT, int BITS>
+__device__ __forceinline__ void radix_step(const uint32_t (&kv)[KPT], uint32_t& prefix, uint32_t& mask, int& rem,
+                                           uint32_t* hist, uint32_t* wtot, uint32_t* found) {
+  constexpr int NB = 1 << BITS;
+  constexpr int BPT = NB >= NT ? NB / NT : 1;  // bins per thread
+  for (int i = threadIdx.x; i < NB; i += NT) hist[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < KPT; ++e)
+    if ((kv[e] & mask) == prefix) atomicAdd(&hist[(kv[e] >> SHIFT) & (NB - 1)], 1u);
+  __syncthreads();
+  const int b0 = threadIdx.x * BPT;
+  uint32_t own = 0;
+  if (b0 < NB)
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) own += hist[b0 + u];
+  uint32_t above = block_excl_suffix<NT>(own, wtot);  // keys in the bins of higher threads
+  if (b0 < NB)
+#pragma unroll
+    for (int u = BPT - 1; u >= 0; --u) {
+      const uint32_t c = hist[b0 + u];
+      if (above < (uint32_t)rem && above + c >= (uint32_t)rem) {
+        found[0] = (uint32_t)(b0 + u);
+        found[1] = above;
+      }
+      above += c;
+    }
+  __syncthreads();
+  rem -= (int)found[1];
+  prefix |= found[0] << SHIFT;
+  mask |= (uint32_t)(NB - 1) << SHIFT;
+  __syncthreads();
+}
+
+// Same result as token_select_kernel for rows of at most NT * KPT candidates: each thread holds
+// KPT consecutive keys in registers. The threshold takes three radix steps of 12, 12 and 8 bits
+// (the first spreads the scores of one row over many bins, where an 8-bit exponent digit would
+// put nearly all of them into one or two and serialize the LDS atomics); the ordered compaction
+// is one block-wide scan of (count above T, count equal to T) per thread.
+template <int NT, int KPT>
+__global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64_t n_rows,
+                                                              const uint32_t* __restrict__ fine_keys, int64_t ldf,
+                                                              const int32_t* __restrict__ pages,
+                                                              int32_t* __restrict__ idx, int32_t* __restrict__ count,
+                                                              int32_t* __restrict__ runs, int32_t* __restrict__ run_count) {
+  extern __shared__ int32_t dyn[];  // lidx [k_cap], rstart [k_cap], lpages [M]
+  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t wtot[NT / 64 + 2];
+  __shared__ int wsum[NT / 64 + 2];
+  const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
+  int32_t* lidx = dyn;
+  int32_t* rstart = dyn + k_cap;
+  int32_t* lpages = dyn + 2 * k_cap;
+
+  const int64_t row = blockIdx.x;
+  const RowInfo ri = row_info(g, row);
+  int cnt = 0;
+  if (!ri.valid) {
+    cnt = 0;
+  } else if (ri.p_hi < ri.p_lo) {
+    cnt = (int)(ri.t + 1);  // sink and window cover [0, t]
+    for (int i = threadIdx.x; i < cnt; i += NT) lidx[i] = i;
+  } else {
+    const bool flat = g.M <= 0;
+    const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
+    const int n_sel = (int)(flat ? n_elig : (n_elig < g.M ? n_elig : g.M));
+    if (!flat)
+      for (int i = threadIdx.x; i < n_sel; i += NT) lpages[i] = pages[row * g.M + i];
+    const int n = n_sel * g.P;
+    const int i0 = (int)threadIdx.x * KPT;
+    uint32_t kv[KPT];
+    const uint32_t* src = fine_keys + row * ldf + i0;
+#pragma unroll
+    for (int e = 0; e < KPT; e += 4) {
+      if (i0 + e + 4 <= n) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(src + e);
+        kv[e] = v.x; kv[e + 1] = v.y; kv[e + 2] = v.z; kv[e + 3] = v.w;
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kv[e + u] = i0 + e + u < n ? src[e + u] : 0u;
+      }
+    }
+    uint32_t nz = 0;
+#pragma unroll
+    for (int e = 0; e < KPT; ++e) nz += kv[e] != 0u;
+    const uint32_t n_valid = block_excl_prefix<NT>(nz, wtot) + nz;  // valid for the last thread only
+    __shared__ uint32_t found[2];
+    if (threadIdx.x == NT - 1) found[0] = n_valid;
+    __syncthreads();
+    const int nv = (int)found[0];
+    __syncthreads();
+    uint32_t T = 0;
+    int take = 0;
+    if (nv > g.k_sparse) {
+      uint32_t prefix = 0, mask = 0;
+      int rem = g.k_sparse;
+      radix_step<NT, KPT, 20, 12>(kv, prefix, mask, rem, hist, wtot, found);
+      radix_step<NT, KPT, 8, 12>(kv, prefix, mask, rem, hist, wtot, found);
+      radix_step<NT, KPT, 0, 8>(kv, prefix, mask, rem, hist, wtot, found);
+      T = prefix;
+      take = rem;
+    }
+    // ordered compaction: selected = key > T, or key == T among the first `take` such (index order)
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int e = 0; e < KPT; ++e) {
+      gt += kv[e] > T;
+      eq += kv[e] == T && kv[e] != 0u;
+    }
+    const uint32_t pre = block_excl_prefix<NT>(gt | (eq << 16), wtot);
+    const int eq_before = (int)(pre >> 16);
+    int out = (int)(pre & 0xFFFFu) + (eq_before < take ? eq_before : take);
+    int eqr = eq_before;
+    const int P = g.P, ks = g.k_sink;
+#pragma unroll
+    for (int e = 0; e < KPT; ++e) {
+      const uint32_t key = kv[e];
+      const bool is_eq = key == T && key != 0u;
+      const bool sel = key > T || (is_eq && eqr < take);
+      eqr += is_eq;
+      if (sel) {
+        const int i = i0 + e;
+        const int64_t page = flat ? ri.p_lo + i / P : (int64_t)lpages[i / P];
+        lidx[ks + out] = (int32_t)(page * P + i % P);
+        ++out;
+      }
+    }
+    const int n_sp = nv > g.k_sparse ? g.k_sparse : nv;
+    for (int i = threadIdx.x; i < g.k_sink; i += NT) lidx[i] = i;
+    for (int i = threadIdx.x; i < g.k_swa; i += NT) lidx[g.k_sink + n_sp + i] = (int32_t)(ri.t - g.k_swa + 1 + i);
+    cnt = g.k_sink + n_sp + g.k_swa;
+  }
+  __syncthreads();
+  emit_row<NT>(g, row, lidx, cnt, rstart, wsum, idx, count, runs, run_count);
 }
 
 // ============================================================================ host launchers
@@ -549,10 +856,27 @@ static hipError_t launch_fine_t(const IndexGeom& g, int64_t n_rows, const uint16
   return hipGetLastError();
 }
 
+template <int D, bool FP8>
+static hipError_t launch_fine_xcd_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
+                                    const void* k, const float* ks, const int32_t* pages, uint32_t* fine_keys,
+                                    int64_t ldf, hipStream_t st) {
+  if (n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL((fine_xcd_kernel<D, FP8>), dim3((unsigned)(n_rows * 8)), dim3(64), 0, st, g, n_rows, q, w, k, ks,
+                     pages, fine_keys, ldf);
+  return hipGetLastError();
+}
+
 hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
                        const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
                        hipStream_t st) {
   const bool paged = g.ctx_len != nullptr, fp8 = g.fp8 != 0;
+  if (!paged) {
+    if (max_sel <= 0) return hipSuccess;
+    if (g.D == 128) return fp8 ? launch_fine_xcd_t<128, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st)
+                               : launch_fine_xcd_t<128, false>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st);
+    return fp8 ? launch_fine_xcd_t<64, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st)
+               : launch_fine_xcd_t<64, false>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st);
+  }
 #define LSA_FINE(D_, F_, P_) return launch_fine_t<D_, F_, P_>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
   if (g.D == 128) {
     if (fp8) { if (paged) LSA_FINE(128, true, true); else LSA_FINE(128, true, false); }
@@ -565,6 +889,7 @@ hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, co
 }
 
 size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M) {
+  if (slots_cap <= kSelectRegMax) return (size_t)(2 * k_cap + (M > 0 ? M : 0)) * 4;  // register-held keys
   const int64_t a = slots_cap > k_cap ? slots_cap : k_cap;
   return (size_t)(a + k_cap + (M > 0 ? M : 0)) * 4;
 }
@@ -575,8 +900,19 @@ hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_
   if (n_rows == 0) return hipSuccess;
   const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
   const size_t lds = token_select_lds_bytes(slots_cap, k_cap, g.M);
-  hipLaunchKernelGGL(token_select_kernel<512>, dim3((unsigned)n_rows), dim3(512), lds, st, g, n_rows, fine_keys, ldf,
-                     pages, idx, count, runs, run_count, (int)slots_cap);
+  const dim3 grid((unsigned)n_rows), block(512);
+  if (slots_cap <= 512 * 16)
+    hipLaunchKernelGGL((token_select_reg_kernel<512, 16>), grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx,
+                       count, runs, run_count);
+  else if (slots_cap <= 512 * 32)
+    hipLaunchKernelGGL((token_select_reg_kernel<512, 32>), grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx,
+                       count, runs, run_count);
+  else if (slots_cap <= kSelectRegMax)
+    hipLaunchKernelGGL((token_select_reg_kernel<512, 64>), grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx,
+                       count, runs, run_count);
+  else
+    hipLaunchKernelGGL(token_select_kernel<512>, grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx, count,
+                       runs, run_count, (int)slots_cap);
   return hipGetLastError();
 }
 
@@ -589,10 +925,15 @@ hipError_t prepare_index_kernels() {
   if (e != hipSuccess) return e;
   if (dev >= 0 && dev < 64 && done[dev]) return hipSuccess;
   const int lim = 160 * 1024 - 4096;
-  e = hipFuncSetAttribute((const void*)token_select_kernel<512>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
-  if (e != hipSuccess) return e;
+  const void* sel[] = {(const void*)token_select_kernel<512>, (const void*)token_select_reg_kernel<512, 16>,
+                       (const void*)token_select_reg_kernel<512, 32>, (const void*)token_select_reg_kernel<512, 64>};
+  for (const void* f : sel) {  // (the register-key kernels have 20 KB of static LDS, the other 4 KB)
+    e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, f == sel[0] ? lim : lim - 16 * 1024);
+    if (e != hipSuccess) return e;
+  }
   e = hipFuncSetAttribute((const void*)page_select_kernel<256>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
   if (e != hipSuccess) return e;
+
   if (dev >= 0 && dev < 64) done[dev] = true;
   return hipSuccess;
 }

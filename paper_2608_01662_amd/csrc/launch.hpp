@@ -29,7 +29,11 @@ hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t
 hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
                        const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
                        hipStream_t st);
+// Dynamic LDS bytes of the token selection; rows of up to kSelectRegMax candidates keep their keys
+// in registers (20 KB of static LDS), larger ones stage them in LDS (4 KB of static LDS).
+constexpr int64_t kSelectRegMax = 512 * 64;
 size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M);
+inline size_t token_select_static_lds(int64_t slots_cap) { return slots_cap <= kSelectRegMax ? 20 * 1024 : 4 * 1024; }
 hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_t* fine_keys, int64_t ldf,
                                const int32_t* pages, int32_t* idx, int32_t* count, int32_t* runs, int32_t* run_count,
                                int64_t slots_cap, hipStream_t st);

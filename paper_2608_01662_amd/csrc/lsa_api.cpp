@@ -87,7 +87,7 @@ IndexPlan plan_index(const lsa_index_params* p, int64_t n_rows, int64_t max_kv) 
 lsa_status check_lds(const lsa_index_params* p, const IndexPlan& pl) {
   const int k_cap = p->k_sink + p->k_swa + p->k_sparse;
   const size_t ts = lsa::token_select_lds_bytes(pl.slots, k_cap, p->keep_pages);
-  LSA_REQUIRE(ts + kSelectStaticLds <= kMaxLds, LSA_ERR_UNSUPPORTED,
+  LSA_REQUIRE(ts + lsa::token_select_static_lds(pl.slots) <= kMaxLds, LSA_ERR_UNSUPPORTED,
               "candidate slots (%lld) plus k_cap (%d) exceed the LDS of one workgroup; lower keep_pages*page",
               (long long)pl.slots, k_cap);
   if (p->keep_pages > 0)
@@ -257,6 +257,7 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
   LSA_REQUIRE(q_start + n_q <= n_kv, LSA_ERR_INVALID_ARG, "q_start + n_q = %lld exceeds n_kv = %lld",
               (long long)(q_start + n_q), (long long)n_kv);
   LSA_REQUIRE(n_kv < (1LL << 31), LSA_ERR_UNSUPPORTED, "n_kv must be < 2^31 (int32 positions)");
+  LSA_REQUIRE(n_q < (1LL << 28), LSA_ERR_UNSUPPORTED, "n_q must be < 2^28 per call (chunk longer prefills)");
   LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
   LSA_REQUIRE(aligned(pages_out, 4), LSA_ERR_INVALID_ARG, "pages_out must be 4-byte aligned");
   const IndexPlan pl = plan_index(p, n_q, n_kv);

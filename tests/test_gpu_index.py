@@ -122,6 +122,41 @@ def test_designed_inputs_select_latest():
             assert np.array_equal(S[w.k_sink:S.size - w.k_swa], want), (mode, t)
 
 
+def test_fine_scoring_orders_every_fp8_code():
+    """The fine stage widens fp8 keys to bf16 on the GPU. Designed case: each eligible token carries
+    one distinct e4m3fn code in component 0 (all 254 non-NaN codes, in seeded random positions),
+    every head's query is +e_0 and the scales are 1, so a token's score is H * ReLU(code value).
+    Sweeping K_sparse over 1..126 (the positive codes) makes the selected set at every threshold
+    the K largest decoded values: a code decoded wrongly (or a flushed denormal) changes the set."""
+    from dataclasses import replace
+    w0 = replace(W.L2K_MQA, fp8=True, keep_pages=0)
+    d, H = w0.head_dim, w0.n_heads
+    n_elig = 256
+    n_kv = w0.k_sink + n_elig + w0.k_swa
+    t = n_kv - 1
+    codes = np.arange(256, dtype=np.int64)
+    codes = codes[(codes & 0x7F) != 0x7F]
+    codes = np.concatenate([codes, [0, 0x80]]).astype(np.uint8)
+    codes = np.random.default_rng(7).permutation(codes)
+    k8 = np.zeros((n_kv, d), np.uint8)
+    k8[w0.k_sink:w0.k_sink + n_elig, 0] = codes
+    vals = orc.e4m3fn_to_f64(codes)
+    order = np.lexsort((np.arange(n_elig), -vals))        # value desc, position asc
+    q = np.zeros((1, H, d), np.float32)
+    q[:, :, 0] = 1.0
+    qd, wd = P.bf16_dev(synth.to_bf16_bits(q)), P.to_dev(np.ones((1, H), np.float32))
+    kd, ksd = P.to_dev(k8), P.to_dev(np.ones(n_kv, np.float32))
+    n_pos = int((vals > 0).sum())
+    assert n_pos == 126
+    for K in range(1, n_pos + 1):
+        prm = replace(w0, k_sparse=K).index_params()
+        out = lsa.index_prefill(prm, qd, wd, kd, ksd, None, t, n_kv=n_kv, runs=False)
+        S = out["idx"][0][: int(out["count"][0])].cpu().numpy()
+        sparse = S[w0.k_sink:S.size - w0.k_swa]
+        want = np.sort(order[:K] + w0.k_sink)
+        assert np.array_equal(sparse, want), K
+
+
 def test_chunked_equals_single_call():
     """Rows of a chunked prefill equal the same rows of one call over the whole sequence."""
     w = W.SMALL_CHUNKED
