@@ -89,6 +89,23 @@ def test_index_prefill_parity(w):
     print(w.name, stats)
 
 
+@pytest.mark.parametrize("base", [W.SMALL_FLAT, W.SMALL_MLA], ids=lambda w: w.name)
+def test_flat_short_window_partial_page(base):
+    """Flat mode with K_swa < P and a cache that ends inside a page: the page holding a row's last
+    eligible positions also holds positions past the cache, whose key rows the fine stage stages
+    (re-reading the last cached key) but never scores. Every row against the oracle."""
+    from dataclasses import replace
+    w = replace(base, keep_pages=0, k_swa=16, k_sparse=192, seq_len=1000)
+    assert w.k_swa < w.page and w.seq_len % w.page != 0
+    inp = P.prefill_inputs(w)
+    out, _ = _run_prefill(w, inp, pages=False)
+    rows = list(range(w.seq_len))
+    res = _oracle_rows(w, inp, rows)
+    stats = P.check_index_rows(w, rows, out["idx"], out["count"], None, res)
+    P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
+    print(w.name, stats)
+
+
 def test_keep_all_equals_flat_on_gpu():
     """With M >= #pages the hierarchical kernels must return exactly the flat selection."""
     w = W.SMALL_MLA
