@@ -15,6 +15,8 @@ Hierarchical Cross-Layer Indexing" (arXiv 2608.01662):
     sparse part chosen by top-K_sparse over positions outside sink and window.
   * Sec. 3.3, Eq. (9)-(12): hierarchical indexing: per-sub-block mean keys, coarse page score,
     top-M pages, fine token score over the recalled pages, final top-K_sparse.
+  * Eq. (13), the pooling ablation of hierarchical indexing: min-max pooling, a block score from
+    the per-dimension extrema of the sub-block's keys in place of the mean-key dot product.
   * Sec. 3.2 and Sec. 4.1: cross-layer indexing has nothing to compute: the owner layer's S_t is
     passed unchanged to every layer of the group.
 
@@ -30,7 +32,8 @@ Readings taken where the paper is silent or 1-based:
   * the coarse stage scores only pages holding at least one eligible token; other pages could
     contribute no candidate (Eq. 7 excludes sink and window).
   * the mean keys are the per-dimension mean of the dequantised keys of a sub-block, stored
-    in bfloat16 with one round-to-nearest-even (the paper keeps them "in a cache").
+    in bfloat16 with one round-to-nearest-even (Stage 1 caches them); the
+    extrema of min-max pooling are stored the same way.
   * both top-K operations order by (score descending, position ascending).
   * fp8 keys are OCP e4m3fn codes times a per-token fp32 scale.
   * runs re-encode S_t: maximal stretches of consecutive positions, cut at multiples of C; the
@@ -123,6 +126,7 @@ class IndexParams:
     k_sink: int          # K_sink
     k_swa: int           # K_swa
     run_align: int       # C, runs never cross a multiple of C
+    pooling: str = "mean"  # coarse-stage block summary: "mean" (Eq. 9) or "minmax" (Eq. 13)
 
     @property
     def k_cap(self) -> int:
@@ -153,6 +157,22 @@ def sub_block_mean_keys(k_hat, sub_block: int) -> np.ndarray:
     return bf16_bits_to_f64(f64_to_bf16_bits(means))
 
 
+def sub_block_minmax_keys(k_hat, sub_block: int):
+    """Eq. (13) (the pooling ablation of hierarchical indexing): per-dimension maximum and minimum
+    of the keys of each sub-block.
+
+    Only complete sub-blocks are formed; like the mean keys they are stored in bfloat16, each
+    extremum rounded once (rounding is monotone, so k_min <= k_max survives it).
+    k_hat [n_tok, d] float64 -> (k_max, k_min), each [n_tok // B, d] float64.
+    """
+    k_hat = np.asarray(k_hat, np.float64)
+    n_sub = k_hat.shape[0] // sub_block
+    blocks = k_hat[: n_sub * sub_block].reshape(n_sub, sub_block, -1)
+    k_max = bf16_bits_to_f64(f64_to_bf16_bits(blocks.max(axis=1)))
+    k_min = bf16_bits_to_f64(f64_to_bf16_bits(blocks.min(axis=1)))
+    return k_max, k_min
+
+
 def streaming_sets(t: int, prm: IndexParams):
     """Eq. (6): the fixed parts of S_t and the range left to the indexer (Eq. 7).
 
@@ -175,6 +195,22 @@ def page_scores(q_t, w_t, k_mean, pages, prm: IndexParams) -> np.ndarray:
     sub = (pages[:, None] * per_page + np.arange(per_page)[None, :]).reshape(-1)
     dots = np.asarray(q_t, np.float64) @ k_mean[sub].T                       # [H_I, n_pages*per_page]
     relu = np.maximum(dots, 0.0).reshape(dots.shape[0], len(pages), per_page).sum(axis=2)
+    return np.asarray(w_t, np.float64) @ relu                                 # [n_pages]
+
+
+def page_scores_minmax(q_t, w_t, k_max, k_min, pages, prm: IndexParams) -> np.ndarray:
+    """Eq. (13) in the coarse score: per head j and sub-block n,
+    s~_{t,n,j} = sum_d max(q_{t,j,d} k^max_{n,d}, q_{t,j,d} k^min_{n,d}), then
+    I^page_{t,p} = sum_j w_{t,j} sum_{n in page p} ReLU(s~_{t,n,j}).
+    """
+    per_page = prm.page // prm.sub_block
+    pages = np.asarray(pages, np.int64)
+    sub = (pages[:, None] * per_page + np.arange(per_page)[None, :]).reshape(-1)
+    q = np.asarray(q_t, np.float64)                                          # [H_I, d]
+    hi = q[:, None, :] * np.asarray(k_max, np.float64)[sub][None, :, :]       # [H_I, n, d]
+    lo = q[:, None, :] * np.asarray(k_min, np.float64)[sub][None, :, :]
+    s_tilde = np.maximum(hi, lo).sum(axis=2)                                 # [H_I, n]
+    relu = np.maximum(s_tilde, 0.0).reshape(q.shape[0], len(pages), per_page).sum(axis=2)
     return np.asarray(w_t, np.float64) @ relu                                 # [n_pages]
 
 
@@ -221,7 +257,8 @@ def index_row(t: int, q_t, w_t, k_hat, k_mean, prm: IndexParams, pages_override=
     """One query row of the LSA indexer: S_t and the intermediate quantities.
 
     t: 0-based position of the query; q_t [H_I, d]; w_t [H_I]; k_hat [>= t+1, d] float64 keys;
-    k_mean: sub-block mean keys (Stage 1 cache), unused in flat mode.
+    k_mean: the Stage 1 block cache, unused in flat mode: the sub-block mean keys (Eq. 9), or
+    with prm.pooling == "minmax" the pair (k_max, k_min) of sub_block_minmax_keys (Eq. 13).
     pages_override: run Eq. (11)-(12) on this page list instead of the coarse stage's own
     choice (used to check the fine stage on the pages another implementation recalled).
 
@@ -242,8 +279,11 @@ def index_row(t: int, q_t, w_t, k_hat, k_mean, prm: IndexParams, pages_override=
     lo, hi = elig
     all_pages = eligible_pages(lo, hi, prm)
     if prm.keep_pages > 0:
-        # Stage 1: coarse page score (Eq. 9) and top-M pages (Eq. 10)
-        ps = page_scores(q_t, w_t, k_mean, all_pages, prm)
+        # Stage 1: coarse page score (Eq. 9, or Eq. 13 with min-max pooling) and top-M pages (Eq. 10)
+        if prm.pooling == "minmax":
+            ps = page_scores_minmax(q_t, w_t, k_mean[0], k_mean[1], all_pages, prm)
+        else:
+            ps = page_scores(q_t, w_t, k_mean, all_pages, prm)
         out["page_ids"], out["page_score"] = all_pages, ps
         pages = arg_top(ps, all_pages, prm.keep_pages)
         if pages_override is not None:

@@ -296,6 +296,62 @@ def pin_homogeneity(orc):
         assert np.array_equal(base, orc.index_row(t, q, w, 4 * k_hat, km4, prm)["S"])
 
 
+def pin_minmax_keys(orc):
+    """Eq. (13) extrema: on bf16-exact keys every key of a sub-block lies inside [k_min, k_max]
+    coordinate-wise, and each bound is attained by one of its keys (brute force over the block)."""
+    g = np.random.default_rng(16)
+    B, n, d = 4, 22, 5
+    k = g.integers(-255, 256, size=(n, d)).astype(np.float64) / 256.0       # bf16-exact
+    k_max, k_min = orc.sub_block_minmax_keys(k, B)
+    assert k_max.shape == (n // B, d) and k_min.shape == (n // B, d)
+    for b in range(n // B):
+        blk = k[b * B:(b + 1) * B]
+        for c in range(d):
+            col = [float(x) for x in blk[:, c]]
+            assert k_max[b, c] == max(col) and k_min[b, c] == min(col), (b, c)
+    # B = 1: both extrema are the (rounded) key itself
+    one_max, one_min = orc.sub_block_minmax_keys(k, 1)
+    assert np.array_equal(one_max, k) and np.array_equal(one_min, k)
+
+
+def pin_minmax_score_is_box_support(orc):
+    """Eq. (13) is the largest value of q . x over the box [k_min, k_max]: brute force over the
+    2^d corners (d = 4), one head, one sub-block per page, so the page score is ReLU of it times
+    the head weight; the box bound is at least every member token's score."""
+    g = np.random.default_rng(17)
+    prm = _prm(orc, page=4, sub_block=4, pooling="minmax")
+    for _ in range(40):
+        k = g.integers(-64, 64, size=(4, 4)).astype(np.float64) / 32.0
+        k_max, k_min = orc.sub_block_minmax_keys(k, 4)
+        q = g.standard_normal((1, 4))
+        w = g.random(1) + 0.5
+        best = max(float(q[0] @ np.where(np.array(bits) == 1, k_max[0], k_min[0]))
+                   for bits in itertools.product((0, 1), repeat=4))
+        got = orc.page_scores_minmax(q, w, k_max, k_min, np.arange(1), prm)
+        assert np.isclose(got[0], w[0] * max(best, 0.0), rtol=1e-13, atol=1e-15)
+        assert best >= float((k @ q[0]).max()) - 1e-12          # upper bound of the block's tokens
+
+
+def pin_minmax_reduces_to_mean_pooling(orc):
+    """With B = 1 the box is a point: Eq. (13) becomes q . k and the min-max page score equals the
+    mean-pooled one (Eq. 9), for several heads and sub-blocks per page; and the whole indexer row
+    then selects the same set under either pooling."""
+    g = np.random.default_rng(18)
+    q, w = g.standard_normal((3, 5)), g.random(3)
+    k = g.integers(-200, 200, size=(32, 5)).astype(np.float64) / 128.0
+    prm_mean = _prm(orc, page=8, sub_block=1)
+    prm_mm = _prm(orc, page=8, sub_block=1, pooling="minmax")
+    km = orc.sub_block_mean_keys(k, 1)
+    kx, kn = orc.sub_block_minmax_keys(k, 1)
+    a = orc.page_scores(q, w, km, np.arange(4), prm_mean)
+    b = orc.page_scores_minmax(q, w, kx, kn, np.arange(4), prm_mm)
+    assert np.allclose(a, b, rtol=1e-13, atol=1e-13)
+    hm = _prm(orc, page=8, sub_block=1, keep_pages=2, k_sparse=4, k_sink=2, k_swa=8)
+    hx = _prm(orc, page=8, sub_block=1, keep_pages=2, k_sparse=4, k_sink=2, k_swa=8, pooling="minmax")
+    for t in range(12, 32):
+        assert np.array_equal(orc.index_row(t, q, w, k, km, hm)["S"], orc.index_row(t, q, w, k, (kx, kn), hx)["S"])
+
+
 # ----------------------------------------------------------------------------- runs
 def pin_runs(orc):
     S = [0, 1, 2, 3, 5, 6, 62, 63, 64, 65, 127, 128]

@@ -85,6 +85,20 @@ def _page_score_unweighted(q_t, w_t, k_mean, pages, prm):
     return orc.__dict__["_orig_page"](q_t, np.ones_like(np.asarray(w_t)), k_mean, pages, prm)
 
 
+def _minmax_min_of_products(q_t, w_t, k_max, k_min, pages, prm):
+    per_page = prm.page // prm.sub_block
+    sub = (np.asarray(pages)[:, None] * per_page + np.arange(per_page)[None, :]).reshape(-1)
+    q = np.asarray(q_t, np.float64)
+    s = np.minimum(q[:, None, :] * k_max[sub][None], q[:, None, :] * k_min[sub][None]).sum(axis=2)
+    relu = np.maximum(s, 0.0).reshape(q.shape[0], len(pages), per_page).sum(axis=2)
+    return np.asarray(w_t) @ relu
+
+
+def _minmax_keys_swapped(k_hat, sub_block):
+    k_max, k_min = orc.__dict__["_orig_minmax"](k_hat, sub_block)
+    return k_min, k_max
+
+
 def _pages_shifted(lo, hi, prm):
     return np.arange(lo // prm.page, hi // prm.page)
 
@@ -103,6 +117,8 @@ MUTANTS = {
     "lse_in_log2": ("sparse_attention_row", _attn_log2),
     "page_score_ignores_w": ("page_scores", _page_score_unweighted),
     "last_eligible_page_dropped": ("eligible_pages", _pages_shifted),
+    "minmax_min_of_products": ("page_scores_minmax", _minmax_min_of_products),
+    "minmax_extrema_swapped": ("sub_block_minmax_keys", _minmax_keys_swapped),
 }
 
 
@@ -110,6 +126,7 @@ MUTANTS = {
 def test_mutant_is_caught(name, monkeypatch):
     monkeypatch.setitem(orc.__dict__, "_orig_attn", orc.sparse_attention_row)
     monkeypatch.setitem(orc.__dict__, "_orig_page", orc.page_scores)
+    monkeypatch.setitem(orc.__dict__, "_orig_minmax", orc.sub_block_minmax_keys)
     attr, fn = MUTANTS[name]
     monkeypatch.setattr(orc, attr, fn)
     failed = []
