@@ -2,7 +2,7 @@
 """Benchmark of the LSA hot path on one MI355X.
 
 One step = the whole hot path over one synthetic single-sequence prefill of L = 131072 tokens:
-mean-key cache (lsa_block_means), hierarchical indexer with streaming merge and runs
+block cache (lsa_block_means, or lsa_block_minmax with --pooling minmax), hierarchical indexer with streaming merge and runs
 (lsa_index_prefill), then sparse attention for the 4 layers of one cross-layer group, all reading
 the same index list (lsa_sparse_attn x 4). Inputs are resident in HBM before timing starts.
 
@@ -121,10 +121,13 @@ def cpu_baseline(w, t, seconds):
     KVb = [kv.view(torch.int16).cpu().numpy().view(np.uint16) for kv in t["KV"]]
     Vb = [None if v is None else v.view(torch.int16).cpu().numpy().view(np.uint16) for v in t["V"]]
     prm = orc.IndexParams(page=w.page, sub_block=w.sub_block, keep_pages=w.keep_pages, k_sparse=w.k_sparse,
-                          k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align)
+                          k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align, pooling=w.pooling)
     t0 = time.perf_counter()
     k_hat = orc.dequantized_keys(kb, ks)
-    k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block)
+    if w.pooling == "minmax":
+        k_mean = orc.sub_block_minmax_keys(k_hat, w.sub_block)
+    else:
+        k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block)
     t_once = time.perf_counter() - t0
     done = 0
     t1 = time.perf_counter()
@@ -139,7 +142,7 @@ def cpu_baseline(w, t, seconds):
     full = t_once + n * per_row
     return {"value": n / full, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": (f"{done} query rows at random positions in [K_cap, L) through the indexer and "
-                       f"{w.layers} attention layers, plus the one-off key decode and mean keys "
+                       f"{w.layers} attention layers, plus the one-off key decode and block cache "
                        f"({t_once:.2f} s); tokens/s extrapolated to all {n} rows "
                        f"({per_row * 1e3:.1f} ms per row)")}
 
@@ -150,6 +153,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL if not w.decode and not w.chunk])
+    ap.add_argument("--pooling", default="mean", choices=["mean", "minmax"],
+                    help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -168,12 +173,15 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = W.BY_NAME[args.workload]
+    if args.pooling != w.pooling:
+        from dataclasses import replace
+        w = replace(w, name=f"{w.name}_{args.pooling}", pooling=args.pooling)
     n = w.seq_len
     H, dqk, dv = w.attn_dims
     prm, aprm = w.index_params(), w.attn_params()
     log(f"[bench] {w.name}: generating inputs on {torch.cuda.get_device_name(dev)}")
     t = make_inputs(w, dev)
-    bk = torch.empty((n // w.sub_block, w.head_dim), dtype=torch.bfloat16, device=dev)
+    bk = torch.empty((n // w.sub_block, prm.block_width), dtype=torch.bfloat16, device=dev)
     out = dict(idx=torch.empty((n, w.k_cap), dtype=torch.int32, device=dev),
                count=torch.empty((n,), dtype=torch.int32, device=dev),
                runs=torch.empty((n, w.k_cap, 2), dtype=torch.int32, device=dev),
@@ -189,7 +197,7 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        lsa.block_means(prm, t["kI"], t["ks"], out=bk)
+        lsa.block_keys(prm, t["kI"], t["ks"], out=bk)
         if ev is not None:
             ev[1].record()
         lsa.index_prefill(prm, t["qI"], t["wI"], t["kI"], t["ks"], bk, 0, n_kv=n, runs=True,
@@ -220,7 +228,7 @@ def main():
     idx_ms = np.mean([e[1].elapsed_time(e[2]) for e in events])
     attn_ms = [np.mean([e[2 + l].elapsed_time(e[3 + l]) for e in events]) for l in range(w.layers)]
     attn_avg = float(np.mean(attn_ms))
-    log(f"[bench] {args.steps} steps: {ms_per_step:.2f} ms/step (block means {bm_ms:.3f}, index {idx_ms:.2f}, "
+    log(f"[bench] {args.steps} steps: {ms_per_step:.2f} ms/step (block cache {bm_ms:.3f}, index {idx_ms:.2f}, "
         f"attention per layer {attn_avg:.2f} ms)")
 
     # ---- algorithmic work (per launch / per step)
@@ -235,7 +243,8 @@ def main():
     n_elig_pages = np.where(hi >= w.k_sink, hi // w.page - w.k_sink // w.page + 1, 0)
     cand = np.where(hi >= w.k_sink, np.minimum(n_elig_pages, w.keep_pages) * w.page, 0)
     sub_per_page = w.page // w.sub_block
-    idx_flops = 2.0 * w.n_heads * w.head_dim * (float(n_elig_pages.sum()) * sub_per_page + float(cand.sum()))
+    coarse_dim = prm.block_width      # min-max pooling scores [q+ | q-] . [k_max | k_min]
+    idx_flops = 2.0 * w.n_heads * (coarse_dim * float(n_elig_pages.sum()) * sub_per_page + w.head_dim * float(cand.sum()))
     attn_gbs = attn_bytes / (attn_avg * 1e-3) / 1e9
     res = {
         "metric": "LSA prefill tokens/s at L=128K (indexer+attn)",
@@ -254,13 +263,13 @@ def main():
                    "indexer": {"heads": w.n_heads, "head_dim": w.head_dim, "keys": "fp8_e4m3fn" if w.fp8 else "bf16",
                                "page": w.page, "sub_block": w.sub_block, "keep_pages": w.keep_pages,
                                "k_sparse": w.k_sparse, "k_sink": w.k_sink, "k_swa": w.k_swa,
-                               "run_align": w.run_align},
+                               "run_align": w.run_align, "pooling": w.pooling},
                    "attention": {"kind": w.attn, "heads": H, "d_qk": dqk, "d_v": dv}},
         "roofline": {"kernel": "mla_attn_kernel", "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_avg},
         "breakdown": {
-            "block_means_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,
+            "block_cache_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,
             "indexer_scoring_tflops": idx_flops / (idx_ms * 1e-3) / 1e12,
             "indexer_mfma_frac": idx_flops / (idx_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
             "attn_tflops": attn_flops / (attn_avg * 1e-3) / 1e12,

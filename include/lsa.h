@@ -50,6 +50,11 @@ typedef enum lsa_key_dtype {
   LSA_KEY_FP8_E4M3FN = 1   /* indexer keys in fp8 with one fp32 scale per token (k = s * k8) */
 } lsa_key_dtype;
 
+/* Block summary of the coarse stage (Stage 1 of Sec. 3.3). */
+typedef enum lsa_pooling {
+  LSA_POOL_MEAN = 0,       /* one mean key per sub-block; block score q . k_mean (Eq. 9)        */
+  LSA_POOL_MINMAX = 1      /* per-dimension extrema per sub-block; block score of Eq. 13          */
+} lsa_pooling;
 /* Hyper-parameters of one LSA indexer (Sec. 3.1 and Sec. 3.3). */
 typedef struct lsa_index_params {
   int32_t n_heads;     /* H^I, indexer heads sharing one key (Eq. 1). 1..32                     */
@@ -64,6 +69,7 @@ typedef struct lsa_index_params {
   int32_t k_swa;       /* K_swa (Eq. 6); must be >= P when keep_pages > 0, so that every scored
                           page lies entirely at or before the query                              */
   int32_t run_align;   /* C: runs are cut at every multiple of C (>= 1)                           */
+  int32_t pooling;     /* lsa_pooling of the coarse stage (hierarchical mode only)               */
 } lsa_index_params;
 
 /* A run of consecutive selected positions [start, start+len) inside one C-aligned chunk. */
@@ -92,6 +98,28 @@ size_t lsa_index_workspace_size(const lsa_index_params* p, int64_t n_rows, int64
  */
 lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void* k,
                            const float* k_scale, void* block_keys, void* stream);
+/*
+ * Min-max block cache (Eq. 13, the pooling ablation of hierarchical indexing): for sub-block n,
+ * block_keys[n] = [k_max | k_min], the per-dimension maximum and minimum of the dequantised keys
+ * s_i * k_i of tokens [n*B, n*B+B). Each extremum is taken exactly (products in fp64) and rounded
+ * once to bf16, nearest-even. Arguments as lsa_block_means, except
+ *   block_keys [n_tok / B, 2 * d_I] bf16 output.
+ */
+lsa_status lsa_block_minmax(const lsa_index_params* p, int64_t n_tok, const void* k,
+                            const float* k_scale, void* block_keys, void* stream);
+/*
+ * Keeps a block cache current while tokens are appended (decode): recomputes, from the keys in
+ * the cache, the summary of every sub-block that contains one of the n_rows token rows in `rows`
+ * (mean keys as lsa_block_means, or [k_max | k_min] as lsa_block_minmax, by p->pooling). The
+ * result is bit-identical to recomputing the whole cache.
+ *   rows       [n_rows] int64 device array of token rows (physical rows of a paged pool); rows
+ *              outside [0, n_tok) or in the incomplete trailing sub-block are skipped. A row may
+ *              repeat; every copy writes the same value.
+ *   n_tok, k, k_scale, block_keys as in lsa_block_means / lsa_block_minmax.
+ */
+lsa_status lsa_block_keys_update(const lsa_index_params* p, int64_t n_rows, const int64_t* rows,
+                                 int64_t n_tok, const void* k, const float* k_scale,
+                                 void* block_keys, void* stream);
 
 /*
  * Indexer for prefill (Eq. 6-7, 9-12): query rows i = 0..n_q-1 at positions t = q_start + i of
@@ -100,7 +128,9 @@ lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void*
  *   q          [n_q, H^I, d_I] bf16 indexer queries
  *   w          [n_q, H^I] fp32 head weights (any sign)
  *   k, k_scale [n_kv, d_I] keys (+ [n_kv] fp32 scales for fp8, NULL for bf16)
- *   block_keys [n_kv / B, d_I] bf16 from lsa_block_means (ignored in flat mode, may be NULL)
+ *   block_keys [n_kv / B, d_I] bf16 from lsa_block_means, or [n_kv / B, 2 d_I] from
+ *              lsa_block_minmax when p->pooling is LSA_POOL_MINMAX (ignored in flat mode, may be
+ *              NULL)
  * Outputs (row i of each):
  *   idx        [n_q, K_cap] int32: S_t in ascending order = sink, then the K_sparse positions of
  *              largest score (ties to the smaller position), then the window; -1 after count[i]
@@ -128,6 +158,7 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
  *   page_table  [batch, max_pages] int32 device array of physical pages in [0, n_phys)
  *   k, k_scale  [n_phys * kv_page_size, d_I] keys (+ scales) of the page pool
  *   block_keys  [n_phys * kv_page_size / B, d_I] bf16 mean keys of the page pool
+ *               ([.., 2 d_I] extrema with LSA_POOL_MINMAX)
  * Outputs as in lsa_index_prefill with n_q = batch. Rows whose ctx_len or page-table entries
  * are out of range get count = 0.
  */

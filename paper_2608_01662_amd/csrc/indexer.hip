@@ -62,17 +62,28 @@ __device__ __forceinline__ int64_t phys_page(const IndexGeom& g, int64_t seq, in
   return (ph >= 0 && ph < g.n_phys) ? ph : -1;
 }
 
-// ============================================================================ mean keys (Stage 1 cache)
-// One thread per (sub-block, group of 4 dims): fp32 sum of s_i * k_i over the B tokens, one
-// multiply by 1/B (B is a power of two, exact), one round-to-nearest-even to bf16.
+// ============================================================================ block cache (Stage 1)
+// Sub-block handled by work item `item`: item itself (whole cache), or the sub-block holding token
+// rows[item] (incremental update); -1 when that row is out of range or in the incomplete tail.
+__device__ __forceinline__ int64_t block_of_item(int64_t item, const int64_t* __restrict__ rows, int64_t n_tok, int B) {
+  if (rows == nullptr) return item;
+  const int64_t r = rows[item];
+  return (r >= 0 && r < n_tok && r / B < n_tok / B) ? r / B : -1;
+}
+
+// Mean keys (Eq. 9). One thread per (work item, group of 4 dims): fp32 sum of s_i * k_i over the
+// B tokens, one multiply by 1/B (B is a power of two, exact), one round-to-nearest-even to bf16.
 template <bool FP8>
-__global__ __launch_bounds__(256) void block_means_kernel(int64_t n_sub, int D, int B, const void* __restrict__ k,
+__global__ __launch_bounds__(256) void block_means_kernel(int64_t n_items, const int64_t* __restrict__ rows, int64_t n_tok,
+                                                          int D, int B, const void* __restrict__ k,
                                                           const float* __restrict__ ks, uint16_t* __restrict__ out) {
   const int groups = D / 4;
   const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (id >= n_sub * groups) return;
-  const int64_t sub = id / groups;
-  const int gq = (int)(id - sub * groups);
+  if (id >= n_items * groups) return;
+  const int64_t item = id / groups;
+  const int gq = (int)(id - item * groups);
+  const int64_t sub = block_of_item(item, rows, n_tok, B);
+  if (sub < 0) return;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < B; ++i) {
     const int64_t tok = sub * B + i;
@@ -93,6 +104,63 @@ __global__ __launch_bounds__(256) void block_means_kernel(int64_t n_sub, int D, 
   o.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
   o.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
   reinterpret_cast<u32x2*>(out)[sub * groups + gq] = o;
+}
+
+// bf16 bits of x rounded to nearest, ties to even, in one step from fp64: the float rounded
+// toward zero keeps x's leading 24 bits exactly, and whether anything non-zero lies below them
+// only matters as a sticky bit (finite values within the float range).
+__device__ __forceinline__ uint32_t bf16_rne_from_f64(double x) {
+  const float t = __double2float_rz(x);
+  const uint32_t b = __float_as_uint(t);
+  const bool below = (double)t != x;
+  const uint32_t lsb = (b >> 16) & 1u, half = (b >> 15) & 1u;
+  const bool rest = (b & 0x7FFFu) != 0u || below;
+  return (b >> 16) + (half & (uint32_t)(rest || lsb));
+}
+
+// Min-max extrema (Eq. 13). One thread per (work item, group of 4 dims): each dequantised key
+// s_i * k_i is formed exactly in fp64 (24-bit scale times 4-bit code), the extrema are exact, and
+// each is rounded once to bf16. Output row: [k_max (D) | k_min (D)].
+template <bool FP8>
+__global__ __launch_bounds__(256) void block_minmax_kernel(int64_t n_items, const int64_t* __restrict__ rows, int64_t n_tok,
+                                                           int D, int B, const void* __restrict__ k,
+                                                           const float* __restrict__ ks, uint16_t* __restrict__ out) {
+  const int groups = D / 4;
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= n_items * groups) return;
+  const int64_t item = id / groups;
+  const int gq = (int)(id - item * groups);
+  const int64_t sub = block_of_item(item, rows, n_tok, B);
+  if (sub < 0) return;
+  double mx[4], mn[4];
+  for (int i = 0; i < B; ++i) {
+    const int64_t tok = sub * B + i;
+    double v[4];
+    if (FP8) {
+      const uint32_t c = reinterpret_cast<const uint32_t*>(k)[tok * groups + gq];
+      const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(c, false);  // codes decode exactly
+      const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(c, true);
+      const double s = (double)ks[tok];
+      v[0] = s * (double)lo.x; v[1] = s * (double)lo.y; v[2] = s * (double)hi.x; v[3] = s * (double)hi.y;
+    } else {
+      const u32x2 c = reinterpret_cast<const u32x2*>(k)[tok * groups + gq];
+      v[0] = (double)__uint_as_float(c.x << 16); v[1] = (double)__uint_as_float(c.x & 0xFFFF0000u);
+      v[2] = (double)__uint_as_float(c.y << 16); v[3] = (double)__uint_as_float(c.y & 0xFFFF0000u);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      mx[e] = (i == 0 || v[e] > mx[e]) ? v[e] : mx[e];
+      mn[e] = (i == 0 || v[e] < mn[e]) ? v[e] : mn[e];
+    }
+  }
+  u32x2 hi, lo;
+  hi.x = bf16_rne_from_f64(mx[0]) | (bf16_rne_from_f64(mx[1]) << 16);
+  hi.y = bf16_rne_from_f64(mx[2]) | (bf16_rne_from_f64(mx[3]) << 16);
+  lo.x = bf16_rne_from_f64(mn[0]) | (bf16_rne_from_f64(mn[1]) << 16);
+  lo.y = bf16_rne_from_f64(mn[2]) | (bf16_rne_from_f64(mn[3]) << 16);
+  u32x2* row = reinterpret_cast<u32x2*>(out + sub * 2 * D);
+  row[gq] = hi;
+  row[groups + gq] = lo;
 }
 
 // ============================================================================ operand loads
@@ -156,15 +224,38 @@ __device__ __forceinline__ float head_reduce(const f32x16& acc, const float (&wr
   return v + __shfl_xor(v, 32);
 }
 
+// A operand of min-max pooling (Eq. 13): per dimension max(q k_max, q k_min) = q+ k_max + q- k_min
+// with q+ = max(q, 0), q- = min(q, 0), so the block score is one dot product of width 2D between
+// [q+ | q-] and the cached [k_max | k_min]. Lane half 0 holds q+, half 1 holds q-; k-step s covers
+// dims 8s..8s+7 in both halves (the key operand's halves are k_max and k_min of the same dims).
+template <int D>
+__device__ __forceinline__ void load_query_minmax(const uint16_t* __restrict__ q, int H, int64_t row, int lane,
+                                                  u32x4 (&a)[D / 8]) {
+  const int j = lane & 31, h = lane >> 5;
+  // per bf16 half-word: all ones where the value is negative (sign bit set)
+  auto neg = [](uint32_t v) { return ((v >> 15) & 0x00010001u) * 0xFFFFu; };
+  auto part = [&](uint32_t v) { return h ? (v & neg(v)) : (v & ~neg(v)); };
+#pragma unroll
+  for (int s = 0; s < D / 8; ++s) {
+    if (j < H) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(q + (row * H + j) * D + 8 * s);
+      a[s] = u32x4{part(v.x), part(v.y), part(v.z), part(v.w)};
+    } else {
+      a[s] = u32x4{0, 0, 0, 0};
+    }
+  }
+}
+
 // ============================================================================ Stage 1: coarse page scores
-// Eq. (9). Grid: (ceil(n_rows / R), chunks). Each wave takes tiles of 32 mean keys of the
-// chunk; R query rows share each loaded tile (prefill). Output: order keys of the page scores,
-// page_keys[row * ld + p] for eligible pages p.
-template <int D, int R, bool PAGED>
+// Eq. (9), or Eq. (13) with MINMAX. Grid: (ceil(n_rows / R), chunks). Each wave takes tiles of 32
+// block keys of the chunk; R query rows share each loaded tile (prefill). Output: order keys of
+// the page scores, page_keys[row * ld + p] for eligible pages p.
+template <int D, int R, bool PAGED, bool MINMAX>
 __global__ __launch_bounds__(256) void coarse_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
                                                      const float* __restrict__ w, const uint16_t* __restrict__ kmean,
                                                      uint32_t* __restrict__ page_keys, int64_t ld, int tiles_per_chunk) {
-  constexpr int KS = D / 16;
+  constexpr int DK = MINMAX ? 2 * D : D;  // width of a block key and of the dot product
+  constexpr int KS = DK / 16;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31;
   const int64_t row0 = (int64_t)blockIdx.x * R;
   const int nsub = g.P / g.B;
@@ -189,7 +280,8 @@ __global__ __launch_bounds__(256) void coarse_kernel(IndexGeom g, int64_t n_rows
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int64_t row = row0 + r < n_rows ? row0 + r : n_rows - 1;
-    load_query_operand<D>(q, g.H, row, lane, a[r]);
+    if constexpr (MINMAX) load_query_minmax<D>(q, g.H, row, lane, a[r]);
+    else load_query_operand<D>(q, g.H, row, lane, a[r]);
     load_head_weights(w, g.H, row, lane, wr[r]);
   }
   const int64_t p_base = ri[0].p_lo;  // identical for every row (depends on k_sink only)
@@ -210,7 +302,7 @@ __global__ __launch_bounds__(256) void coarse_kernel(IndexGeom g, int64_t n_rows
     }
     u32x4 b[KS];
     {
-      const u32x4* pk = reinterpret_cast<const u32x4*>(kmean + mrow * D + (D / 2) * (lane >> 5));
+      const u32x4* pk = reinterpret_cast<const u32x4*>(kmean + mrow * DK + (DK / 2) * (lane >> 5));
 #pragma unroll
       for (int s = 0; s < KS; ++s) b[s] = pk[s];
     }
@@ -872,21 +964,31 @@ __global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64
 }
 
 // ============================================================================ host launchers
-template <bool FP8>
-static hipError_t launch_bm(int64_t n_sub, int D, int B, const void* k, const float* ks, uint16_t* out, hipStream_t st) {
-  const int64_t threads = n_sub * (D / 4);
+template <bool FP8, bool MINMAX>
+static hipError_t launch_bk(int64_t n_items, const int64_t* rows, int64_t n_tok, int D, int B, const void* k,
+                            const float* ks, uint16_t* out, hipStream_t st) {
+  const int64_t threads = n_items * (D / 4);
   if (threads == 0) return hipSuccess;
   const int64_t blocks = (threads + 255) / 256;
-  hipLaunchKernelGGL(block_means_kernel<FP8>, dim3((unsigned)blocks), dim3(256), 0, st, n_sub, D, B, k, ks, out);
+  if (MINMAX)
+    hipLaunchKernelGGL(block_minmax_kernel<FP8>, dim3((unsigned)blocks), dim3(256), 0, st, n_items, rows, n_tok, D, B,
+                       k, ks, out);
+  else
+    hipLaunchKernelGGL(block_means_kernel<FP8>, dim3((unsigned)blocks), dim3(256), 0, st, n_items, rows, n_tok, D, B,
+                       k, ks, out);
   return hipGetLastError();
 }
 
-hipError_t launch_block_means(int64_t n_sub, int D, int B, bool fp8, const void* k, const float* ks, uint16_t* out,
-                              hipStream_t st) {
-  return fp8 ? launch_bm<true>(n_sub, D, B, k, ks, out, st) : launch_bm<false>(n_sub, D, B, k, ks, out, st);
+hipError_t launch_block_keys(int64_t n_items, const int64_t* rows, int64_t n_tok, int D, int B, bool fp8, bool minmax,
+                             const void* k, const float* ks, uint16_t* out, hipStream_t st) {
+  if (minmax)
+    return fp8 ? launch_bk<true, true>(n_items, rows, n_tok, D, B, k, ks, out, st)
+               : launch_bk<false, true>(n_items, rows, n_tok, D, B, k, ks, out, st);
+  return fp8 ? launch_bk<true, false>(n_items, rows, n_tok, D, B, k, ks, out, st)
+             : launch_bk<false, false>(n_items, rows, n_tok, D, B, k, ks, out, st);
 }
 
-template <int D, int R, bool PAGED>
+template <int D, int R, bool PAGED, bool MINMAX>
 static hipError_t launch_coarse_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
                                   const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
                                   hipStream_t st) {
@@ -894,19 +996,28 @@ static hipError_t launch_coarse_t(const IndexGeom& g, int64_t n_rows, const uint
   const int64_t chunks = (max_tiles + tiles_per_chunk - 1) / tiles_per_chunk;
   if (chunks == 0 || n_rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((n_rows + R - 1) / R), (unsigned)chunks);
-  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED>), grid, dim3(256), 0, st, g, n_rows, q, w, kmean, page_keys, ld,
-                     tiles_per_chunk);
+  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED, MINMAX>), grid, dim3(256), 0, st, g, n_rows, q, w, kmean, page_keys,
+                     ld, tiles_per_chunk);
   return hipGetLastError();
+}
+
+template <int D, bool MINMAX>
+static hipError_t launch_coarse_d(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
+                                  const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
+                                  hipStream_t st) {
+  // min-max doubles the operands' width: fewer query rows share a tile (register budget)
+  constexpr int R = MINMAX ? 2 : 4;
+  return g.ctx_len != nullptr ? launch_coarse_t<D, 1, true, MINMAX>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
+                              : launch_coarse_t<D, R, false, MINMAX>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
 }
 
 hipError_t launch_coarse(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const uint16_t* kmean,
                          uint32_t* page_keys, int64_t ld, int64_t max_tiles, hipStream_t st) {
-  const bool paged = g.ctx_len != nullptr;
   if (g.D == 128)
-    return paged ? launch_coarse_t<128, 1, true>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
-                 : launch_coarse_t<128, 4, false>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
-  return paged ? launch_coarse_t<64, 1, true>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
-               : launch_coarse_t<64, 4, false>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
+    return g.minmax ? launch_coarse_d<128, true>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
+                    : launch_coarse_d<128, false>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
+  return g.minmax ? launch_coarse_d<64, true>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
+                  : launch_coarse_d<64, false>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
 }
 
 hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t* page_keys, int64_t ld,

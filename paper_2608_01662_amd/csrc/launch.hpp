@@ -10,6 +10,7 @@ namespace lsa {
 struct IndexGeom {
   int H, D, fp8;                 // indexer heads, head dim, fp8 keys
   int P, B, M;                   // page, sub-block, kept pages (M <= 0: flat)
+  int minmax;                    // coarse stage: min-max pooling (block keys [k_max | k_min])
   int k_sparse, k_sink, k_swa, C;
   int64_t q_start;               // prefill: position of row 0
   int64_t n_kv;                  // prefill: cached tokens
@@ -20,8 +21,10 @@ struct IndexGeom {
   int64_t n_phys;
 };
 
-hipError_t launch_block_means(int64_t n_sub, int D, int B, bool fp8, const void* k, const float* ks, uint16_t* out,
-                              hipStream_t st);
+// Block cache of the coarse stage: mean keys [n_sub, D] or min-max extrema [n_sub, 2D]. rows == nullptr:
+// every sub-block 0..n_items-1; otherwise the sub-blocks holding token rows[0..n_items).
+hipError_t launch_block_keys(int64_t n_items, const int64_t* rows, int64_t n_tok, int D, int B, bool fp8, bool minmax,
+                             const void* k, const float* ks, uint16_t* out, hipStream_t st);
 hipError_t launch_coarse(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const uint16_t* kmean,
                          uint32_t* page_keys, int64_t ld, int64_t max_tiles, hipStream_t st);
 hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t* page_keys, int64_t ld,

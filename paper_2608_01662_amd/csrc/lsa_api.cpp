@@ -54,6 +54,8 @@ lsa_status check_index_params(const lsa_index_params* p) {
               p->k_swa);
   LSA_REQUIRE(p->run_align >= 1, LSA_ERR_INVALID_ARG, "run_align=%d must be >= 1", p->run_align);
   LSA_REQUIRE((int64_t)p->k_sink + p->k_swa + p->k_sparse < (1LL << 30), LSA_ERR_INVALID_ARG, "k_cap too large");
+  LSA_REQUIRE(p->pooling == LSA_POOL_MEAN || p->pooling == LSA_POOL_MINMAX, LSA_ERR_INVALID_ARG, "pooling=%d unknown",
+              p->pooling);
   if (p->keep_pages > 0)
     LSA_REQUIRE(p->k_swa >= p->page, LSA_ERR_UNSUPPORTED,
                 "hierarchical mode needs k_swa=%d >= page=%d (scored pages must not reach past the query)", p->k_swa,
@@ -104,6 +106,7 @@ lsa::IndexGeom make_geom(const lsa_index_params* p) {
   g.P = p->page;
   g.B = p->sub_block;
   g.M = p->keep_pages > 0 ? p->keep_pages : 0;
+  g.minmax = p->pooling == LSA_POOL_MINMAX;
   g.k_sparse = p->k_sparse;
   g.k_sink = p->k_sink;
   g.k_swa = p->k_swa;
@@ -205,23 +208,46 @@ size_t lsa_index_workspace_size(const lsa_index_params* p, int64_t n_rows, int64
   return plan_index(p, n_rows, max_kv).total;
 }
 
-lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void* k, const float* k_scale,
-                           void* block_keys, void* stream) {
+static lsa_status run_block_cache(const lsa_index_params* p, bool minmax, int64_t n_items, const int64_t* rows,
+                                  int64_t n_tok, const void* k, const float* k_scale, void* block_keys, void* stream,
+                                  const char* what) {
   g_err[0] = 0;
   lsa_status s = check_index_params(p);
   if (s != LSA_OK) return s;
   const bool fp8 = p->key_dtype == LSA_KEY_FP8_E4M3FN;
-  LSA_REQUIRE(n_tok >= 0, LSA_ERR_INVALID_ARG, "n_tok=%lld < 0", (long long)n_tok);
-  const int64_t n_sub = n_tok / p->sub_block;
-  if (n_sub == 0) return LSA_OK;  // nothing to read or write
+  LSA_REQUIRE(n_tok >= 0 && n_items >= 0, LSA_ERR_INVALID_ARG, "n_tok=%lld / n_rows=%lld < 0", (long long)n_tok,
+              (long long)n_items);
+  if (n_items == 0 || n_tok / p->sub_block == 0) return LSA_OK;  // nothing to read or write
   LSA_REQUIRE(k && block_keys, LSA_ERR_INVALID_ARG, "k / block_keys is NULL");
   LSA_REQUIRE(fp8 == (k_scale != nullptr), LSA_ERR_INVALID_ARG, "k_scale must be given exactly for fp8 keys");
-  LSA_REQUIRE(aligned(k, 16) && aligned(block_keys, 16) && aligned(k_scale, 4), LSA_ERR_INVALID_ARG,
-              "k/block_keys must be 16-byte aligned, k_scale 4-byte aligned");
-  hipError_t e = lsa::launch_block_means(n_sub, p->head_dim, p->sub_block, fp8, k, k_scale,
-                                         static_cast<uint16_t*>(block_keys), static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "block means");
+  LSA_REQUIRE(aligned(k, 16) && aligned(block_keys, 16) && aligned(k_scale, 4) && aligned(rows, 8),
+              LSA_ERR_INVALID_ARG, "k/block_keys must be 16-byte aligned, k_scale 4-byte, rows 8-byte aligned");
+  hipError_t e = lsa::launch_block_keys(n_items, rows, n_tok, p->head_dim, p->sub_block, fp8, minmax, k, k_scale,
+                                        static_cast<uint16_t*>(block_keys), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, what);
   return LSA_OK;
+}
+
+lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void* k, const float* k_scale,
+                           void* block_keys, void* stream) {
+  if (p == nullptr) return fail(LSA_ERR_INVALID_ARG, "params is NULL");
+  const int64_t n_sub = n_tok / (p->sub_block > 0 ? p->sub_block : 1);
+  return run_block_cache(p, false, n_sub, nullptr, n_tok, k, k_scale, block_keys, stream, "block means");
+}
+
+lsa_status lsa_block_minmax(const lsa_index_params* p, int64_t n_tok, const void* k, const float* k_scale,
+                            void* block_keys, void* stream) {
+  if (p == nullptr) return fail(LSA_ERR_INVALID_ARG, "params is NULL");
+  const int64_t n_sub = n_tok / (p->sub_block > 0 ? p->sub_block : 1);
+  return run_block_cache(p, true, n_sub, nullptr, n_tok, k, k_scale, block_keys, stream, "block min-max");
+}
+
+lsa_status lsa_block_keys_update(const lsa_index_params* p, int64_t n_rows, const int64_t* rows, int64_t n_tok,
+                                 const void* k, const float* k_scale, void* block_keys, void* stream) {
+  if (p == nullptr) return fail(LSA_ERR_INVALID_ARG, "params is NULL");
+  if (n_rows > 0 && rows == nullptr) return fail(LSA_ERR_INVALID_ARG, "rows is NULL");
+  return run_block_cache(p, p->pooling == LSA_POOL_MINMAX, n_rows, rows, n_tok, k, k_scale, block_keys, stream,
+                         "block cache update");
 }
 
 static lsa_status check_index_io(const lsa_index_params* p, const void* q, const float* w, const void* k,

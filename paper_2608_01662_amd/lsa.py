@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "liblsa.so")
 
 LSA_KEY_BF16 = 0
 LSA_KEY_FP8_E4M3FN = 1
+POOLING = {"mean": 0, "minmax": 1}   # lsa_pooling
 
 
 class LSAError(RuntimeError):
@@ -28,7 +29,7 @@ class LSAError(RuntimeError):
 class _IndexParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_heads", "head_dim", "key_dtype", "page", "sub_block", "keep_pages",
-        "k_sparse", "k_sink", "k_swa", "run_align")]
+        "k_sparse", "k_sink", "k_swa", "run_align", "pooling")]
 
 
 class _AttnParams(ctypes.Structure):
@@ -49,15 +50,21 @@ class IndexParams:
     k_sink: int
     k_swa: int
     run_align: int
+    pooling: str = "mean"    # coarse-stage block summary: "mean" (Eq. 9) or "minmax" (Eq. 13)
 
     @property
     def k_cap(self) -> int:
         return self.k_sink + self.k_swa + self.k_sparse
 
+    @property
+    def block_width(self) -> int:
+        """Columns of one block-cache row: d_I (mean keys) or 2 d_I ([k_max | k_min])."""
+        return 2 * self.head_dim if self.pooling == "minmax" else self.head_dim
+
     def c(self) -> _IndexParams:
         return _IndexParams(self.n_heads, self.head_dim, LSA_KEY_FP8_E4M3FN if self.fp8 else LSA_KEY_BF16,
                             self.page, self.sub_block, self.keep_pages, self.k_sparse, self.k_sink,
-                            self.k_swa, self.run_align)
+                            self.k_swa, self.run_align, POOLING[self.pooling])
 
 
 @dataclass(frozen=True)
@@ -94,6 +101,10 @@ def lib() -> ctypes.CDLL:
         L.lsa_index_workspace_size.restype = _sz
         L.lsa_block_means.argtypes = [P, _i64, _vp, _vp, _vp, _vp]
         L.lsa_block_means.restype = _i32
+        L.lsa_block_minmax.argtypes = [P, _i64, _vp, _vp, _vp, _vp]
+        L.lsa_block_minmax.restype = _i32
+        L.lsa_block_keys_update.argtypes = [P, _i64, _vp, _i64, _vp, _vp, _vp, _vp]
+        L.lsa_block_keys_update.restype = _i32
         L.lsa_index_prefill.argtypes = [P, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                         _vp, _sz, _vp]
         L.lsa_index_prefill.restype = _i32
@@ -162,6 +173,34 @@ def block_means(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None 
     _check(lib().lsa_block_means(ctypes.byref(prm.c()), n_tok, _p(k), _p(k_scale), _p(out), _stream(k.device)),
            "lsa_block_means")
     return out
+
+
+def block_minmax(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None = None,
+                 out: torch.Tensor | None = None) -> torch.Tensor:
+    """Min-max block cache (Eq. 13): [n_tok // sub_block, 2 * head_dim] bf16 rows [k_max | k_min]."""
+    k = _keys_u8_or_bf16(k)
+    n_tok = k.shape[0]
+    if out is None:
+        out = torch.empty((n_tok // prm.sub_block, 2 * prm.head_dim), dtype=torch.bfloat16, device=k.device)
+    _check(lib().lsa_block_minmax(ctypes.byref(prm.c()), n_tok, _p(k), _p(k_scale), _p(out), _stream(k.device)),
+           "lsa_block_minmax")
+    return out
+
+
+def block_keys(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None = None,
+               out: torch.Tensor | None = None) -> torch.Tensor:
+    """The block cache the coarse stage of `prm` reads: mean keys or min-max extrema."""
+    return (block_minmax if prm.pooling == "minmax" else block_means)(prm, k, k_scale, out)
+
+
+def block_keys_update(prm: IndexParams, rows: torch.Tensor, k: torch.Tensor, k_scale: torch.Tensor | None,
+                      block: torch.Tensor) -> torch.Tensor:
+    """Recompute, in place, the block-cache rows of the sub-blocks holding token rows `rows` (int64)."""
+    k = _keys_u8_or_bf16(k)
+    assert rows.dtype == torch.int64
+    _check(lib().lsa_block_keys_update(ctypes.byref(prm.c()), rows.numel(), _p(rows), k.shape[0], _p(k),
+                                       _p(k_scale), _p(block), _stream(k.device)), "lsa_block_keys_update")
+    return block
 
 
 def _index_outputs(prm: IndexParams, n_rows: int, device, runs: bool, pages: bool, out: dict | None):

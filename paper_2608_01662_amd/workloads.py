@@ -36,6 +36,7 @@ class Workload:
     ctx_lo: int = 0
     ctx_hi: int = 0
     kv_page: int = 0             # decode: tokens per cache page
+    pooling: str = "mean"        # coarse-stage block summary: "mean" (Eq. 9) or "minmax" (Eq. 13)
 
     @property
     def k_cap(self) -> int:
@@ -48,7 +49,7 @@ class Workload:
     def index_params(self):
         from .lsa import IndexParams
         return IndexParams(self.n_heads, self.head_dim, self.fp8, self.page, self.sub_block, self.keep_pages,
-                           self.k_sparse, self.k_sink, self.k_swa, self.run_align)
+                           self.k_sparse, self.k_sink, self.k_swa, self.run_align, self.pooling)
 
     def attn_params(self):
         from .lsa import MLA, MQA, AttnParams
@@ -93,7 +94,11 @@ SMALL_CLI = replace(L128K_CLI4, name="small_L8192_cli4", seq_len=8192, keep_page
 SMALL_SUBBLOCK = replace(L128K_CLI4, name="small_L8192_B8", seq_len=8192, sub_block=8, keep_pages=8,
                          k_sparse=384, k_swa=512, layers=1)
 SMALL_FLAT = replace(L2K_MQA, name="small_L2048_flat", keep_pages=0)
+# min-max pooling of the coarse stage (Eq. 13), with one and with 16 sub-blocks per page
+SMALL_MINMAX = replace(SMALL_CLI, name="small_L8192_cli4_minmax", pooling="minmax")
+SMALL_MINMAX_B8 = replace(SMALL_SUBBLOCK, name="small_L8192_B8_minmax", pooling="minmax")
 SMALL_DECODE = replace(DECODE64, name="small_decode_b8", batch=8, ctx_lo=2048, ctx_hi=6000, keep_pages=16,
                        k_sparse=256, k_swa=128)
+SMALL_DECODE_MINMAX = replace(SMALL_DECODE, name="small_decode_b8_minmax", pooling="minmax")
 SMALL_CHUNKED = replace(L1M_CHUNKED, name="small_L16384_chunk1000", seq_len=16384, chunk=1000, keep_pages=16,
                         k_sparse=512, k_swa=256, layers=2)

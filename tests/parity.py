@@ -23,7 +23,14 @@ ATOL_O, RTOL_O, ATOL_LSE = 2e-2, 1e-2, 2e-3
 
 def oracle_params(w) -> orc.IndexParams:
     return orc.IndexParams(page=w.page, sub_block=w.sub_block, keep_pages=w.keep_pages, k_sparse=w.k_sparse,
-                           k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align)
+                           k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align, pooling=w.pooling)
+
+
+def oracle_block_cache(w, k_hat):
+    """The oracle's Stage 1 cache for workload w: mean keys, or (k_max, k_min) with min-max pooling."""
+    if w.pooling == "minmax":
+        return orc.sub_block_minmax_keys(k_hat, w.sub_block)
+    return orc.sub_block_mean_keys(k_hat, w.sub_block)
 
 
 def tie_equivalent(gpu_sel, orc_sel, ids, scores, k, tol=TOL_SCORE) -> int:

@@ -66,6 +66,29 @@ def test_bad_index_params(kw, status):
     assert lsa.lib().lsa_index_workspace_size(ctypes.byref(P(**kw).c()), 16, 4096) == 0
 
 
+def test_unknown_pooling_rejected():
+    c = P().c()
+    c.pooling = 7
+    L = lsa.lib()
+    assert L.lsa_index_prefill(ctypes.byref(c), 0, 16, 4096, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None,
+                               None, FAKE, 1 << 40, None) == INVALID
+    assert L.lsa_block_minmax(ctypes.byref(c), 4096, FAKE, FAKE, FAKE, None) == INVALID
+
+
+def test_bad_block_cache_arguments():
+    """Block-cache calls validate before launching: the rows list of an update must be given and
+    8-byte aligned, keys and output 16-byte aligned, a scale exactly for fp8 keys."""
+    L = lsa.lib()
+    prm = P(pooling="minmax").c()
+    assert L.lsa_block_keys_update(ctypes.byref(prm), 4, None, 4096, FAKE, FAKE, FAKE, None) == INVALID
+    assert L.lsa_block_keys_update(ctypes.byref(prm), 4, ctypes.c_void_p(0x100004), 4096, FAKE, FAKE, FAKE,
+                                   None) == INVALID
+    assert L.lsa_block_keys_update(ctypes.byref(prm), 4, FAKE, -1, FAKE, FAKE, FAKE, None) == INVALID
+    assert L.lsa_block_minmax(ctypes.byref(prm), 4096, MISALIGNED, FAKE, FAKE, None) == INVALID
+    assert L.lsa_block_minmax(ctypes.byref(prm), 4096, FAKE, None, FAKE, None) == INVALID      # fp8 needs scales
+    assert L.lsa_block_keys_update(ctypes.byref(prm), 0, None, 4096, None, None, None, None) == OK   # no rows
+
+
 def test_bad_index_arguments():
     prm = P()
     assert prefill(prm, q_start=4090, n_q=16, n_kv=4096) == INVALID           # rows past the cache

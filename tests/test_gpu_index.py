@@ -24,7 +24,7 @@ def _run_prefill(w, inp, q_start=0, n_q=None, pages=True):
     n_q = n_kv - q_start if n_q is None else n_q
     prm = w.index_params()
     q, wt, k, ks = P.gpu_index_inputs(inp, w)
-    bk = lsa.block_means(prm, k, ks) if w.keep_pages > 0 else None
+    bk = lsa.block_keys(prm, k, ks) if w.keep_pages > 0 else None
     out = lsa.index_prefill(prm, q[q_start:q_start + n_q], wt[q_start:q_start + n_q], k, ks, bk, q_start,
                             n_kv=n_kv, runs=True, pages=pages)
     torch.cuda.synchronize()
@@ -34,7 +34,7 @@ def _run_prefill(w, inp, q_start=0, n_q=None, pages=True):
 def _oracle_rows(w, inp, rows_t):
     prm = P.oracle_params(w)
     k_hat = P.oracle_keys(inp)
-    k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block) if w.keep_pages > 0 else None
+    k_mean = P.oracle_block_cache(w, k_hat) if w.keep_pages > 0 else None
     qf = orc.bf16_bits_to_f64(inp["q"])
     return [orc.index_row(t, qf[t], inp["w"][t], k_hat, k_mean, prm) for t in rows_t]
 
@@ -56,6 +56,54 @@ def test_block_means_parity(fp8, B):
     assert diff.max() <= 1 and (diff > 0).mean() < 1e-3, (diff.max(), (diff > 0).mean())
 
 
+@pytest.mark.parametrize("fp8,B", [(True, 64), (True, 8), (False, 64), (False, 1)])
+def test_block_minmax_parity(fp8, B):
+    """Min-max block cache (Eq. 13): exact extrema rounded once to bf16, bit-exact."""
+    w = W.L2K_MQA
+    inp = synth.indexer_inputs(5, 8, 1000, w.n_heads, w.head_dim, fp8)
+    prm = lsa.IndexParams(w.n_heads, w.head_dim, fp8, 32 if B == 1 else 64, B, 16, 256, 4, 128, 64, "minmax")
+    k = P.to_dev(inp["k"]) if fp8 else P.bf16_dev(inp["k"])
+    ks = P.to_dev(inp["k_scale"]) if fp8 else None
+    got = lsa.block_minmax(prm, k, ks).view(torch.int16).cpu().numpy().view(np.uint16)
+    k_max, k_min = orc.sub_block_minmax_keys(P.oracle_keys(inp), B)
+    ref = np.concatenate([orc.f64_to_bf16_bits(k_max), orc.f64_to_bf16_bits(k_min)], axis=1)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("pooling", ["mean", "minmax"])
+@pytest.mark.parametrize("fp8", [True, False])
+def test_block_keys_update_after_append(pooling, fp8):
+    """Decode appends tokens to a cache whose block cache already exists: updating the sub-blocks
+    of the appended rows (a list with repeats and out-of-range rows, which are skipped) gives the
+    cache a full recomputation gives, bit for bit; untouched sub-blocks keep their values."""
+    w = W.L2K_MQA
+    n = 1024
+    inp = synth.indexer_inputs(6, 8, n, w.n_heads, w.head_dim, fp8)
+    prm = lsa.IndexParams(w.n_heads, w.head_dim, fp8, 64, 8, 16, 256, 4, 128, 64, pooling)
+    k = P.to_dev(inp["k"]) if fp8 else P.bf16_dev(inp["k"])
+    ks = P.to_dev(inp["k_scale"]) if fp8 else None
+    full0 = lsa.block_keys(prm, k, ks)
+    # overwrite rows [700, 713) (the "appended" tokens) with other keys, then update
+    other = synth.indexer_inputs(7, 8, n, w.n_heads, w.head_dim, fp8)
+    new_rows = np.arange(700, 713)
+    sel = torch.from_numpy(new_rows).to(k.device)
+    k2 = (P.to_dev(other["k"]) if fp8 else P.bf16_dev(other["k"]))
+    k[sel] = k2[sel]
+    if fp8:
+        ks[sel] = P.to_dev(other["k_scale"])[sel]
+    block = full0.clone()
+    rows = torch.tensor(np.concatenate([new_rows, [705, -3, n, n + 100]]), dtype=torch.int64, device=k.device)
+    lsa.block_keys_update(prm, rows, k, ks, block)
+    full1 = lsa.block_keys(prm, k, ks)
+    torch.cuda.synchronize()
+    assert torch.equal(block.view(torch.int16), full1.view(torch.int16))
+    touched = set((new_rows // 8).tolist())
+    for b in range(n // 8):
+        if b not in touched:
+            assert torch.equal(block[b].view(torch.int16), full0[b].view(torch.int16))
+
+
 def test_fp8_decode_all_codes():
     """Mean keys with B = 1 and unit scales are the decoded codes: all 256 e4m3fn codes, exactly."""
     codes = np.arange(256, dtype=np.uint32).astype(np.uint8)
@@ -69,8 +117,8 @@ def test_fp8_decode_all_codes():
 
 
 # ----------------------------------------------------------------------------- prefill
-@pytest.mark.parametrize("w", [W.L2K_MQA, W.SMALL_FLAT, W.SMALL_MLA, W.SMALL_CLI, W.SMALL_SUBBLOCK],
-                         ids=lambda w: w.name)
+@pytest.mark.parametrize("w", [W.L2K_MQA, W.SMALL_FLAT, W.SMALL_MLA, W.SMALL_CLI, W.SMALL_SUBBLOCK, W.SMALL_MINMAX,
+                               W.SMALL_MINMAX_B8], ids=lambda w: w.name)
 def test_index_prefill_parity(w):
     inp = P.prefill_inputs(w)
     out, _ = _run_prefill(w, inp)
@@ -230,12 +278,12 @@ def _decode_case(w):
     return ctx, table, n_phys, inp
 
 
-def test_index_decode_parity():
-    w = W.SMALL_DECODE
+@pytest.mark.parametrize("w", [W.SMALL_DECODE, W.SMALL_DECODE_MINMAX], ids=lambda w: w.name)
+def test_index_decode_parity(w):
     ctx, table, n_phys, inp = _decode_case(w)
     prm = w.index_params()
     q, wt, k, ks = P.gpu_index_inputs(inp, w)
-    bk = lsa.block_means(prm, k, ks)
+    bk = lsa.block_keys(prm, k, ks)
     out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk, pages=True)
     torch.cuda.synchronize()
     out = {key: v.cpu().numpy() for key, v in out.items()}
@@ -246,7 +294,7 @@ def test_index_decode_parity():
     for b in range(w.batch):
         t = int(ctx[b]) - 1
         k_log = orc.logical_rows(k_hat_pool, table[b], t + 1, w.kv_page)
-        k_mean = orc.sub_block_mean_keys(k_log, w.sub_block)
+        k_mean = P.oracle_block_cache(w, k_log)
         res.append(orc.index_row(t, qf[b], inp["w"][b], k_log, k_mean, prmo))
         rows_t.append(t)
     P.check_index_rows(w, rows_t, out["idx"], out["count"], out["pages"], res)
@@ -262,7 +310,7 @@ def test_decode_bad_rows_are_skipped():
     ctx[1] = table.shape[1] * w.kv_page + 1
     prm = w.index_params()
     q, wt, k, ks = P.gpu_index_inputs(inp, w)
-    bk = lsa.block_means(prm, k, ks)
+    bk = lsa.block_keys(prm, k, ks)
     out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk)
     torch.cuda.synchronize()
     assert out["count"][0].item() == 0 and out["count"][1].item() == 0
