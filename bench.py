@@ -80,19 +80,21 @@ def copy_probe(nbytes: int):
     print(json.dumps({"copy_probe_bytes": nbytes, "copies": 3}), flush=True)
 
 
-def make_inputs(w, dev):
+def make_inputs(w, dev, n_q):
+    """Indexer and attention inputs: the key caches of all L tokens, the queries of the n_q rows
+    of one step."""
     n = w.seq_len
     H, dqk, dv = w.attn_dims
     t = {}
-    t["qI"] = synth.device_normal_bf16((n, w.n_heads, w.head_dim), w.seed, synth.T_QI, dev,
+    t["qI"] = synth.device_normal_bf16((n_q, w.n_heads, w.head_dim), w.seed, synth.T_QI, dev,
                                        scale=1.0 / math.sqrt(w.head_dim))
-    t["wI"] = synth.device_uniform_f32((n, w.n_heads), w.seed, synth.T_W, dev)
+    t["wI"] = synth.device_uniform_f32((n_q, w.n_heads), w.seed, synth.T_W, dev)
     if w.fp8:
         t["kI"], t["ks"] = synth.device_fp8_keys(n, w.head_dim, w.seed, dev)
     else:
         t["kI"] = synth.device_normal_bf16((n, w.head_dim), w.seed, synth.T_KI, dev, scale=1.0 / math.sqrt(w.head_dim))
         t["ks"] = None
-    t["Q"] = [synth.device_normal_bf16((n, H, dqk), w.seed, synth.T_Q + l, dev, rows_per_chunk=2048)
+    t["Q"] = [synth.device_normal_bf16((n_q, H, dqk), w.seed, synth.T_Q + l, dev, rows_per_chunk=2048)
               for l in range(w.layers)]
     t["KV"] = [synth.device_normal_bf16((n, dqk), w.seed, synth.T_KV + l, dev) for l in range(w.layers)]
     t["V"] = [None if w.attn == "mla" else synth.device_normal_bf16((n, dv), w.seed, synth.T_V + l, dev)
@@ -100,8 +102,9 @@ def make_inputs(w, dev):
     return t
 
 
-def cpu_baseline(w, t, seconds):
-    """The float64 oracle on a bounded sample of query rows of the same workload."""
+def cpu_baseline(w, t, seconds, q_start=0):
+    """The float64 oracle on a bounded sample of query rows of the same workload (rows of the
+    step: positions q_start .. L-1)."""
     import oracle.lsa_oracle as orc
     try:
         from threadpoolctl import threadpool_info
@@ -111,10 +114,11 @@ def cpu_baseline(w, t, seconds):
     n = w.seq_len
     H, dqk, dv = w.attn_dims
     g = np.random.default_rng(1234)
-    rows = np.sort(g.choice(np.arange(w.k_cap, n), size=min(512, n - w.k_cap), replace=False))
+    lo = max(w.k_cap, q_start)
+    rows = np.sort(g.choice(np.arange(lo, n), size=min(512, n - lo), replace=False))
     kb = t["kI"].cpu().numpy() if w.fp8 else t["kI"].view(torch.int16).cpu().numpy().view(np.uint16)
     ks = t["ks"].cpu().numpy() if w.fp8 else None
-    ridx = torch.from_numpy(rows).cuda()
+    ridx = torch.from_numpy(rows - q_start).cuda()
     qrows = t["qI"].index_select(0, ridx).float().cpu().numpy().astype(np.float64)
     wrows = t["wI"].index_select(0, ridx).cpu().numpy()
     Qrows = [q.index_select(0, ridx).view(torch.int16).cpu().numpy().view(np.uint16) for q in t["Q"]]
@@ -139,11 +143,12 @@ def cpu_baseline(w, t, seconds):
         if time.perf_counter() - t1 > seconds:
             break
     per_row = (time.perf_counter() - t1) / done
-    full = t_once + n * per_row
-    return {"value": n / full, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"{done} query rows at random positions in [K_cap, L) through the indexer and "
+    n_q = n - q_start
+    full = t_once + n_q * per_row
+    return {"value": n_q / full, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"{done} query rows at random positions in [{lo}, L) through the indexer and "
                        f"{w.layers} attention layers, plus the one-off key decode and block cache "
-                       f"({t_once:.2f} s); tokens/s extrapolated to all {n} rows "
+                       f"({t_once:.2f} s); tokens/s extrapolated to all {n_q} rows of the step "
                        f"({per_row * 1e3:.1f} ms per row)")}
 
 
@@ -152,7 +157,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL if not w.decode and not w.chunk])
+    ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL if not w.decode],
+                    help="single-call prefill workloads time the whole prefill; chunked ones time the last "
+                         "chunk (its block-cache update, indexer and attention) against the full cache")
     ap.add_argument("--pooling", default="mean", choices=["mean", "minmax"],
                     help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -177,30 +184,38 @@ def main():
         from dataclasses import replace
         w = replace(w, name=f"{w.name}_{args.pooling}", pooling=args.pooling)
     n = w.seq_len
+    q_start = n - w.chunk if w.chunk else 0   # chunked workloads: the step is the last chunk
+    n_q = n - q_start
     H, dqk, dv = w.attn_dims
     prm, aprm = w.index_params(), w.attn_params()
     log(f"[bench] {w.name}: generating inputs on {torch.cuda.get_device_name(dev)}")
-    t = make_inputs(w, dev)
+    t = make_inputs(w, dev, n_q)
     bk = torch.empty((n // w.sub_block, prm.block_width), dtype=torch.bfloat16, device=dev)
-    out = dict(idx=torch.empty((n, w.k_cap), dtype=torch.int32, device=dev),
-               count=torch.empty((n,), dtype=torch.int32, device=dev),
-               runs=torch.empty((n, w.k_cap, 2), dtype=torch.int32, device=dev),
-               run_count=torch.empty((n,), dtype=torch.int32, device=dev))
-    ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n, n)), dtype=torch.uint8, device=dev)
-    ws_attn_n = lsa.attn_workspace_size(aprm, n, w.k_cap, False)
+    chunk_rows = torch.arange(q_start, n, dtype=torch.int64, device=dev)
+    if w.chunk:
+        lsa.block_keys(prm, t["kI"], t["ks"], out=bk)   # the earlier chunks' block cache exists already
+    out = dict(idx=torch.empty((n_q, w.k_cap), dtype=torch.int32, device=dev),
+               count=torch.empty((n_q,), dtype=torch.int32, device=dev),
+               runs=torch.empty((n_q, w.k_cap, 2), dtype=torch.int32, device=dev),
+               run_count=torch.empty((n_q,), dtype=torch.int32, device=dev))
+    ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n_q, n)), dtype=torch.uint8, device=dev)
+    ws_attn_n = lsa.attn_workspace_size(aprm, n_q, w.k_cap, False)
     ws_attn = torch.empty(max(1, ws_attn_n), dtype=torch.uint8, device=dev)
-    O = [torch.empty((n, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
-    LSE = [torch.empty((n, H), dtype=torch.float32, device=dev) for _ in range(w.layers)]
+    O = [torch.empty((n_q, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
+    LSE = [torch.empty((n_q, H), dtype=torch.float32, device=dev) for _ in range(w.layers)]
     torch.cuda.synchronize()
     log(f"[bench] inputs ready; {torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated")
 
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        lsa.block_keys(prm, t["kI"], t["ks"], out=bk)
+        if w.chunk:   # the chunk's own keys just entered the cache: refresh their sub-blocks
+            lsa.block_keys_update(prm, chunk_rows, t["kI"], t["ks"], bk)
+        else:
+            lsa.block_keys(prm, t["kI"], t["ks"], out=bk)
         if ev is not None:
             ev[1].record()
-        lsa.index_prefill(prm, t["qI"], t["wI"], t["kI"], t["ks"], bk, 0, n_kv=n, runs=True,
+        lsa.index_prefill(prm, t["qI"], t["wI"], t["kI"], t["ks"], bk, q_start, n_kv=n, runs=True,
                           workspace=ws_idx, out=out)
         if ev is not None:
             ev[2].record()
@@ -236,9 +251,9 @@ def main():
     sum_s = int(cnt.sum())
     row_kv_bytes = dqk * 2 if w.attn == "mla" else (dqk + dv) * 2
     attn_bytes = (sum_s * row_kv_bytes + sum_s * 4                       # gathered rows + their indices
-                  + n * H * dqk * 2 + n * H * dv * 2 + n * H * 4 + n * 4)  # Q in, O and lse out, count
+                  + n_q * H * dqk * 2 + n_q * H * dv * 2 + n_q * H * 4 + n_q * 4)  # Q in, O and lse out, count
     attn_flops = 2.0 * H * sum_s * (dqk + dv)
-    tpos = np.arange(n)
+    tpos = np.arange(q_start, n)
     hi = tpos - w.k_swa
     n_elig_pages = np.where(hi >= w.k_sink, hi // w.page - w.k_sink // w.page + 1, 0)
     cand = np.where(hi >= w.k_sink, np.minimum(n_elig_pages, w.keep_pages) * w.page, 0)
@@ -247,8 +262,9 @@ def main():
     idx_flops = 2.0 * w.n_heads * (coarse_dim * float(n_elig_pages.sum()) * sub_per_page + w.head_dim * float(cand.sum()))
     attn_gbs = attn_bytes / (attn_avg * 1e-3) / 1e9
     res = {
-        "metric": "LSA prefill tokens/s at L=128K (indexer+attn)",
-        "value": n / (ms_per_step * 1e-3),
+        "metric": ("LSA prefill tokens/s at L=128K (indexer+attn)" if not w.chunk else
+                   f"LSA chunked-prefill tokens/s, last {w.chunk}-row chunk at L={n} (indexer+attn)"),
+        "value": n_q / (ms_per_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -259,7 +275,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "seq_len": n, "layers_sharing_index": w.layers,
+        "config": {"workload": w.name, "seq_len": n, "rows_per_step": n_q, "q_start": q_start,
+                   "layers_sharing_index": w.layers,
                    "indexer": {"heads": w.n_heads, "head_dim": w.head_dim, "keys": "fp8_e4m3fn" if w.fp8 else "bf16",
                                "page": w.page, "sub_block": w.sub_block, "keep_pages": w.keep_pages,
                                "k_sparse": w.k_sparse, "k_sink": w.k_sink, "k_swa": w.k_swa,
@@ -275,13 +292,13 @@ def main():
             "attn_tflops": attn_flops / (attn_avg * 1e-3) / 1e12,
             "attn_mfma_frac": attn_flops / (attn_avg * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
             "attn_gather_gbs": sum_s * row_kv_bytes / (attn_avg * 1e-3) / 1e9,
-            "attn_tokens_per_s_per_layer": n / (attn_avg * 1e-3),
-            "mean_index_list_len": sum_s / n,
+            "attn_tokens_per_s_per_layer": n_q / (attn_avg * 1e-3),
+            "mean_index_list_len": sum_s / n_q,
         },
     }
     if not args.no_cpu_baseline:
         log(f"[bench] timing the oracle for ~{args.cpu_seconds:.0f} s on the host")
-        res["cpu_baseline"] = cpu_baseline(w, t, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(w, t, args.cpu_seconds, q_start)
     print(json.dumps(res), flush=True)
 
 

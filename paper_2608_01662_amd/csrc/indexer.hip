@@ -735,8 +735,9 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
 
 // Eq. (12) / Eq. (7) then Eq. (6): S_t = sink ++ (top K_sparse candidates, ascending) ++ window;
 // idx padded with -1; runs re-encode idx, cut at gaps and at multiples of C. General version:
-// the candidate keys are staged in LDS (any number that fits).
-template <int NT>
+// the candidate keys are staged in LDS (any number that fits), or with GK (rows too long for
+// LDS) every pass reads them from the fine-score rows in global memory.
+template <int NT, bool GK>
 __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ fine_keys,
                                                           int64_t ldf, const int32_t* __restrict__ pages,
                                                           int32_t* __restrict__ idx, int32_t* __restrict__ count,
@@ -746,9 +747,12 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
   __shared__ uint32_t hist[256];
   __shared__ int wsum[2 * NT / 64 + 2];
   const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
-  uint32_t* keys = smem;                                                  // [max(slots_cap, k_cap)]
-  int32_t* lidx = reinterpret_cast<int32_t*>(smem + (slots_cap > k_cap ? slots_cap : k_cap));   // [k_cap]
-  int32_t* lpages = lidx + k_cap;                                         // [M] (HI only)
+  // LDS: keys [max(slots_cap, k_cap)] (not with GK), lidx [k_cap], lpages [M], and with GK the
+  // run-start scratch [k_cap] (otherwise the keys area serves for it)
+  const int key_words = GK ? 0 : (slots_cap > k_cap ? slots_cap : k_cap);
+  int32_t* lidx = reinterpret_cast<int32_t*>(smem + key_words);
+  int32_t* lpages = lidx + k_cap;
+  int32_t* rstart = GK ? lpages + (g.M > 0 ? g.M : 0) : reinterpret_cast<int32_t*>(smem);
 
   const int64_t row = blockIdx.x;
   const RowInfo ri = row_info(g, row);
@@ -766,7 +770,9 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
     if (!flat)
       for (int i = threadIdx.x; i < n_sel; i += NT) lpages[i] = pages[row * g.M + i];
     const int n = n_sel * g.P;
-    for (int i = threadIdx.x; i < n; i += NT) keys[i] = fine_keys[row * ldf + i];
+    const uint32_t* keys = GK ? fine_keys + row * ldf : smem;
+    if (!GK)
+      for (int i = threadIdx.x; i < n; i += NT) smem[i] = fine_keys[row * ldf + i];
     __syncthreads();
     const int n_valid = block_count_nonzero(keys, n, wsum);
     uint32_t T = 0;
@@ -784,7 +790,7 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
     cnt = g.k_sink + n_sp + g.k_swa;
   }
   __syncthreads();
-  emit_row<NT>(g, row, lidx, cnt, reinterpret_cast<int32_t*>(keys), wsum, idx, count, runs, run_count);
+  emit_row<NT>(g, row, lidx, cnt, rstart, wsum, idx, count, runs, run_count);
 }
 
 // Block-wide scans over NT threads of one 32-bit value each.
@@ -1072,10 +1078,24 @@ hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, co
 #undef LSA_FINE
 }
 
-size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M) {
-  if (slots_cap <= kSelectRegMax) return (size_t)(2 * k_cap + (M > 0 ? M : 0)) * 4;  // register-held keys
+// Which selection kernel serves rows of slots_cap candidates: keys in registers, staged in LDS,
+// or read from global memory in every pass (rows too long for LDS).
+enum class SelectMode { kRegisters, kLds, kGlobal };
+constexpr size_t kSelectLdsLimit = 160 * 1024 - 4096;  // dynamic LDS the select kernels may use
+
+static SelectMode select_mode(int64_t slots_cap, int k_cap, int M) {
+  if (slots_cap <= kSelectRegMax) return SelectMode::kRegisters;
   const int64_t a = slots_cap > k_cap ? slots_cap : k_cap;
-  return (size_t)(a + k_cap + (M > 0 ? M : 0)) * 4;
+  return (size_t)(a + k_cap + (M > 0 ? M : 0)) * 4 <= kSelectLdsLimit ? SelectMode::kLds : SelectMode::kGlobal;
+}
+
+size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M) {
+  const size_t m = (size_t)(M > 0 ? M : 0);
+  switch (select_mode(slots_cap, k_cap, M)) {
+    case SelectMode::kRegisters: return (2 * (size_t)k_cap + m) * 4;
+    case SelectMode::kLds: return ((size_t)(slots_cap > k_cap ? slots_cap : k_cap) + k_cap + m) * 4;
+    default: return (2 * (size_t)k_cap + m) * 4;
+  }
 }
 
 hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_t* fine_keys, int64_t ldf,
@@ -1094,9 +1114,12 @@ hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_
   else if (slots_cap <= kSelectRegMax)
     hipLaunchKernelGGL((token_select_reg_kernel<512, 64>), grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx,
                        count, runs, run_count);
+  else if (select_mode(slots_cap, k_cap, g.M) == SelectMode::kLds)
+    hipLaunchKernelGGL((token_select_kernel<512, false>), grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx,
+                       count, runs, run_count, (int)slots_cap);
   else
-    hipLaunchKernelGGL(token_select_kernel<512>, grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx, count,
-                       runs, run_count, (int)slots_cap);
+    hipLaunchKernelGGL((token_select_kernel<1024, true>), grid, dim3(1024), lds, st, g, n_rows, fine_keys, ldf, pages,
+                       idx, count, runs, run_count, (int)slots_cap);
   return hipGetLastError();
 }
 
@@ -1108,11 +1131,13 @@ hipError_t prepare_index_kernels() {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev >= 0 && dev < 64 && done[dev]) return hipSuccess;
-  const int lim = 160 * 1024 - 4096;
-  const void* sel[] = {(const void*)token_select_kernel<512>, (const void*)token_select_reg_kernel<512, 16>,
-                       (const void*)token_select_reg_kernel<512, 32>, (const void*)token_select_reg_kernel<512, 64>};
-  for (const void* f : sel) {  // (the register-key kernels have 20 KB of static LDS, the other 4 KB)
-    e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, f == sel[0] ? lim : lim - 16 * 1024);
+  const int lim = (int)kSelectLdsLimit;
+  const void* sel[] = {(const void*)token_select_kernel<512, false>, (const void*)token_select_kernel<1024, true>,
+                       (const void*)token_select_reg_kernel<512, 16>, (const void*)token_select_reg_kernel<512, 32>,
+                       (const void*)token_select_reg_kernel<512, 64>};
+  for (const void* f : sel) {  // (the register-key kernels have 20 KB of static LDS, the others 4 KB)
+    e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (f == sel[0] || f == sel[1]) ? lim : lim - 16 * 1024);
     if (e != hipSuccess) return e;
   }
   e = hipFuncSetAttribute((const void*)page_select_kernel<256>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);

@@ -90,7 +90,8 @@ lsa_status check_lds(const lsa_index_params* p, const IndexPlan& pl) {
   const int k_cap = p->k_sink + p->k_swa + p->k_sparse;
   const size_t ts = lsa::token_select_lds_bytes(pl.slots, k_cap, p->keep_pages);
   LSA_REQUIRE(ts + lsa::token_select_static_lds(pl.slots) <= kMaxLds, LSA_ERR_UNSUPPORTED,
-              "candidate slots (%lld) plus k_cap (%d) exceed the LDS of one workgroup; lower keep_pages*page",
+              "the selection of %lld candidate slots with k_cap=%d does not fit the LDS of one workgroup; "
+              "lower k_sparse + k_sink + k_swa or keep_pages",
               (long long)pl.slots, k_cap);
   if (p->keep_pages > 0)
     LSA_REQUIRE((size_t)pl.n_pages * 4 + kSelectStaticLds <= kMaxLds, LSA_ERR_UNSUPPORTED,

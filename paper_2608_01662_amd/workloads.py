@@ -84,7 +84,11 @@ L1M_CHUNKED = Workload("prefill_L1048576_chunk8192_cli4_mla", seed=4, n_heads=32
                        page=128, sub_block=128, keep_pages=256, k_sparse=4096, k_sink=4, k_swa=2048,
                        run_align=128, attn="mla", sm_scale=MLA_SCALE, layers=4, seq_len=1048576, chunk=8192)
 
-FULL = [L2K_MQA, L32K_MLA, L128K_CLI4, DECODE64, L1M_CHUNKED]
+# 6. the paper's chosen hierarchical setting at scale: 16 mean keys per 128-token page (B = 8) and
+#    M = 1024 recalled pages (131072 fine candidates per row), on the 1M-token chunked prefill
+L1M_HI_B8 = replace(L1M_CHUNKED, name="prefill_L1048576_chunk8192_cli4_hi_b8_m1024", sub_block=8, keep_pages=1024)
+
+FULL = [L2K_MQA, L32K_MLA, L128K_CLI4, DECODE64, L1M_CHUNKED, L1M_HI_B8]
 BY_NAME = {w.name: w for w in FULL}
 
 # Reduced shapes for oracle parity at full-row coverage (same structure, smaller L and budgets).

@@ -38,7 +38,7 @@ def _indexer_oracle(w, q_rows, w_rows, codes, scales, rows_t, n_kv):
     """Oracle index rows for positions rows_t; q_rows / w_rows are the rows' own inputs."""
     prm = P.oracle_params(w)
     k_hat = orc.dequantized_keys(codes[:n_kv], scales[:n_kv])
-    k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block)
+    k_mean = P.oracle_block_cache(w, k_hat)
     qf = orc.bf16_bits_to_f64(q_rows)
     return [orc.index_row(t, qf[i], w_rows[i], k_hat, k_mean, prm) for i, t in enumerate(rows_t)]
 
@@ -70,7 +70,7 @@ def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed):
                                   scale=1.0 / math.sqrt(w.head_dim))
     wI = synth.device_uniform_f32((n_q, w.n_heads), w.seed, synth.T_W, DEV)
     kI, ks = synth.device_fp8_keys(n_kv, w.head_dim, w.seed, DEV)
-    bk = lsa.block_means(prm, kI, ks)
+    bk = lsa.block_keys(prm, kI, ks)
     out = lsa.index_prefill(prm, qI, wI, kI, ks, bk, q_start, n_kv=n_kv, runs=True, pages=True)
     rows_t = _sample_positions(w, q_start, q_start + n_q - 1, n_random, seed)
     rows = [t - q_start for t in rows_t]
@@ -111,6 +111,15 @@ def test_fullsize_prefill_L1M_last_chunk():
     _prefill_case(w, q_start, w.chunk, w.seq_len, layers=[0], n_random=16, seed=103)
 
 
+def test_fullsize_prefill_L1M_paper_hi_setting():
+    """The paper's chosen hierarchical setting at scale (B = 8, P = 128, M = 1024: 131072 fine
+    candidates per row, selected with the candidate keys read from global memory), on the last
+    8192-row chunk of the 1M-token prefill."""
+    w = W.L1M_HI_B8
+    q_start = w.seq_len - w.chunk
+    _prefill_case(w, q_start, w.chunk, w.seq_len, layers=[0], n_random=12, seed=104)
+
+
 def test_fullsize_decode_b64():
     """64 sequences of 16K..128K tokens in randomly permuted 64-token pages, one new token each;
     every sequence is checked."""
@@ -123,7 +132,7 @@ def test_fullsize_decode_b64():
                                   scale=1.0 / math.sqrt(w.head_dim))
     wI = synth.device_uniform_f32((w.batch, w.n_heads), w.seed, synth.T_W, DEV)
     kI, ks = synth.device_fp8_keys(n_tok, w.head_dim, w.seed, DEV)
-    bk = lsa.block_means(prm, kI, ks)
+    bk = lsa.block_keys(prm, kI, ks)
     ctx_d, table_d = P.to_dev(ctx), P.to_dev(table)
     out = lsa.index_decode(prm, ctx_d, table_d, w.kv_page, n_phys, qI, wI, kI, ks, bk, runs=True, pages=True)
     g = {k: v.cpu().numpy() for k, v in out.items()}
@@ -137,7 +146,7 @@ def test_fullsize_decode_b64():
         t = int(ctx[b]) - 1
         k_log = orc.dequantized_keys(orc.logical_rows(codes, table[b], t + 1, w.kv_page),
                                      orc.logical_rows(scales, table[b], t + 1, w.kv_page))
-        k_mean = orc.sub_block_mean_keys(k_log, w.sub_block)
+        k_mean = P.oracle_block_cache(w, k_log)
         res.append(orc.index_row(t, orc.bf16_bits_to_f64(qb[b]), wb[b], k_log, k_mean, prmo))
         rows_t.append(t)
     stats = P.check_index_rows(w, rows_t, g["idx"][batch_rows], g["count"][batch_rows], g["pages"][batch_rows], res)

@@ -154,6 +154,25 @@ def test_flat_short_window_partial_page(base):
     print(w.name, stats)
 
 
+@pytest.mark.parametrize("keep_pages", [0, 600])
+def test_select_from_global_keys(keep_pages):
+    """Rows with more candidates than the LDS holds (here 45056 in flat mode, 38400 with M = 600
+    pages) are selected by the kernel that reads the candidate keys from global memory in every
+    pass: the last 384 query rows of a 45056-token cache against the oracle, stage-wise."""
+    from dataclasses import replace
+    w = replace(W.L32K_MLA, seq_len=45056, keep_pages=keep_pages, k_sparse=1024)
+    inp = P.prefill_inputs(w)
+    q0 = w.seq_len - 384
+    out, _ = _run_prefill(w, inp, q_start=q0, pages=keep_pages > 0)
+    rows = sorted(set(range(q0, w.seq_len, 9)) | {w.seq_len - 1})
+    res = _oracle_rows(w, inp, rows)
+    sel = [t - q0 for t in rows]
+    stats = P.check_index_rows(w, rows, out["idx"][sel], out["count"][sel],
+                               out["pages"][sel] if "pages" in out else None, res)
+    P.check_runs(out["runs"][sel], out["run_count"][sel], out["idx"][sel], out["count"][sel], w.run_align)
+    print(w.name, keep_pages, stats)
+
+
 def test_keep_all_equals_flat_on_gpu():
     """With M >= #pages the hierarchical kernels must return exactly the flat selection."""
     w = W.SMALL_MLA
