@@ -80,6 +80,40 @@ def copy_probe(nbytes: int):
     print(json.dumps({"copy_probe_bytes": nbytes, "copies": 3}), flush=True)
 
 
+def index_sweep(lengths, pooling):
+    """Indexer time of one whole prefill (every row) at each cache length, hierarchical (the
+    benchmark workload's M and P) against flat (dense causal scoring of every eligible token): the
+    measurement behind the adaptive dispatch length hi_min_kv. One JSON line per length."""
+    from dataclasses import replace
+    dev = torch.device("cuda:0")
+    base = replace(W.L128K_CLI4, pooling=pooling)
+    for L in lengths:
+        w = replace(base, seq_len=L)
+        qI = synth.device_normal_bf16((L, w.n_heads, w.head_dim), w.seed, synth.T_QI, dev,
+                                      scale=1.0 / math.sqrt(w.head_dim))
+        wI = synth.device_uniform_f32((L, w.n_heads), w.seed, synth.T_W, dev)
+        kI, ks = synth.device_fp8_keys(L, w.head_dim, w.seed, dev)
+        res = {"seq_len": L, "rows": L}
+        for mode, keep in (("hierarchical", w.keep_pages), ("flat", 0)):
+            prm = replace(w, keep_pages=keep).index_params()
+            bk = lsa.block_keys(prm, kI, ks)
+            out = lsa.index_prefill(prm, qI, wI, kI, ks, bk, 0, n_kv=L, runs=True)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(3):
+                lsa.index_prefill(prm, qI, wI, kI, ks, bk, 0, n_kv=L, runs=True, out=out)
+            e1.record()
+            torch.cuda.synchronize()
+            res[f"{mode}_ms"] = e0.elapsed_time(e1) / 3
+            del out, bk
+            torch.cuda.empty_cache()
+        res["faster"] = "flat" if res["flat_ms"] < res["hierarchical_ms"] else "hierarchical"
+        print(json.dumps(res), flush=True)
+        del qI, wI, kI, ks
+        torch.cuda.empty_cache()
+
+
 def make_inputs(w, dev, n_q):
     """Indexer and attention inputs: the key caches of all L tokens, the queries of the n_q rows
     of one step."""
@@ -164,6 +198,8 @@ def main():
                     help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--index-sweep", default="", metavar="L1,L2,...",
+                    help="only time the indexer, hierarchical against flat, at these cache lengths, and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
@@ -175,6 +211,9 @@ def main():
         sys.exit("--steps must be >= 1 and --warmup >= 0")
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.index_sweep:
+        index_sweep([int(x) for x in args.index_sweep.split(",")], args.pooling)
         return
 
     dev = torch.device("cuda:0")

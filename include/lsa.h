@@ -70,6 +70,11 @@ typedef struct lsa_index_params {
                           page lies entirely at or before the query                              */
   int32_t run_align;   /* C: runs are cut at every multiple of C (>= 1)                           */
   int32_t pooling;     /* lsa_pooling of the coarse stage (hierarchical mode only)               */
+  int32_t hi_min_kv;   /* adaptive dispatch between hierarchical and flat indexing (Sec. 3.3: the
+                          hierarchy pays off only beyond a crossover length): with keep_pages > 0,
+                          a call whose cache covers at most hi_min_kv tokens (prefill: n_kv;
+                          decode: max_pages * kv_page_size) runs flat, and its pages_out rows are
+                          all -1. 0: always hierarchical when keep_pages > 0                      */
 } lsa_index_params;
 
 /* A run of consecutive selected positions [start, start+len) inside one C-aligned chunk. */

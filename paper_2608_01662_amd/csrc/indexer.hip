@@ -681,6 +681,136 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 
   }
 }
 
+// ============================================================================ flat mode: dense causal scoring
+// Eq. (7) scored densely (flat mode, prefill). A workgroup of 8 waves takes 8 consecutive query
+// rows (wave w: row r0 + w) and walks the block's eligible keys in 64-key chunks, contiguous in the
+// cache from the first eligible page on. Each chunk is copied into LDS once (its direct loads spread
+// over the 8 waves) and every wave scores it for its own row, so 8 rows share every key byte
+// brought on chip. Two LDS buffers: chunk c+1 is copied while chunk c is scored. Output as the fine
+// stage's in flat mode: slot s of a row holds position p_lo*P + s, with the order key of its Eq. (1)
+// score, or 0 outside the row's eligible range; a row writes its (#eligible pages) * P slots.
+constexpr int kFlatRows = 8;  // query rows per workgroup
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(64 * kFlatRows) void flat_dense_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
+                                                                  const float* __restrict__ w, const void* __restrict__ k,
+                                                                  const float* __restrict__ kscale,
+                                                                  uint32_t* __restrict__ fine_keys, int64_t ldf) {
+  constexpr int KS = D / 16;
+  constexpr int RB = FP8 ? D : 2 * D;
+  constexpr int GR = RB / 16;
+  constexpr int LG = FP8 ? D / 32 : D / 16;
+  constexpr int CB = kFineChunk * RB;  // bytes of one chunk buffer
+  constexpr int NINS = CB / 1024;      // direct loads of 64 x 16 bytes per chunk
+  __shared__ __attribute__((aligned(16))) uint8_t fsm[2 * CB];
+  __shared__ float lsc[2 * kFineChunk];
+  const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, as a scalar
+  const int64_t row0 = (int64_t)blockIdx.x * kFlatRows;
+  const int64_t last = row0 + kFlatRows - 1 < n_rows ? row0 + kFlatRows - 1 : n_rows - 1;
+  const RowInfo rl = row_info(g, last);  // the block's last row has the longest eligible range
+  const int64_t bslots = rl.p_hi >= rl.p_lo ? (rl.p_hi - rl.p_lo + 1) * g.P : 0;
+  const int n_chunks = (int)((bslots + kFineChunk - 1) / kFineChunk);
+  if (n_chunks == 0) return;  // (uniform over the workgroup)
+  const int64_t row = row0 + wv;
+  const bool have_row = row < n_rows;
+  const RowInfo ri = row_info(g, have_row ? row : last);
+  const int64_t nslots = (have_row && ri.p_hi >= ri.p_lo) ? (ri.p_hi - ri.p_lo + 1) * g.P : 0;
+  const int64_t base = rl.p_lo * g.P;  // position of slot 0 (p_lo depends on k_sink only)
+
+  u32x4 a[KS];
+  float wr[16];
+  load_query_operand<D>(q, g.H, have_row ? row : last, lane, a);
+  load_head_weights(w, g.H, have_row ? row : last, lane, wr);
+  const uint8_t* kb = reinterpret_cast<const uint8_t*>(k);
+  uint32_t* const out_row = fine_keys + (have_row ? row : 0) * ldf;
+
+  auto widen = [&](const u32x4 (&raw)[LG], int s) -> u32x4 {
+    if (FP8) {
+      const u32x4 r = raw[s >> 1];
+      return (s & 1) ? fp8x8_to_bf16x8_pk(r.z, r.w) : fp8x8_to_bf16x8_pk(r.x, r.y);
+    }
+    return raw[s];
+  };
+  // LDS layout of a chunk as in the fine stage (row-major rows, granule c of row t at c ^ swz(t));
+  // load m fills slots 64 m + lane, which hold src_off(64 (m % 2) + lane) + 2048 (m / 2) bytes
+  // into the chunk's rows
+  auto src_off = [](int s) { const int t = s / GR; return t * RB + 16 * ((s % GR) ^ fine_swz<D, FP8>(t)); };
+  const uint32_t voff0 = (uint32_t)src_off(lane), voff1 = (uint32_t)src_off(64 + lane);
+  const uint32_t rd0 = (uint32_t)(j * RB + 16 * ((LG * h) ^ fine_swz<D, FP8>(j)));
+  const uint32_t lds0 = lds_addr(fsm), lsc0 = lds_addr(lsc);
+  // chunk c (key positions base + 64 c .. + 63) -> buffer c & 1; this wave's share of the loads.
+  // Positions past the cache (a block whose last page is partly cached) re-read the last key.
+  auto issue = [&](int c) {
+    const int64_t r0 = base + (int64_t)kFineChunk * c;
+    const uint32_t lb = lds0 + (uint32_t)((c & 1) * CB);
+    if (r0 + kFineChunk <= g.n_kv) {
+      const uint8_t* sb = kb + r0 * RB;
+      for (int m = wv; m < NINS; m += kFlatRows) lds_dma<16>(sb + 2048 * (m / 2), (m & 1) ? voff1 : voff0, lb + 1024 * m);
+      if (FP8 && wv == kFlatRows - 1) lds_dma<4>(kscale + r0, 4u * lane, lsc0 + (uint32_t)((c & 1) * 4 * kFineChunk));
+    } else {
+      const int64_t rb = r0 < g.n_kv ? r0 : g.n_kv - 1;
+      const int rmax = (int)(g.n_kv - 1 - rb), rd = (int)(r0 - rb);
+      const uint8_t* sb = kb + rb * RB;
+      for (int m = wv; m < NINS; m += kFlatRows) {
+        const int sl = 64 * m + lane, t = sl / GR, cc = (sl % GR) ^ fine_swz<D, FP8>(t);
+        const int tr = rd + t < rmax ? rd + t : rmax;
+        lds_dma<16>(sb, (uint32_t)(tr * RB + 16 * cc), lb + 1024 * m);
+      }
+      const int tr = rd + lane < rmax ? rd + lane : rmax;
+      if (FP8 && wv == kFlatRows - 1)
+        lds_dma<4>(kscale + rb, (uint32_t)(4 * tr), lsc0 + (uint32_t)((c & 1) * 4 * kFineChunk));
+    }
+  };
+
+  issue(0);
+  uint32_t pk0 = 0, pk1 = 0;  // scores of the previous chunk, stored one chunk late
+  int64_t pslot = -1;
+  for (int c = 0; c < n_chunks; ++c) {
+    vm_wait_barrier<0>();  // every wave's share of chunk c has landed (and its older stores)
+    if (pslot >= 0 && lane < 32) {
+      if (pslot + j < nslots) out_row[pslot + j] = pk0;
+      if (pslot + 32 + j < nslots) out_row[pslot + 32 + j] = pk1;
+    }
+    pslot = -1;
+    if (c + 1 < n_chunks) issue(c + 1);  // its buffer was last read before this barrier
+    const int64_t s0 = (int64_t)kFineChunk * c;
+    if (s0 < nslots) {
+      const uint8_t* cb = fsm + (c & 1) * CB;
+      const float* sb = lsc + (c & 1) * kFineChunk;
+      u32x4 raw0[LG], raw1[LG];
+      uint32_t rd = rd0;
+      asm volatile("" : "+v"(rd));
+#pragma unroll
+      for (int v = 0; v < LG; ++v) {
+        raw0[v] = *reinterpret_cast<const u32x4*>(cb + (rd ^ (16 * v)));
+        raw1[v] = *reinterpret_cast<const u32x4*>(cb + (rd ^ (16 * v)) + 32 * RB);
+      }
+      const float sc0 = FP8 ? sb[j] : 1.f, sc1 = FP8 ? sb[32 + j] : 1.f;
+      f32x16 acc0 = {}, acc1 = {};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        acc0 = mfma32(a[s], widen(raw0, s), acc0);
+        acc1 = mfma32(a[s], widen(raw1, s), acc1);
+      }
+      // key t of the chunk (position base + s0 + t) is scored iff lo <= t <= hi
+      const int64_t p0 = base + s0;
+      const int lo = (int)(ri.lo - p0 < 0 ? -1 : ri.lo - p0 > 64 ? 64 : ri.lo - p0);
+      const int hi = (int)(ri.hi - p0 < 0 ? -1 : ri.hi - p0 > 64 ? 64 : ri.hi - p0);
+      const float v0 = head_reduce(acc0, wr) * sc0;
+      const float v1 = head_reduce(acc1, wr) * sc1;
+      pk0 = (j >= lo && j <= hi) ? score_key(v0) : 0u;
+      pk1 = (32 + j >= lo && 32 + j <= hi) ? score_key(v1) : 0u;
+      pslot = s0;
+    }
+    lds_read_wait();
+  }
+  if (pslot >= 0 && lane < 32) {
+    if (pslot + j < nslots) out_row[pslot + j] = pk0;
+    if (pslot + 32 + j < nslots) out_row[pslot + 32 + j] = pk1;
+  }
+}
+
 // ============================================================================ final top-K_sparse, merge, runs
 // Writes idx/count of one row from lidx[0..cnt) and, if requested, its runs: maximal stretches of
 // consecutive positions, also cut at multiples of C. rstart is LDS scratch of >= cnt entries.
@@ -1056,10 +1186,26 @@ static hipError_t launch_fine_xcd_t(const IndexGeom& g, int64_t n_rows, const ui
   return hipGetLastError();
 }
 
+template <int D, bool FP8>
+static hipError_t launch_flat_dense_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
+                                      const void* k, const float* ks, uint32_t* fine_keys, int64_t ldf, hipStream_t st) {
+  if (n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL((flat_dense_kernel<D, FP8>), dim3((unsigned)((n_rows + kFlatRows - 1) / kFlatRows)),
+                     dim3(64 * kFlatRows), 0, st, g, n_rows, q, w, k, ks, fine_keys, ldf);
+  return hipGetLastError();
+}
+
 hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
                        const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
                        hipStream_t st) {
   const bool paged = g.ctx_len != nullptr, fp8 = g.fp8 != 0;
+  if (!paged && g.M <= 0) {  // flat prefill: dense causal scoring
+    if (max_sel <= 0) return hipSuccess;
+    if (g.D == 128) return fp8 ? launch_flat_dense_t<128, true>(g, n_rows, q, w, k, ks, fine_keys, ldf, st)
+                               : launch_flat_dense_t<128, false>(g, n_rows, q, w, k, ks, fine_keys, ldf, st);
+    return fp8 ? launch_flat_dense_t<64, true>(g, n_rows, q, w, k, ks, fine_keys, ldf, st)
+               : launch_flat_dense_t<64, false>(g, n_rows, q, w, k, ks, fine_keys, ldf, st);
+  }
   if (!paged) {
     if (max_sel <= 0) return hipSuccess;
     if (g.D == 128) return fp8 ? launch_fine_xcd_t<128, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st)
@@ -1120,6 +1266,17 @@ hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_
   else
     hipLaunchKernelGGL((token_select_kernel<1024, true>), grid, dim3(1024), lds, st, g, n_rows, fine_keys, ldf, pages,
                        idx, count, runs, run_count, (int)slots_cap);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n, v);
   return hipGetLastError();
 }
 

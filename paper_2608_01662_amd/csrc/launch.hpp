@@ -41,6 +41,8 @@ hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_
                                const int32_t* pages, int32_t* idx, int32_t* count, int32_t* runs, int32_t* run_count,
                                int64_t slots_cap, hipStream_t st);
 hipError_t prepare_index_kernels();
+// p[0..n) = v (a kernel, so that the call also records correctly inside a captured graph).
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st);
 
 // Sparse attention over gathered rows.
 struct AttnGeom {

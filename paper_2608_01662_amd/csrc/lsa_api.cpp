@@ -56,6 +56,7 @@ lsa_status check_index_params(const lsa_index_params* p) {
   LSA_REQUIRE((int64_t)p->k_sink + p->k_swa + p->k_sparse < (1LL << 30), LSA_ERR_INVALID_ARG, "k_cap too large");
   LSA_REQUIRE(p->pooling == LSA_POOL_MEAN || p->pooling == LSA_POOL_MINMAX, LSA_ERR_INVALID_ARG, "pooling=%d unknown",
               p->pooling);
+  LSA_REQUIRE(p->hi_min_kv >= 0, LSA_ERR_INVALID_ARG, "hi_min_kv=%d < 0", p->hi_min_kv);
   if (p->keep_pages > 0)
     LSA_REQUIRE(p->k_swa >= p->page, LSA_ERR_UNSUPPORTED,
                 "hierarchical mode needs k_swa=%d >= page=%d (scored pages must not reach past the query)", p->k_swa,
@@ -63,10 +64,24 @@ lsa_status check_index_params(const lsa_index_params* p) {
   return LSA_OK;
 }
 
-// Rows of fine-score slots and page-score entries for a given key range.
+// Adaptive dispatch: a hierarchical indexer whose call covers at most hi_min_kv cached tokens runs
+// flat (Eq. 7 over the whole eligible range), where scoring every candidate costs less than the
+// coarse stage plus the recalled pages.
+lsa_index_params effective_params(const lsa_index_params* p, int64_t max_kv) {
+  lsa_index_params e = *p;
+  if (e.keep_pages > 0 && max_kv <= (int64_t)e.hi_min_kv) e.keep_pages = 0;
+  return e;
+}
+
+// Rows of fine-score slots and page-score entries for a given key range. Rows are processed in
+// passes of rows_per_pass so that the workspace stays within kPassBytes however long the rows are
+// (flat mode over a long cache holds one score per cached token per row).
+constexpr size_t kPassBytes = size_t(8) << 30;
+
 struct IndexPlan {
-  int64_t n_pages;     // pages in [0, max_kv)
-  int64_t slots;       // fine-score slots per row
+  int64_t n_pages;        // pages in [0, max_kv)
+  int64_t slots;          // fine-score slots per row
+  int64_t rows_per_pass;  // query rows per pass over the workspace
   size_t off_page_keys, off_pages, off_fine, total;
 };
 
@@ -75,13 +90,18 @@ IndexPlan plan_index(const lsa_index_params* p, int64_t n_rows, int64_t max_kv) 
   pl.n_pages = cdiv(max_kv, p->page);
   const bool hi = p->keep_pages > 0;
   pl.slots = (hi ? (int64_t)p->keep_pages : pl.n_pages) * p->page;
+  const size_t per_row = (size_t)pl.slots * 4 + (hi ? (size_t)(pl.n_pages + p->keep_pages) * 4 : 0);
+  int64_t rpp = (int64_t)(kPassBytes / (per_row > 0 ? per_row : 1));
+  rpp = rpp < 8 ? 8 : rpp / 8 * 8;
+  pl.rows_per_pass = n_rows < rpp ? n_rows : rpp;
+  const size_t r = (size_t)pl.rows_per_pass;
   size_t off = 0;
   pl.off_page_keys = off;
-  if (hi) off += round_up((size_t)n_rows * pl.n_pages * 4, 256);
+  if (hi) off += round_up(r * pl.n_pages * 4, 256);
   pl.off_pages = off;
-  if (hi) off += round_up((size_t)n_rows * p->keep_pages * 4, 256);
+  if (hi) off += round_up(r * p->keep_pages * 4, 256);
   pl.off_fine = off;
-  off += round_up((size_t)n_rows * pl.slots * 4, 256);
+  off += round_up(r * pl.slots * 4, 256);
   pl.total = off;
   return pl;
 }
@@ -122,27 +142,42 @@ lsa_status run_index(const lsa_index_params* p, const lsa::IndexGeom& g, int64_t
   const IndexPlan pl = plan_index(p, n_rows, max_kv);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint32_t* page_keys = reinterpret_cast<uint32_t*>(ws + pl.off_page_keys);
-  int32_t* pages = pages_out ? pages_out : reinterpret_cast<int32_t*>(ws + pl.off_pages);
   uint32_t* fine = reinterpret_cast<uint32_t*>(ws + pl.off_fine);
-  const auto* q16 = static_cast<const uint16_t*>(q);
   hipError_t e = lsa::prepare_index_kernels();
   if (e != hipSuccess) return hip_fail(e, "prepare");
+  const int k_cap = p->k_sink + p->k_swa + p->k_sparse;
   // eligible pages of the last row bound every row's work
   const int64_t max_elig = pl.n_pages;
-  if (g.M > 0) {
-    const int64_t max_tiles = cdiv(max_elig * (g.P / g.B), 32);
-    e = lsa::launch_coarse(g, n_rows, q16, w, static_cast<const uint16_t*>(block_keys), page_keys, pl.n_pages,
-                           max_tiles, st);
-    if (e != hipSuccess) return hip_fail(e, "coarse page scoring");
-    e = lsa::launch_page_select(g, n_rows, page_keys, pl.n_pages, pages, max_elig, st);
-    if (e != hipSuccess) return hip_fail(e, "page selection");
-  }
   const int64_t max_sel = g.M > 0 ? (max_elig < g.M ? max_elig : g.M) : max_elig;
-  e = lsa::launch_fine(g, n_rows, q16, w, k, k_scale, pages, fine, pl.slots, max_sel, st);
-  if (e != hipSuccess) return hip_fail(e, "fine token scoring");
-  e = lsa::launch_token_select(g, n_rows, fine, pl.slots, g.M > 0 ? pages : nullptr, idx, count,
-                               reinterpret_cast<int32_t*>(runs), run_count, pl.slots, st);
-  if (e != hipSuccess) return hip_fail(e, "token selection");
+  for (int64_t r0 = 0; r0 < n_rows; r0 += pl.rows_per_pass) {
+    const int64_t nr = n_rows - r0 < pl.rows_per_pass ? n_rows - r0 : pl.rows_per_pass;
+    // this pass's rows: shift the row-indexed inputs and outputs (prefill: positions; decode:
+    // context lengths and page-table rows)
+    lsa::IndexGeom gp = g;
+    if (g.ctx_len) {
+      gp.ctx_len = g.ctx_len + r0;
+      gp.page_table = g.page_table + r0 * g.max_pages;
+    } else {
+      gp.q_start = g.q_start + r0;
+    }
+    const auto* q16 = static_cast<const uint16_t*>(q) + r0 * g.H * g.D;
+    const float* wp = w + r0 * g.H;
+    int32_t* pages = pages_out ? pages_out + r0 * g.M : reinterpret_cast<int32_t*>(ws + pl.off_pages);
+    if (g.M > 0) {
+      const int64_t max_tiles = cdiv(max_elig * (g.P / g.B), 32);
+      e = lsa::launch_coarse(gp, nr, q16, wp, static_cast<const uint16_t*>(block_keys), page_keys, pl.n_pages,
+                             max_tiles, st);
+      if (e != hipSuccess) return hip_fail(e, "coarse page scoring");
+      e = lsa::launch_page_select(gp, nr, page_keys, pl.n_pages, pages, max_elig, st);
+      if (e != hipSuccess) return hip_fail(e, "page selection");
+    }
+    e = lsa::launch_fine(gp, nr, q16, wp, k, k_scale, pages, fine, pl.slots, max_sel, st);
+    if (e != hipSuccess) return hip_fail(e, "fine token scoring");
+    e = lsa::launch_token_select(gp, nr, fine, pl.slots, g.M > 0 ? pages : nullptr, idx + r0 * k_cap, count + r0,
+                                 runs ? reinterpret_cast<int32_t*>(runs + r0 * k_cap) : nullptr,
+                                 run_count ? run_count + r0 : nullptr, pl.slots, st);
+    if (e != hipSuccess) return hip_fail(e, "token selection");
+  }
   return LSA_OK;
 }
 
@@ -206,7 +241,8 @@ int32_t lsa_index_k_cap(const lsa_index_params* p) {
 
 size_t lsa_index_workspace_size(const lsa_index_params* p, int64_t n_rows, int64_t max_kv) {
   if (check_index_params(p) != LSA_OK || n_rows < 0 || max_kv < 0) return 0;
-  return plan_index(p, n_rows, max_kv).total;
+  const lsa_index_params e = effective_params(p, max_kv);
+  return plan_index(&e, n_rows, max_kv).total;
 }
 
 static lsa_status run_block_cache(const lsa_index_params* p, bool minmax, int64_t n_items, const int64_t* rows,
@@ -251,6 +287,14 @@ lsa_status lsa_block_keys_update(const lsa_index_params* p, int64_t n_rows, cons
                          "block cache update");
 }
 
+// A hierarchical call that the dispatch ran flat recalls no pages: its pages_out rows are all -1.
+static lsa_status clear_pages_if_flat(const lsa_index_params* p, const lsa_index_params* e, int32_t* pages_out,
+                                      int64_t n_rows, hipStream_t st) {
+  if (pages_out == nullptr || e->keep_pages > 0 || n_rows == 0) return LSA_OK;
+  hipError_t err = lsa::launch_fill_i32(pages_out, n_rows * p->keep_pages, -1, st);
+  return err == hipSuccess ? LSA_OK : hip_fail(err, "clear pages_out");
+}
+
 static lsa_status check_index_io(const lsa_index_params* p, const void* q, const float* w, const void* k,
                                  const float* k_scale, const void* block_keys, int64_t n_sub, int32_t* idx,
                                  int32_t* count, lsa_run* runs, int32_t* run_count, void* workspace,
@@ -287,19 +331,22 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
   LSA_REQUIRE(n_q < (1LL << 28), LSA_ERR_UNSUPPORTED, "n_q must be < 2^28 per call (chunk longer prefills)");
   LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
   LSA_REQUIRE(aligned(pages_out, 4), LSA_ERR_INVALID_ARG, "pages_out must be 4-byte aligned");
-  const IndexPlan pl = plan_index(p, n_q, n_kv);
-  s = check_lds(p, pl);
+  const lsa_index_params e = effective_params(p, n_kv);
+  const IndexPlan pl = plan_index(&e, n_q, n_kv);
+  s = check_lds(&e, pl);
   if (s != LSA_OK) return s;
   if (n_q == 0) return LSA_OK;  // nothing to read or write
-  s = check_index_io(p, q, w, k, k_scale, block_keys, n_kv / p->sub_block, idx, count, runs, run_count, workspace,
+  s = check_index_io(&e, q, w, k, k_scale, block_keys, n_kv / p->sub_block, idx, count, runs, run_count, workspace,
                      ws_bytes, pl.total);
   if (s != LSA_OK) return s;
-  lsa::IndexGeom g = make_geom(p);
+  s = clear_pages_if_flat(p, &e, pages_out, n_q, static_cast<hipStream_t>(stream));
+  if (s != LSA_OK) return s;
+  lsa::IndexGeom g = make_geom(&e);
   g.q_start = q_start;
   g.n_kv = n_kv;
   g.n_sub = n_kv / p->sub_block;
-  return run_index(p, g, n_q, n_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count, pages_out, workspace,
-                   static_cast<hipStream_t>(stream));
+  return run_index(&e, g, n_q, n_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count,
+                   e.keep_pages > 0 ? pages_out : nullptr, workspace, static_cast<hipStream_t>(stream));
 }
 
 lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
@@ -322,14 +369,17 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
               "ctx_len, page_table, pages_out must be 4-byte aligned");
   LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
   const int64_t max_kv = (int64_t)max_pages * kv_page_size;
-  const IndexPlan pl = plan_index(p, batch, max_kv);
-  s = check_lds(p, pl);
+  const lsa_index_params e = effective_params(p, max_kv);
+  const IndexPlan pl = plan_index(&e, batch, max_kv);
+  s = check_lds(&e, pl);
   if (s != LSA_OK) return s;
   if (batch == 0) return LSA_OK;  // nothing to read or write
-  s = check_index_io(p, q, w, k, k_scale, block_keys, n_phys * kv_page_size / p->sub_block, idx, count, runs,
+  s = check_index_io(&e, q, w, k, k_scale, block_keys, n_phys * kv_page_size / p->sub_block, idx, count, runs,
                      run_count, workspace, ws_bytes, pl.total);
   if (s != LSA_OK) return s;
-  lsa::IndexGeom g = make_geom(p);
+  s = clear_pages_if_flat(p, &e, pages_out, batch, static_cast<hipStream_t>(stream));
+  if (s != LSA_OK) return s;
+  lsa::IndexGeom g = make_geom(&e);
   g.ctx_len = ctx_len;
   g.page_table = page_table;
   g.max_pages = max_pages;
@@ -337,8 +387,8 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
   g.n_phys = n_phys;
   g.n_kv = n_phys * kv_page_size;
   g.n_sub = g.n_kv / p->sub_block;
-  return run_index(p, g, batch, max_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count, pages_out,
-                   workspace, static_cast<hipStream_t>(stream));
+  return run_index(&e, g, batch, max_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count,
+                   e.keep_pages > 0 ? pages_out : nullptr, workspace, static_cast<hipStream_t>(stream));
 }
 
 size_t lsa_sparse_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int32_t paged) {

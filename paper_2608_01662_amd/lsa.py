@@ -29,7 +29,7 @@ class LSAError(RuntimeError):
 class _IndexParams(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_heads", "head_dim", "key_dtype", "page", "sub_block", "keep_pages",
-        "k_sparse", "k_sink", "k_swa", "run_align", "pooling")]
+        "k_sparse", "k_sink", "k_swa", "run_align", "pooling", "hi_min_kv")]
 
 
 class _AttnParams(ctypes.Structure):
@@ -51,6 +51,7 @@ class IndexParams:
     k_swa: int
     run_align: int
     pooling: str = "mean"    # coarse-stage block summary: "mean" (Eq. 9) or "minmax" (Eq. 13)
+    hi_min_kv: int = 0       # adaptive dispatch: caches of at most this many tokens are indexed flat
 
     @property
     def k_cap(self) -> int:
@@ -64,7 +65,7 @@ class IndexParams:
     def c(self) -> _IndexParams:
         return _IndexParams(self.n_heads, self.head_dim, LSA_KEY_FP8_E4M3FN if self.fp8 else LSA_KEY_BF16,
                             self.page, self.sub_block, self.keep_pages, self.k_sparse, self.k_sink,
-                            self.k_swa, self.run_align, POOLING[self.pooling])
+                            self.k_swa, self.run_align, POOLING[self.pooling], self.hi_min_kv)
 
 
 @dataclass(frozen=True)

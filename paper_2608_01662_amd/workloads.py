@@ -37,6 +37,7 @@ class Workload:
     ctx_hi: int = 0
     kv_page: int = 0             # decode: tokens per cache page
     pooling: str = "mean"        # coarse-stage block summary: "mean" (Eq. 9) or "minmax" (Eq. 13)
+    hi_min_kv: int = 0           # adaptive dispatch: caches of at most this many tokens indexed flat
 
     @property
     def k_cap(self) -> int:
@@ -49,7 +50,7 @@ class Workload:
     def index_params(self):
         from .lsa import IndexParams
         return IndexParams(self.n_heads, self.head_dim, self.fp8, self.page, self.sub_block, self.keep_pages,
-                           self.k_sparse, self.k_sink, self.k_swa, self.run_align, self.pooling)
+                           self.k_sparse, self.k_sink, self.k_swa, self.run_align, self.pooling, self.hi_min_kv)
 
     def attn_params(self):
         from .lsa import MLA, MQA, AttnParams

@@ -75,6 +75,25 @@ def test_unknown_pooling_rejected():
     assert L.lsa_block_minmax(ctypes.byref(c), 4096, FAKE, FAKE, FAKE, None) == INVALID
 
 
+def test_negative_hi_min_kv_rejected():
+    c = P().c()
+    c.hi_min_kv = -1
+    assert lsa.lib().lsa_index_prefill(ctypes.byref(c), 0, 16, 4096, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                       None, None, FAKE, 1 << 40, None) == INVALID
+
+
+def test_adaptive_dispatch_workspace():
+    """Below the dispatch length the workspace is the flat plan's (no page scores), above it the
+    hierarchical one's."""
+    L = lsa.lib()
+    hi = P(hi_min_kv=0)
+    auto = P(hi_min_kv=8192)
+    flat = P(keep_pages=0)
+    ws = lambda prm, kv: L.lsa_index_workspace_size(ctypes.byref(prm.c()), 64, kv)
+    assert ws(auto, 8192) == ws(flat, 8192) != ws(hi, 8192)
+    assert ws(auto, 8193) == ws(hi, 8193)
+
+
 def test_bad_block_cache_arguments():
     """Block-cache calls validate before launching: the rows list of an update must be given and
     8-byte aligned, keys and output 16-byte aligned, a scale exactly for fp8 keys."""

@@ -120,6 +120,32 @@ def test_fullsize_prefill_L1M_paper_hi_setting():
     _prefill_case(w, q_start, w.chunk, w.seq_len, layers=[0], n_random=12, seed=104)
 
 
+def test_fullsize_flat_L131072_row_passes():
+    """Flat indexing (Eq. 7 over every eligible token) of the last 20000 rows of the 128K prefill:
+    512 KB of candidate scores per row, so the library scores the rows in two passes over its
+    workspace (16384 rows, then 3616), each selecting from global memory. Rows on both sides of
+    the pass boundary, the last row and seeded random rows against the oracle."""
+    from dataclasses import replace
+    w = replace(W.L128K_CLI4, keep_pages=0)
+    n, n_q = w.seq_len, 20000
+    q_start = n - n_q
+    prm = w.index_params()
+    qI = synth.device_normal_bf16((n_q, w.n_heads, w.head_dim), w.seed, synth.T_QI, DEV,
+                                  scale=1.0 / math.sqrt(w.head_dim))
+    wI = synth.device_uniform_f32((n_q, w.n_heads), w.seed, synth.T_W, DEV)
+    kI, ks = synth.device_fp8_keys(n, w.head_dim, w.seed, DEV)
+    out = lsa.index_prefill(prm, qI, wI, kI, ks, None, q_start, n_kv=n, runs=True)
+    rows = sorted({0, 1, 16383, 16384, 16385, n_q - 1} |
+                  set(np.random.default_rng(105).integers(0, n_q, 6).tolist()))
+    sel = torch.tensor(rows, device=DEV)
+    rows_t = [q_start + r for r in rows]
+    g_idx, g_cnt = out["idx"][sel].cpu().numpy(), out["count"][sel].cpu().numpy()
+    res = _indexer_oracle(w, _bits(qI[sel]), wI[sel].cpu().numpy(), kI.cpu().numpy(), ks.cpu().numpy(), rows_t, n)
+    stats = P.check_index_rows(w, rows_t, g_idx, g_cnt, None, res)
+    P.check_runs(out["runs"][sel].cpu().numpy(), out["run_count"][sel].cpu().numpy(), g_idx, g_cnt, w.run_align)
+    print(f"flat L=131072 rows {rows_t[0]}..{rows_t[-1]}: index {stats}")
+
+
 def test_fullsize_decode_b64():
     """64 sequences of 16K..128K tokens in randomly permuted 64-token pages, one new token each;
     every sequence is checked."""

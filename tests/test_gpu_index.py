@@ -173,6 +173,24 @@ def test_select_from_global_keys(keep_pages):
     print(w.name, keep_pages, stats)
 
 
+def test_adaptive_dispatch():
+    """hi_min_kv >= n_kv: the hierarchical parameters run flat (the same output as keep_pages = 0,
+    pages_out all -1); hi_min_kv < n_kv: the hierarchical output, unchanged."""
+    from dataclasses import replace
+    w = W.SMALL_CLI
+    inp = P.prefill_inputs(w)
+    hi, _ = _run_prefill(w, inp)
+    flat, _ = _run_prefill(replace(w, keep_pages=0), inp, pages=False)
+    auto_flat, _ = _run_prefill(replace(w, hi_min_kv=w.seq_len), inp)
+    auto_hi, _ = _run_prefill(replace(w, hi_min_kv=w.seq_len - 1), inp)
+    for key in ("idx", "count", "runs", "run_count"):
+        assert np.array_equal(auto_flat[key], flat[key]), key
+        assert np.array_equal(auto_hi[key], hi[key]), key
+    assert np.all(auto_flat["pages"] == -1)
+    assert np.array_equal(auto_hi["pages"], hi["pages"])
+    assert not np.array_equal(hi["idx"], flat["idx"])      # the two modes do differ here
+
+
 def test_keep_all_equals_flat_on_gpu():
     """With M >= #pages the hierarchical kernels must return exactly the flat selection."""
     w = W.SMALL_MLA
