@@ -196,6 +196,10 @@ def main():
                          "chunk (its block-cache update, indexer and attention) against the full cache")
     ap.add_argument("--pooling", default="mean", choices=["mean", "minmax"],
                     help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
+    ap.add_argument("--attn", default="fused", choices=["fused", "split"],
+                    help="sparse attention as one fused pass over S_t (lsa_sparse_attn), or split into the "
+                         "listed part and the contiguous window on two streams, merged by log-sum-exp "
+                         "(lsa_hfa_attn)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--index-sweep", default="", metavar="L1,L2,...",
@@ -238,7 +242,8 @@ def main():
                runs=torch.empty((n_q, w.k_cap, 2), dtype=torch.int32, device=dev),
                run_count=torch.empty((n_q,), dtype=torch.int32, device=dev))
     ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n_q, n)), dtype=torch.uint8, device=dev)
-    ws_attn_n = lsa.attn_workspace_size(aprm, n_q, w.k_cap, False)
+    split_attn = args.attn == "split"
+    ws_attn_n = (lsa.hfa_workspace_size(aprm, n_q) if split_attn else lsa.attn_workspace_size(aprm, n_q, w.k_cap, False))
     ws_attn = torch.empty(max(1, ws_attn_n), dtype=torch.uint8, device=dev)
     O = [torch.empty((n_q, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
     LSE = [torch.empty((n_q, H), dtype=torch.float32, device=dev) for _ in range(w.layers)]
@@ -259,8 +264,12 @@ def main():
         if ev is not None:
             ev[2].record()
         for l in range(w.layers):
-            lsa.sparse_attn(aprm, t["Q"][l], t["KV"][l], t["V"][l], out["idx"], out["count"], out=O[l],
-                            lse=LSE[l], workspace=ws_attn if ws_attn_n else None)
+            if split_attn:
+                lsa.hfa_attn(aprm, t["Q"][l], t["KV"][l], out["idx"], out["count"], q_start, w.k_swa, out=O[l],
+                             lse=LSE[l], workspace=ws_attn)
+            else:
+                lsa.sparse_attn(aprm, t["Q"][l], t["KV"][l], t["V"][l], out["idx"], out["count"], out=O[l],
+                                lse=LSE[l], workspace=ws_attn if ws_attn_n else None)
             if ev is not None:
                 ev[3 + l].record()
 
@@ -320,9 +329,13 @@ def main():
                                "page": w.page, "sub_block": w.sub_block, "keep_pages": w.keep_pages,
                                "k_sparse": w.k_sparse, "k_sink": w.k_sink, "k_swa": w.k_swa,
                                "run_align": w.run_align, "pooling": w.pooling},
-                   "attention": {"kind": w.attn, "heads": H, "d_qk": dqk, "d_v": dv}},
-        "roofline": {"kernel": "mla_attn_kernel", "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                   "attention": {"kind": w.attn, "heads": H, "d_qk": dqk, "d_v": dv,
+                                 "operator": "split (listed part + window, two streams)" if split_attn else "fused"}},
+        "roofline": {"kernel": ("lsa_hfa_attn (two mla_attn_kernel parts + attn_combine_kernel)" if split_attn
+                                else "mla_attn_kernel"),
+                     "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS,
+                     "traffic": None if split_attn else measured_traffic(),
                      "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_avg},
         "breakdown": {
             "block_cache_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,

@@ -212,6 +212,26 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
                            int32_t max_pages, int32_t kv_page_size, int32_t rows_per_seq,
                            void* out, float* lse, void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * Split sparse attention of prefill (Sec. 4.1.1, the hybrid operator): the same result as
+ * lsa_sparse_attn over S_t, computed as two partial attentions merged by online-softmax
+ * (log-sum-exp) rescaling: the listed part of S_t without its sliding window (sink and sparse
+ * positions: the first count[r] - min(k_swa, t+1) entries of the ascending list), and the window
+ * [t - k_swa + 1, t] read as contiguous cache rows. The two run on two streams (the caller's and a
+ * library-owned non-blocking one, default priority, joined by events before the merge), in passes
+ * of 16384 rows. MLA latent cache only, contiguous cache only.
+ *   q_start    position t of row 0 (row r is the query at t = q_start + r); q_start + n_rows <=
+ *              n_kv_rows
+ *   k_swa      the indexer's window size: idx must end with the whole window of each row, as
+ *              lsa_index_prefill writes it (rows shorter than the window hold [0, t])
+ *   workspace  >= lsa_hfa_attn_workspace_size(p, n_rows) bytes, 256-byte aligned (fp32 partials)
+ * Other arguments as lsa_sparse_attn. Calls on one device share the side stream: concurrent calls
+ * from several host threads on one device are serialised by it.
+ */
+size_t lsa_hfa_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows);
+lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv, int64_t n_kv_rows,
+                        const int32_t* idx, const int32_t* count, int32_t k_cap, int64_t q_start, int32_t k_swa,
+                        void* out, float* lse, void* workspace, size_t ws_bytes, void* stream);
 /* Human-readable name of a status code (static string). */
 const char* lsa_status_string(int32_t status);
 

@@ -85,11 +85,22 @@ void mla_attn_kernel(AttnGeom a) {
   const int head = 16 * hq + i16;
   const bool loader = wv < kMlaLoaders;
   const int64_t row = xcd_band(blockIdx.x, a.n_rows);
-  const int split = SPLIT ? (int)blockIdx.y : 0;
+  const int split = SPLIT ? (a.part >= 0 ? a.part : (int)blockIdx.y) : 0;
   int cnt = a.count[row];
   cnt = cnt < 0 ? 0 : (cnt > a.k_cap ? a.k_cap : cnt);
-  const int s0 = split * a.split_len;
-  const int s1 = SPLIT ? (cnt < s0 + a.split_len ? cnt : s0 + a.split_len) : cnt;
+  int s0 = SPLIT && a.part < 0 ? split * a.split_len : 0;
+  int s1 = SPLIT && a.part < 0 ? (cnt < s0 + a.split_len ? cnt : s0 + a.split_len) : cnt;
+  int64_t win0 = -1;  // first cache row of the window part (contiguous rows, no list)
+  if (a.part >= 0) {
+    const int64_t t = a.q_pos0 + row;
+    const int nwin = (int)(a.k_swa < t + 1 ? a.k_swa : t + 1);
+    if (a.part == 0) {
+      s1 = cnt - nwin > 0 ? cnt - nwin : 0;
+    } else {
+      s1 = cnt > 0 ? nwin : 0;  // an empty list (a skipped row) has no window either
+      win0 = t - nwin + 1;
+    }
+  }
   const int n = s1 > s0 ? s1 - s0 : 0;
   const int32_t* slots = a.rows + row * a.k_cap + s0;
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
@@ -137,7 +148,7 @@ void mla_attn_kernel(AttnGeom a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int i = (int)threadIdx.x + 512 * u;
-        v[u] = i < nc ? slots[c0 + i] : -1;
+        v[u] = i < nc ? (win0 >= 0 ? (int)(win0 + c0 + i) : slots[c0 + i]) : -1;
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -446,6 +457,12 @@ hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st) {
     return launch_attn_combine(a, 64, 512, st);
   }
   hipLaunchKernelGGL((mla_attn_kernel<false, kMlaBufs>), dim3((unsigned)a.n_rows), dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st) {
+  if (a.n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL((mla_attn_kernel<true, kMlaBufs>), dim3((unsigned)a.n_rows), dim3(512), 0, st, a);
   return hipGetLastError();
 }
 

@@ -60,11 +60,19 @@ struct AttnGeom {
   int64_t n_rows;
   int n_split, split_len;  // slots per split (multiple of the tile)
   float scale_log2;        // sm_scale * log2(e)
+  // Split by kind of position (Sec. 4.1.1): part -1 = the whole list; 0 = the list without its
+  // window entries (the sliding window is the list's last min(k_swa, t + 1) entries); 1 = the
+  // window [t - k_swa + 1, t] as contiguous cache rows. Parts write split `part` of n_split = 2.
+  int part;
+  int k_swa;
+  int64_t q_pos0;          // position t of row 0
 };
 
 hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st);
 hipError_t launch_mqa_attn(const AttnGeom& a, hipStream_t st);
 hipError_t launch_attn_combine(const AttnGeom& a, int H, int d_v, hipStream_t st);
+// One part (a.part = 0 or 1) of the split attention into the partials a.part_o / a.part_ml.
+hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st);
 hipError_t launch_translate_rows(const int32_t* idx, const int32_t* count, int64_t n_rows, int k_cap,
                                  const int32_t* page_table, int max_pages, int kv_page, int rows_per_seq,
                                  int64_t n_kv_rows, int32_t* out_rows, hipStream_t st);

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "launch.hpp"
 
@@ -441,6 +442,7 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
   a.n_split = pl.n_split;
   a.split_len = pl.split_len;
   a.scale_log2 = p->sm_scale * 1.4426950408889634f;
+  a.part = -1;  // the whole index list
   if (paged) {
     int32_t* rows = reinterpret_cast<int32_t*>(ws + pl.off_rows);
     hipError_t e = lsa::launch_translate_rows(idx, count, n_rows, k_cap, page_table, max_pages, kv_page_size,
@@ -454,6 +456,115 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
   }
   hipError_t e = mla ? lsa::launch_mla_attn(a, st) : lsa::launch_mqa_attn(a, st);
   if (e != hipSuccess) return hip_fail(e, "sparse attention");
+  return LSA_OK;
+}
+
+// ---------------------------------------------------------------- split attention (HFA)
+// Rows per pass of lsa_hfa_attn: the two fp32 partials of a row take 2 * 64 * (512 + 2) * 4 bytes.
+constexpr int64_t kHfaRowsPerPass = 16384;
+constexpr size_t kHfaRowBytes = size_t(2) * 64 * (512 + 2) * 4;
+
+static int64_t hfa_rows_per_pass(int64_t n_rows) { return n_rows < kHfaRowsPerPass ? n_rows : kHfaRowsPerPass; }
+
+size_t lsa_hfa_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows) {
+  if (check_attn_params(p) != LSA_OK || n_rows < 0 || p->latent == 0) return 0;
+  const size_t r = (size_t)hfa_rows_per_pass(n_rows);
+  return round_up(r * 2 * 64 * 512 * 4, 256) + round_up(r * 2 * 64 * 2 * 4, 256);
+}
+
+namespace {
+// The second stream of the split attention and the two events that fork and join it, one set
+// per device, created on first use (default priority, non-blocking).
+struct HfaStreams {
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_hfa_mu;
+HfaStreams g_hfa[64];
+
+hipError_t hfa_streams(HfaStreams** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_hfa_mu);
+  HfaStreams& h = g_hfa[dev];
+  if (h.side == nullptr) {
+    if ((e = hipStreamCreateWithFlags(&h.side, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&h.fork, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&h.join, hipEventDisableTiming)) != hipSuccess) return e;
+  }
+  *out = &h;
+  return hipSuccess;
+}
+}  // namespace
+
+lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv, int64_t n_kv_rows,
+                        const int32_t* idx, const int32_t* count, int32_t k_cap, int64_t q_start, int32_t k_swa,
+                        void* out, float* lse, void* workspace, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  lsa_status s = check_attn_params(p);
+  if (s != LSA_OK) return s;
+  LSA_REQUIRE(p->latent != 0, LSA_ERR_UNSUPPORTED, "the split attention is implemented for the MLA latent cache");
+  LSA_REQUIRE(n_rows >= 0 && k_cap >= 1 && q_start >= 0 && k_swa >= 0, LSA_ERR_INVALID_ARG,
+              "n_rows, q_start, k_swa must be >= 0 and k_cap >= 1");
+  LSA_REQUIRE(n_rows < (1LL << 31), LSA_ERR_UNSUPPORTED, "n_rows must be < 2^31");
+  if (n_rows == 0) return LSA_OK;  // nothing to read or write
+  LSA_REQUIRE(n_kv_rows >= 1 && n_kv_rows < (1LL << 31), LSA_ERR_INVALID_ARG, "n_kv_rows=%lld not in [1, 2^31)",
+              (long long)n_kv_rows);
+  LSA_REQUIRE(q_start + n_rows <= n_kv_rows, LSA_ERR_INVALID_ARG,
+              "q_start + n_rows = %lld exceeds n_kv_rows = %lld (the window reads the cache up to the query)",
+              (long long)(q_start + n_rows), (long long)n_kv_rows);
+  LSA_REQUIRE(q && kv && idx && count && out, LSA_ERR_INVALID_ARG, "q, kv, idx, count and out must be non-NULL");
+  LSA_REQUIRE(aligned(q, 16) && aligned(kv, 16) && aligned(out, 16), LSA_ERR_INVALID_ARG,
+              "q, kv and out must be 16-byte aligned");
+  LSA_REQUIRE(aligned(idx, 4) && aligned(count, 4) && aligned(lse, 4), LSA_ERR_INVALID_ARG,
+              "idx, count and lse must be 4-byte aligned");
+  const size_t need = lsa_hfa_attn_workspace_size(p, n_rows);
+  LSA_REQUIRE(workspace != nullptr && aligned(workspace, 256), LSA_ERR_WORKSPACE,
+              "workspace must be non-NULL and 256-byte aligned");
+  LSA_REQUIRE(ws_bytes >= need, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, need);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  HfaStreams* hs = nullptr;
+  hipError_t e = hfa_streams(&hs);
+  if (e != hipSuccess) return hip_fail(e, "split attention streams");
+  const int64_t rpp = hfa_rows_per_pass(n_rows);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* part_o = reinterpret_cast<float*>(ws);
+  float* part_ml = reinterpret_cast<float*>(ws + round_up((size_t)rpp * 2 * 64 * 512 * 4, 256));
+  for (int64_t r0 = 0; r0 < n_rows; r0 += rpp) {
+    const int64_t nr = n_rows - r0 < rpp ? n_rows - r0 : rpp;
+    lsa::AttnGeom a{};
+    a.q = static_cast<const uint16_t*>(q) + r0 * 64 * 576;
+    a.kv = static_cast<const uint16_t*>(kv);
+    a.n_kv_rows = n_kv_rows;
+    a.rows = idx + r0 * k_cap;
+    a.count = count + r0;
+    a.k_cap = k_cap;
+    a.out = static_cast<uint16_t*>(out) + r0 * 64 * 512;
+    a.lse = lse ? lse + r0 * 64 : nullptr;
+    a.part_o = part_o;
+    a.part_ml = part_ml;
+    a.n_rows = nr;
+    a.n_split = 2;
+    a.split_len = k_cap;
+    a.scale_log2 = p->sm_scale * 1.4426950408889634f;
+    a.k_swa = k_swa;
+    a.q_pos0 = q_start + r0;
+    // the listed non-window part on the caller's stream, the window on the side stream, then the
+    // log-sum-exp merge once both partials exist (each pass reuses the partial buffers, which the
+    // stream order of the merge and the next pass's first kernel protects)
+    if ((e = hipEventRecord(hs->fork, st)) != hipSuccess) return hip_fail(e, "split attention fork");
+    if ((e = hipStreamWaitEvent(hs->side, hs->fork, 0)) != hipSuccess) return hip_fail(e, "split attention fork");
+    a.part = 0;
+    if ((e = lsa::launch_mla_attn_part(a, st)) != hipSuccess) return hip_fail(e, "split attention (listed part)");
+    a.part = 1;
+    if ((e = lsa::launch_mla_attn_part(a, hs->side)) != hipSuccess) return hip_fail(e, "split attention (window)");
+    if ((e = hipEventRecord(hs->join, hs->side)) != hipSuccess) return hip_fail(e, "split attention join");
+    if ((e = hipStreamWaitEvent(st, hs->join, 0)) != hipSuccess) return hip_fail(e, "split attention join");
+    if ((e = lsa::launch_attn_combine(a, 64, 512, st)) != hipSuccess) return hip_fail(e, "split attention merge");
+  }
   return LSA_OK;
 }
 

@@ -117,6 +117,10 @@ def lib() -> ctypes.CDLL:
         L.lsa_sparse_attn.argtypes = [A, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _i32, _i32, _i32, _vp,
                                       _vp, _vp, _sz, _vp]
         L.lsa_sparse_attn.restype = _i32
+        L.lsa_hfa_attn_workspace_size.argtypes = [A, _i64]
+        L.lsa_hfa_attn_workspace_size.restype = _sz
+        L.lsa_hfa_attn.argtypes = [A, _i64, _vp, _vp, _i64, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _sz, _vp]
+        L.lsa_hfa_attn.restype = _i32
         L.lsa_status_string.argtypes = [_i32]
         L.lsa_status_string.restype = ctypes.c_char_p
         L.lsa_last_error.argtypes = []
@@ -273,6 +277,29 @@ def sparse_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, v: torch.Ten
                                  _p(count), k_cap, _p(page_table), max_pages, kv_page_size, rows_per_seq,
                                  _p(out), _p(lse), _p(ws), wsb, _stream(q.device)),
            "lsa_sparse_attn")
+    return out, lse
+
+
+def hfa_workspace_size(prm: AttnParams, n_rows: int) -> int:
+    return int(lib().lsa_hfa_attn_workspace_size(ctypes.byref(prm.c()), n_rows))
+
+
+def hfa_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, idx: torch.Tensor, count: torch.Tensor,
+             q_start: int, k_swa: int, out: torch.Tensor | None = None, lse: torch.Tensor | bool | None = True,
+             workspace: torch.Tensor | None = None):
+    """Split attention (lsa_hfa_attn): listed non-window part and contiguous window on two streams,
+    merged by log-sum-exp rescaling. Returns (out, lse or None) as sparse_attn."""
+    n_rows = q.shape[0]
+    k_cap = idx.shape[1]
+    if out is None:
+        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=q.device)
+    if lse is True:
+        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=q.device)
+    elif lse is False:
+        lse = None
+    ws, wsb = _workspace(hfa_workspace_size(prm, n_rows), q.device, workspace)
+    _check(lib().lsa_hfa_attn(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), kv.shape[0], _p(idx), _p(count), k_cap,
+                              q_start, k_swa, _p(out), _p(lse), _p(ws), wsb, _stream(q.device)), "lsa_hfa_attn")
     return out, lse
 
 

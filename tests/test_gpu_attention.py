@@ -188,3 +188,30 @@ def test_attention_determinism():
     o1, l1 = _gpu_attn(w, a, rows, idx, cnt)
     o2, l2 = _gpu_attn(w, a, rows, idx, cnt)
     assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+@pytest.mark.parametrize("w", [W.SMALL_MLA, W.SMALL_CLI], ids=lambda w: w.name)
+def test_split_attention_parity(w):
+    """Split attention (listed non-window part and contiguous window on two streams, merged by
+    log-sum-exp): every row of a chunk against the oracle's Eq. (3) over the whole list, and
+    against the fused kernel. The lists come from the oracle's indexer (the window part is read
+    from the cache, not from the list, so the lists must hold the whole window: they do), over a
+    chunk whose first rows are shorter than the window."""
+    n = w.seq_len
+    q0, n_q = 0, min(n, 1536)
+    rows = list(range(q0, q0 + n_q))
+    idx, cnt = _oracle_index(w, rows, n)
+    a = _attn_inputs(w, 0, n, n)
+    q = P.bf16_dev(a["q"][rows])
+    kv = P.bf16_dev(a["kv"])
+    o, l = lsa.hfa_attn(w.attn_params(), q, kv, P.to_dev(idx), P.to_dev(cnt), q0, w.k_swa)
+    of, lf = lsa.sparse_attn(w.attn_params(), q, kv, None, P.to_dev(idx), P.to_dev(cnt))
+    torch.cuda.synchronize()
+    o, l, of, lf = o.float().cpu().numpy(), l.cpu().numpy(), of.float().cpu().numpy(), lf.cpu().numpy()
+    sel = list(range(0, n_q, 7)) + [n_q - 1]
+    worst = _check_rows(w, a, [rows[i] for i in sel], idx[sel], cnt[sel], o[sel], l[sel])
+    # against the fused kernel: two bf16 roundings of the same value apart at most
+    assert np.max(np.abs(o - of)) <= 2e-2, np.max(np.abs(o - of))
+    assert np.max(np.abs(l - lf)) <= 2e-3, np.max(np.abs(l - lf))
+    print(w.name, "worst vs oracle", worst, "max |hfa - fused|", float(np.max(np.abs(o - of))))
+
