@@ -447,22 +447,26 @@ __global__ __launch_bounds__(256) void translate_rows_kernel(const int32_t* __re
 // Two tile buffers: one tile in flight while one is consumed. A third buffer (two in flight)
 // measured no faster at the L = 128K shape.
 constexpr int kMlaBufs = 2;
+template <bool SPLIT>
+static void launch_mla_kernel(dim3 grid, const AttnGeom& a, hipStream_t st) {
+  hipLaunchKernelGGL((mla_attn_kernel<SPLIT, kMlaBufs>), grid, dim3(512), 0, st, a);
+}
 
 hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st) {
   if (a.n_rows == 0) return hipSuccess;
   if (a.n_split > 1) {
-    hipLaunchKernelGGL((mla_attn_kernel<true, kMlaBufs>), dim3((unsigned)a.n_rows, (unsigned)a.n_split), dim3(512), 0, st, a);
+    launch_mla_kernel<true>(dim3((unsigned)a.n_rows, (unsigned)a.n_split), a, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_attn_combine(a, 64, 512, st);
   }
-  hipLaunchKernelGGL((mla_attn_kernel<false, kMlaBufs>), dim3((unsigned)a.n_rows), dim3(512), 0, st, a);
+  launch_mla_kernel<false>(dim3((unsigned)a.n_rows), a, st);
   return hipGetLastError();
 }
 
 hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st) {
   if (a.n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL((mla_attn_kernel<true, kMlaBufs>), dim3((unsigned)a.n_rows), dim3(512), 0, st, a);
+  launch_mla_kernel<true>(dim3((unsigned)a.n_rows), a, st);
   return hipGetLastError();
 }
 

@@ -95,28 +95,38 @@ __device__ __forceinline__ void block_sync() { __syncthreads(); }
 // [lds + 1024k + 16 lane, +16). Written as one asm block so that the compiler does not see LDS
 // being written by vector-memory loads: it would otherwise drain every such load in flight before
 // any later LDS read it cannot prove disjoint. Callers order these loads with explicit vmcnt
-// waits and barriers. M0, which holds the LDS base of the loads, is saved and restored.
+// waits and barriers. M0, which holds the LDS base of the loads, is saved and restored; the
+// s_nop after each write of M0 is the wait state before a load may read it.
 __device__ __forceinline__ void lds_dma16x9(const uint8_t* const (&src)[9], uint32_t lds) {
   uint32_t save;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
       "s_mov_b32 m0, %10\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %1, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %2, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %3, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %4, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %5, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %6, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %7, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %8, off\n\t"
       "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
       "global_load_lds_dwordx4 %9, off\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(save)
