@@ -863,6 +863,83 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
   if (threadIdx.x == 0) run_count[row] = nr;
 }
 
+// Threshold of the k largest of the n keys of a row held in global memory (see radix_threshold),
+// in two passes over them instead of five: an 11-bit histogram of the non-zero keys (counting
+// them), then the keys of the bin holding the k-th largest are gathered into LDS, where radix
+// passes over the remaining bits finish. When that bin holds more than cap keys, the radix
+// passes run over the whole row instead. Returns the non-zero count; T = 0, take_eq = 0 when at
+// most k keys are non-zero (every one is selected).
+constexpr int kSelHistBits = 11;
+constexpr int kSelGatherCap = 8192;
+
+template <int NT>
+__device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h11, uint32_t* sub, int* gcnt,
+                                uint32_t* hist, int* wsum, uint32_t& T, int& take_eq) {
+  constexpr int NB = 1 << kSelHistBits;
+  for (int i = threadIdx.x; i < NB; i += NT) h11[i] = 0;
+  if (threadIdx.x == 0) *gcnt = 0;
+  __syncthreads();
+  int nz = 0;
+  for (int i = threadIdx.x; i < n; i += NT) {
+    const uint32_t key = keys[i];
+    if (key != 0u) {
+      atomicAdd(&h11[key >> (32 - kSelHistBits)], 1u);
+      ++nz;
+    }
+  }
+  nz = wave_sum(nz);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = nz;
+  __syncthreads();
+  int n_valid = 0;
+  for (int x = 0; x < NT / 64; ++x) n_valid += wsum[x];
+  T = 0;
+  take_eq = 0;
+  if (n_valid <= k) return n_valid;  // (uniform)
+  __syncthreads();  // wsum is reused below
+  // bin b* holding the k-th largest key, and the count of keys in the bins above it
+  if (threadIdx.x < 64) {
+    constexpr int PER = NB / 64;
+    const int l = threadIdx.x;
+    uint32_t tot = 0;
+    for (int b = 0; b < PER; ++b) tot += h11[PER * l + b];
+    uint32_t suf = tot;  // totals of lanes >= l
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t x = __shfl_down(suf, o);
+      if (l + o < 64) suf += x;
+    }
+    uint32_t above = suf - tot;
+    if (above < (uint32_t)k && suf >= (uint32_t)k) {
+      for (int b = PER - 1; b >= 0; --b) {
+        const uint32_t c = h11[PER * l + b];
+        if (above + c >= (uint32_t)k) {
+          wsum[0] = PER * l + b;
+          wsum[1] = (int)above;
+          break;
+        }
+        above += c;
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t bstar = (uint32_t)wsum[0];
+  const int rem = k - wsum[1];
+  // the boundary bin's keys -> LDS (order is irrelevant: only the threshold and the number of
+  // ties to take are derived from them; select_compact then takes ties in position order)
+  for (int i = threadIdx.x; i < n; i += NT) {
+    const uint32_t key = keys[i];
+    if (key != 0u && (key >> (32 - kSelHistBits)) == bstar) {
+      const int at = atomicAdd(gcnt, 1);
+      if (at < kSelGatherCap) sub[at] = key;
+    }
+  }
+  __syncthreads();
+  const int nb = *gcnt;
+  __syncthreads();
+  if (nb <= kSelGatherCap) radix_threshold<NT>(sub, nb, rem, hist, wsum, T, take_eq);
+  else radix_threshold<NT>(keys, n, k, hist, wsum, T, take_eq);
+  return n_valid;
+}
+
 // Eq. (12) / Eq. (7) then Eq. (6): S_t = sink ++ (top K_sparse candidates, ascending) ++ window;
 // idx padded with -1; runs re-encode idx, cut at gaps and at multiples of C. General version:
 // the candidate keys are staged in LDS (any number that fits), or with GK (rows too long for
@@ -878,11 +955,15 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
   __shared__ int wsum[2 * NT / 64 + 2];
   const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
   // LDS: keys [max(slots_cap, k_cap)] (not with GK), lidx [k_cap], lpages [M], and with GK the
-  // run-start scratch [k_cap] (otherwise the keys area serves for it)
+  // run-start scratch [k_cap] (otherwise the keys area serves for it), the 11-bit histogram, the
+  // gathered boundary-bin keys and their counter
   const int key_words = GK ? 0 : (slots_cap > k_cap ? slots_cap : k_cap);
   int32_t* lidx = reinterpret_cast<int32_t*>(smem + key_words);
   int32_t* lpages = lidx + k_cap;
   int32_t* rstart = GK ? lpages + (g.M > 0 ? g.M : 0) : reinterpret_cast<int32_t*>(smem);
+  uint32_t* h11 = reinterpret_cast<uint32_t*>(rstart + k_cap);
+  uint32_t* gsub = h11 + (1 << kSelHistBits);
+  int* gcnt = reinterpret_cast<int*>(gsub + kSelGatherCap);
 
   const int64_t row = blockIdx.x;
   const RowInfo ri = row_info(g, row);
@@ -904,10 +985,14 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
     if (!GK)
       for (int i = threadIdx.x; i < n; i += NT) smem[i] = fine_keys[row * ldf + i];
     __syncthreads();
-    const int n_valid = block_count_nonzero(keys, n, wsum);
     uint32_t T = 0;
     int take = 0;
-    if (n_valid > g.k_sparse) radix_threshold<NT>(keys, n, g.k_sparse, hist, wsum, T, take);
+    if (GK) {
+      global_threshold<NT>(keys, n, g.k_sparse, h11, gsub, gcnt, hist, wsum, T, take);
+    } else {
+      const int n_valid = block_count_nonzero(keys, n, wsum);
+      if (n_valid > g.k_sparse) radix_threshold<NT>(keys, n, g.k_sparse, hist, wsum, T, take);
+    }
     const int P = g.P;
     const int64_t p_lo = ri.p_lo;
     const int ks = g.k_sink;
@@ -1240,7 +1325,7 @@ size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M) {
   switch (select_mode(slots_cap, k_cap, M)) {
     case SelectMode::kRegisters: return (2 * (size_t)k_cap + m) * 4;
     case SelectMode::kLds: return ((size_t)(slots_cap > k_cap ? slots_cap : k_cap) + k_cap + m) * 4;
-    default: return (2 * (size_t)k_cap + m) * 4;
+    default: return (2 * (size_t)k_cap + m + (1u << kSelHistBits) + kSelGatherCap + 1) * 4;
   }
 }
 
