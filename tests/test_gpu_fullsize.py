@@ -61,7 +61,7 @@ def _check_attention(w, Q, KV, rows, idx, cnt, o, lse):
     return worst
 
 
-def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed):
+def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed, split_attn=False):
     """Indexer + sparse attention for query rows [q_start, q_start + n_q) of one sequence with
     n_kv cached tokens, as the library runs them; checks the sampled rows against the oracle."""
     H, dqk, dv = w.attn_dims
@@ -86,7 +86,10 @@ def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed):
     for layer in layers:
         Q = synth.device_normal_bf16((n_q, H, dqk), w.seed, synth.T_Q + layer, DEV, rows_per_chunk=2048)
         KV = synth.device_normal_bf16((n_kv, dqk), w.seed, synth.T_KV + layer, DEV)
-        o, lse = lsa.sparse_attn(w.attn_params(), Q, KV, None, out["idx"], out["count"])
+        if split_attn:   # listed part and contiguous window on two streams, merged by LSE
+            o, lse = lsa.hfa_attn(w.attn_params(), Q, KV, out["idx"], out["count"], q_start, w.k_swa)
+        else:
+            o, lse = lsa.sparse_attn(w.attn_params(), Q, KV, None, out["idx"], out["count"])
         worst = _check_attention(w, Q, KV, rows, g_idx, g_cnt, o[sel].float().cpu().numpy(),
                                  lse[sel].cpu().numpy())
         print(f"{w.name} layer {layer}: index {stats}, attention worst max|d| {worst[0]:.2e} rel {worst[1]:.2e}")
@@ -102,6 +105,13 @@ def test_fullsize_prefill_L32768():
 def test_fullsize_prefill_L131072_cross_layer():
     w = W.L128K_CLI4
     _prefill_case(w, 0, w.seq_len, w.seq_len, layers=[0, w.layers - 1], n_random=32, seed=102)
+
+
+def test_fullsize_split_attention_L131072():
+    """The split attention (Sec. 4.1.1) at the benchmark's size: 131072 rows in 8 passes of 16384,
+    sampled rows against the oracle's Eq. (3) over the GPU's own index lists."""
+    w = W.L128K_CLI4
+    _prefill_case(w, 0, w.seq_len, w.seq_len, layers=[0], n_random=24, seed=106, split_attn=True)
 
 
 def test_fullsize_prefill_L1M_last_chunk():
