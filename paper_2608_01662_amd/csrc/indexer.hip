@@ -518,6 +518,7 @@ __device__ __forceinline__ int fine_swz(int t) {
 }
 
 constexpr int kFineChunk = 64;  // key rows staged in LDS at a time
+constexpr int kFineRowsPerWave = 4;  // query rows a fine-scoring wave takes in turn
 
 // One direct global->LDS load (16 or 4 bytes per lane; lane i writes LDS bytes [lds + SIZE*i, ..)),
 // issued from asm so that the compiler's wait insertion does not drain it before LDS reads that it
@@ -551,132 +552,135 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 
   __shared__ float lsc[kFineChunk];
   const int lane = threadIdx.x, j = lane & 31, h = lane >> 5;
   const int x = (int)(blockIdx.x & 7);
-  const int64_t row = (int64_t)(blockIdx.x >> 3);
-  if (row >= n_rows) return;
-  const RowInfo ri = row_info(g, row);
-  if (!ri.valid || ri.p_hi < ri.p_lo) return;
-  const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
-  const bool flat = g.M <= 0;
-  const int n_sel = (int)(flat ? n_elig : (n_elig < g.M ? n_elig : g.M));
-  const int P = g.P;
+  // kFineRowsPerWave consecutive query rows, one after the other (fewer, longer-lived waves)
+  const int64_t rbeg = (int64_t)(blockIdx.x >> 3) * kFineRowsPerWave;
+  const int64_t rend = rbeg + kFineRowsPerWave < n_rows ? rbeg + kFineRowsPerWave : n_rows;
+  for (int64_t row = rbeg; row < rend; ++row) {
+    const RowInfo ri = row_info(g, row);
+    if (!ri.valid || ri.p_hi < ri.p_lo) continue;
+    const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
+    const bool flat = g.M <= 0;
+    const int n_sel = (int)(flat ? n_elig : (n_elig < g.M ? n_elig : g.M));
+    const int P = g.P;
 
-  u32x4 a[KS];
-  float wr[16];
-  load_query_operand<D>(q, g.H, row, lane, a);
-  load_head_weights(w, g.H, row, lane, wr);
-  const uint8_t* kb = reinterpret_cast<const uint8_t*>(k);
-  uint32_t* const out_row = fine_keys + row * ldf;
+    u32x4 a[KS];
+    float wr[16];
+    load_query_operand<D>(q, g.H, row, lane, a);
+    load_head_weights(w, g.H, row, lane, wr);
+    const uint8_t* kb = reinterpret_cast<const uint8_t*>(k);
+    uint32_t* const out_row = fine_keys + row * ldf;
 
-  auto widen = [&](const u32x4 (&raw)[LG], int s) -> u32x4 {
-    if (FP8) {
-      const u32x4 r = raw[s >> 1];
-      return (s & 1) ? fp8x8_to_bf16x8_pk(r.z, r.w) : fp8x8_to_bf16x8_pk(r.x, r.y);
-    }
-    return raw[s];
-  };
-  auto tiles_of = [&](int c0) { return P - c0 < kFineChunk ? (P - c0) / 32 : kFineChunk / 32; };  // 1 or 2
-  // LDS layout of a chunk: row-major key rows, 16-byte granule c of row t at granule c ^ swz(t)
-  // (conflict-free reads of one granule by 8 consecutive rows). Load m fills slots 64 m + lane;
-  // src_off(s) is the byte offset, in the chunk's rows, of what slot s holds. It repeats with
-  // period 128 slots up to a multiple of 2048 bytes, so two per-lane offsets serve every load.
-  auto src_off = [](int s) { const int t = s / GR; return t * RB + 16 * ((s % GR) ^ fine_swz<D, FP8>(t)); };
-  const uint32_t voff0 = (uint32_t)src_off(lane), voff1 = (uint32_t)src_off(64 + lane);
-  const uint32_t rd0 = (uint32_t)(j * RB + 16 * ((LG * h) ^ fine_swz<D, FP8>(j)));
-  const uint32_t lds0 = lds_addr(fsm), lsc0 = lds_addr(lsc);
-  // Key rows pg*P + c0 .. + 32 nt - 1 -> the LDS chunk buffer (rows past the last cached key,
-  // possible in flat mode when K_swa < P, re-read the last key; their positions get no score).
-  auto issue = [&](int64_t pg, int c0) {
-    const int nt = tiles_of(c0);
-    const int64_t r0 = pg * P + c0;
-    if (r0 + 32 * nt <= g.n_kv) {
-      const uint8_t* sb = kb + r0 * RB;
-#pragma unroll
-      for (int m = 0; m < GR; ++m)
-        if (m < GR / 2 || nt == 2) lds_dma<16>(sb + 2048 * (m / 2), (m & 1) ? voff1 : voff0, lds0 + 1024 * m);
-      if (FP8 && lane < 32 * nt) lds_dma<4>(kscale + r0, 4u * lane, lsc0);
-    } else {
-      const int64_t rb = r0 < g.n_kv ? r0 : g.n_kv - 1;  // base row; per-lane rows are clamped to >= it
-      const int rmax = (int)(g.n_kv - 1 - rb), rd = (int)(r0 - rb);
-      const uint8_t* sb = kb + rb * RB;
-      for (int m = 0; m < nt * GR / 2; ++m) {
-        const int s = 64 * m + lane, t = s / GR, c = (s % GR) ^ fine_swz<D, FP8>(t);
-        const int tr = rd + t < rmax ? rd + t : rmax;
-        lds_dma<16>(sb, (uint32_t)(tr * RB + 16 * c), lds0 + 1024 * m);
+    auto widen = [&](const u32x4 (&raw)[LG], int s) -> u32x4 {
+      if (FP8) {
+        const u32x4 r = raw[s >> 1];
+        return (s & 1) ? fp8x8_to_bf16x8_pk(r.z, r.w) : fp8x8_to_bf16x8_pk(r.x, r.y);
       }
-      const int tr = rd + lane < rmax ? rd + lane : rmax;
-      if (FP8 && lane < 32 * nt) lds_dma<4>(kscale + rb, (uint32_t)(4 * tr), lsc0);
-    }
-  };
+      return raw[s];
+    };
+    auto tiles_of = [&](int c0) { return P - c0 < kFineChunk ? (P - c0) / 32 : kFineChunk / 32; };  // 1 or 2
+    // LDS layout of a chunk: row-major key rows, 16-byte granule c of row t at granule c ^ swz(t)
+    // (conflict-free reads of one granule by 8 consecutive rows). Load m fills slots 64 m + lane;
+    // src_off(s) is the byte offset, in the chunk's rows, of what slot s holds. It repeats with
+    // period 128 slots up to a multiple of 2048 bytes, so two per-lane offsets serve every load.
+    auto src_off = [](int s) { const int t = s / GR; return t * RB + 16 * ((s % GR) ^ fine_swz<D, FP8>(t)); };
+    const uint32_t voff0 = (uint32_t)src_off(lane), voff1 = (uint32_t)src_off(64 + lane);
+    const uint32_t rd0 = (uint32_t)(j * RB + 16 * ((LG * h) ^ fine_swz<D, FP8>(j)));
+    const uint32_t lds0 = lds_addr(fsm), lsc0 = lds_addr(lsc);
+    // Key rows pg*P + c0 .. + 32 nt - 1 -> the LDS chunk buffer (rows past the last cached key,
+    // possible in flat mode when K_swa < P, re-read the last key; their positions get no score).
+    auto issue = [&](int64_t pg, int c0) {
+      const int nt = tiles_of(c0);
+      const int64_t r0 = pg * P + c0;
+      if (r0 + 32 * nt <= g.n_kv) {
+        const uint8_t* sb = kb + r0 * RB;
+  #pragma unroll
+        for (int m = 0; m < GR; ++m)
+          if (m < GR / 2 || nt == 2) lds_dma<16>(sb + 2048 * (m / 2), (m & 1) ? voff1 : voff0, lds0 + 1024 * m);
+        if (FP8 && lane < 32 * nt) lds_dma<4>(kscale + r0, 4u * lane, lsc0);
+      } else {
+        const int64_t rb = r0 < g.n_kv ? r0 : g.n_kv - 1;  // base row; per-lane rows are clamped to >= it
+        const int rmax = (int)(g.n_kv - 1 - rb), rd = (int)(r0 - rb);
+        const uint8_t* sb = kb + rb * RB;
+        for (int m = 0; m < nt * GR / 2; ++m) {
+          const int s = 64 * m + lane, t = s / GR, c = (s % GR) ^ fine_swz<D, FP8>(t);
+          const int tr = rd + t < rmax ? rd + t : rmax;
+          lds_dma<16>(sb, (uint32_t)(tr * RB + 16 * c), lds0 + 1024 * m);
+        }
+        const int tr = rd + lane < rmax ? rd + lane : rmax;
+        if (FP8 && lane < 32 * nt) lds_dma<4>(kscale + rb, (uint32_t)(4 * tr), lsc0);
+      }
+    };
 
-  // Pipeline over this wave's work items (page, 64-key chunk): the chunk is read from LDS into
-  // registers, the copy of the next chunk into the same buffer starts, and the current one is
-  // scored meanwhile. Scores are stored one item late, so that a store has a whole item's compute
-  // to complete before the next wait on the memory counter (which counts stores too).
-  for (int base = 0; base < n_sel; base += 64) {
-    const int kk = base + lane;
-    // page ids fit in 31 bits (n_kv < 2^31)
-    const int page = kk < n_sel ? (flat ? (int)(ri.p_lo + kk) : pages[row * g.M + kk]) : -1;
-    // this wave's pages in this block (recalled pages are always eligible; checked anyway)
-    const uint64_t mine = __ballot(page >= ri.p_lo && page <= ri.p_hi && (page & 7) == x);
-    if (!mine) continue;
-    // page id held by lane b, as a wave-uniform value
-    auto page_of = [&](int b) { return (int64_t)__builtin_amdgcn_readlane(page, b); };
-    int bit = __builtin_ctzll(mine), c0 = 0;
-    issue(page_of(bit), 0);
-    uint32_t* pdst = nullptr;                   // pending scores: destination, tiles, values
-    int pnt = 0;
-    uint32_t pk0 = 0, pk1 = 0;
-    while (true) {
-      int nbit = bit, nc0 = c0 + kFineChunk;
-      bool has_next = true;
-      if (nc0 >= P) {
-        const uint64_t rest = mine & ~((2ull << bit) - 1ull);  // (2 << 63 wraps to 0: rest = 0)
-        has_next = rest != 0;
-        nbit = has_next ? __builtin_ctzll(rest) : bit;
-        nc0 = 0;
+    // Pipeline over this wave's work items (page, 64-key chunk): the chunk is read from LDS into
+    // registers, the copy of the next chunk into the same buffer starts, and the current one is
+    // scored meanwhile. Scores are stored one item late, so that a store has a whole item's compute
+    // to complete before the next wait on the memory counter (which counts stores too).
+    for (int base = 0; base < n_sel; base += 64) {
+      const int kk = base + lane;
+      // page ids fit in 31 bits (n_kv < 2^31)
+      const int page = kk < n_sel ? (flat ? (int)(ri.p_lo + kk) : pages[row * g.M + kk]) : -1;
+      // this wave's pages in this block (recalled pages are always eligible; checked anyway)
+      const uint64_t mine = __ballot(page >= ri.p_lo && page <= ri.p_hi && (page & 7) == x);
+      if (!mine) continue;
+      // page id held by lane b, as a wave-uniform value
+      auto page_of = [&](int b) { return (int64_t)__builtin_amdgcn_readlane(page, b); };
+      int bit = __builtin_ctzll(mine), c0 = 0;
+      issue(page_of(bit), 0);
+      uint32_t* pdst = nullptr;                   // pending scores: destination, tiles, values
+      int pnt = 0;
+      uint32_t pk0 = 0, pk1 = 0;
+      while (true) {
+        int nbit = bit, nc0 = c0 + kFineChunk;
+        bool has_next = true;
+        if (nc0 >= P) {
+          const uint64_t rest = mine & ~((2ull << bit) - 1ull);  // (2 << 63 wraps to 0: rest = 0)
+          has_next = rest != 0;
+          nbit = has_next ? __builtin_ctzll(rest) : bit;
+          nc0 = 0;
+        }
+        vm_wait<0>();  // this item's keys (and the previous store) have landed
+        const int t0 = j, t1 = 32 + j;
+        u32x4 raw0[LG], raw1[LG];
+        // granule LG h + v of row j sits at byte rd ^ 16 v (row 32 + j: 32 RB further); rd is
+        // re-derived every item so that the compiler keeps one address register, not LG of them
+        uint32_t rd = rd0;
+        asm volatile("" : "+v"(rd));
+  #pragma unroll
+        for (int v = 0; v < LG; ++v) {
+          raw0[v] = *reinterpret_cast<const u32x4*>(fsm + (rd ^ (16 * v)));
+          raw1[v] = *reinterpret_cast<const u32x4*>(fsm + (rd ^ (16 * v)) + 32 * RB);
+        }
+        const float sc0 = FP8 ? lsc[t0] : 1.f, sc1 = FP8 ? lsc[t1] : 1.f;
+        if (pdst != nullptr && lane < 32) {
+          pdst[t0] = pk0;
+          if (pnt == 2) pdst[t1] = pk1;
+        }
+        lds_read_wait();  // the buffer may be refilled once every read of it has returned
+        if (has_next) issue(page_of(nbit), nc0);
+        f32x16 acc0 = {}, acc1 = {};
+  #pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          acc0 = mfma32(a[s], widen(raw0, s), acc0);
+          acc1 = mfma32(a[s], widen(raw1, s), acc1);
+        }
+        // key t of the chunk (position r0 + t) is scored iff lo <= t <= hi (32-bit, wave-uniform bounds)
+        const int64_t r0 = page_of(bit) * P + c0;
+        const int lo = (int)(ri.lo - r0 < 0 ? -1 : ri.lo - r0 > 64 ? 64 : ri.lo - r0);
+        const int hi = (int)(ri.hi - r0 < 0 ? -1 : ri.hi - r0 > 64 ? 64 : ri.hi - r0);
+        const float v0 = head_reduce(acc0, wr) * sc0;
+        const float v1 = head_reduce(acc1, wr) * sc1;
+        pk0 = (t0 >= lo && t0 <= hi) ? score_key(v0) : 0u;
+        pk1 = (t1 >= lo && t1 <= hi) ? score_key(v1) : 0u;
+        pdst = out_row + (int64_t)(base + bit) * P + c0;
+        pnt = tiles_of(c0);
+        if (!has_next) break;
+        bit = nbit;
+        c0 = nc0;
       }
-      vm_wait<0>();  // this item's keys (and the previous store) have landed
-      const int t0 = j, t1 = 32 + j;
-      u32x4 raw0[LG], raw1[LG];
-      // granule LG h + v of row j sits at byte rd ^ 16 v (row 32 + j: 32 RB further); rd is
-      // re-derived every item so that the compiler keeps one address register, not LG of them
-      uint32_t rd = rd0;
-      asm volatile("" : "+v"(rd));
-#pragma unroll
-      for (int v = 0; v < LG; ++v) {
-        raw0[v] = *reinterpret_cast<const u32x4*>(fsm + (rd ^ (16 * v)));
-        raw1[v] = *reinterpret_cast<const u32x4*>(fsm + (rd ^ (16 * v)) + 32 * RB);
+      if (lane < 32) {
+        pdst[j] = pk0;
+        if (pnt == 2) pdst[32 + j] = pk1;
       }
-      const float sc0 = FP8 ? lsc[t0] : 1.f, sc1 = FP8 ? lsc[t1] : 1.f;
-      if (pdst != nullptr && lane < 32) {
-        pdst[t0] = pk0;
-        if (pnt == 2) pdst[t1] = pk1;
-      }
-      lds_read_wait();  // the buffer may be refilled once every read of it has returned
-      if (has_next) issue(page_of(nbit), nc0);
-      f32x16 acc0 = {}, acc1 = {};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        acc0 = mfma32(a[s], widen(raw0, s), acc0);
-        acc1 = mfma32(a[s], widen(raw1, s), acc1);
-      }
-      // key t of the chunk (position r0 + t) is scored iff lo <= t <= hi (32-bit, wave-uniform bounds)
-      const int64_t r0 = page_of(bit) * P + c0;
-      const int lo = (int)(ri.lo - r0 < 0 ? -1 : ri.lo - r0 > 64 ? 64 : ri.lo - r0);
-      const int hi = (int)(ri.hi - r0 < 0 ? -1 : ri.hi - r0 > 64 ? 64 : ri.hi - r0);
-      const float v0 = head_reduce(acc0, wr) * sc0;
-      const float v1 = head_reduce(acc1, wr) * sc1;
-      pk0 = (t0 >= lo && t0 <= hi) ? score_key(v0) : 0u;
-      pk1 = (t1 >= lo && t1 <= hi) ? score_key(v1) : 0u;
-      pdst = out_row + (int64_t)(base + bit) * P + c0;
-      pnt = tiles_of(c0);
-      if (!has_next) break;
-      bit = nbit;
-      c0 = nc0;
-    }
-    if (lane < 32) {
-      pdst[j] = pk0;
-      if (pnt == 2) pdst[32 + j] = pk1;
     }
   }
 }
@@ -1266,7 +1270,8 @@ static hipError_t launch_fine_xcd_t(const IndexGeom& g, int64_t n_rows, const ui
                                     const void* k, const float* ks, const int32_t* pages, uint32_t* fine_keys,
                                     int64_t ldf, hipStream_t st) {
   if (n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL((fine_xcd_kernel<D, FP8>), dim3((unsigned)(n_rows * 8)), dim3(64), 0, st, g, n_rows, q, w, k, ks,
+  const int64_t waves_per_xcd = (n_rows + kFineRowsPerWave - 1) / kFineRowsPerWave;
+  hipLaunchKernelGGL((fine_xcd_kernel<D, FP8>), dim3((unsigned)(waves_per_xcd * 8)), dim3(64), 0, st, g, n_rows, q, w, k, ks,
                      pages, fine_keys, ldf);
   return hipGetLastError();
 }
