@@ -114,6 +114,102 @@ def index_sweep(lengths, pooling):
         torch.cuda.empty_cache()
 
 
+def bench_decode(w, args):
+    """Batched decode step: the indexer for one new token per sequence over the paged key cache
+    (lsa_index_decode), then the paged sparse attention of each layer (lsa_sparse_attn). With
+    --graph the step is captured once into a HIP graph (torch.cuda.CUDAGraph) and replayed, which
+    removes the per-kernel launch cost of this small, launch-bound step. One JSON line."""
+    dev = torch.device("cuda:0")
+    prm, aprm = w.index_params(), w.attn_params()
+    H, dqk, dv = w.attn_dims
+    ctx, table, n_phys = synth.decode_layout(w.seed, w.batch, w.ctx_lo, w.ctx_hi, w.kv_page)
+    n_tok = n_phys * w.kv_page
+    B = w.batch
+    log(f"[bench] {w.name}: {B} sequences, {n_tok} cached tokens in {n_phys} pages")
+    qI = synth.device_normal_bf16((B, w.n_heads, w.head_dim), w.seed, synth.T_QI, dev, scale=1.0 / math.sqrt(w.head_dim))
+    wI = synth.device_uniform_f32((B, w.n_heads), w.seed, synth.T_W, dev)
+    kI, ks = synth.device_fp8_keys(n_tok, w.head_dim, w.seed, dev)
+    bk = lsa.block_keys(prm, kI, ks)
+    Q = [synth.device_normal_bf16((B, H, dqk), w.seed, synth.T_Q + l, dev) for l in range(w.layers)]
+    KV = [synth.device_normal_bf16((n_tok, dqk), w.seed, synth.T_KV + l, dev).view(n_phys, w.kv_page, dqk)
+          for l in range(w.layers)]
+    ctx_d = torch.from_numpy(ctx).to(dev)
+    table_d = torch.from_numpy(table).to(dev)
+    out = dict(idx=torch.empty((B, w.k_cap), dtype=torch.int32, device=dev),
+               count=torch.empty((B,), dtype=torch.int32, device=dev),
+               runs=torch.empty((B, w.k_cap, 2), dtype=torch.int32, device=dev),
+               run_count=torch.empty((B,), dtype=torch.int32, device=dev))
+    ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, B, table.shape[1] * w.kv_page)), dtype=torch.uint8, device=dev)
+    ws_attn = torch.empty(max(1, lsa.attn_workspace_size(aprm, B, w.k_cap, True)), dtype=torch.uint8, device=dev)
+    O = [torch.empty((B, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
+    LSE = [torch.empty((B, H), dtype=torch.float32, device=dev) for _ in range(w.layers)]
+
+    def step():
+        lsa.index_decode(prm, ctx_d, table_d, w.kv_page, n_phys, qI, wI, kI, ks, bk, runs=True, workspace=ws_idx,
+                         out=out)
+        for l in range(w.layers):
+            lsa.sparse_attn(aprm, Q[l], KV[l], None, out["idx"], out["count"], page_table=table_d,
+                            kv_page_size=w.kv_page, out=O[l], lse=LSE[l], workspace=ws_attn)
+
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    # separate timings of the two calls (eager)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
+    lsa.index_decode(prm, ctx_d, table_d, w.kv_page, n_phys, qI, wI, kI, ks, bk, runs=True, workspace=ws_idx, out=out)
+    e[1].record()
+    for l in range(w.layers):
+        lsa.sparse_attn(aprm, Q[l], KV[l], None, out["idx"], out["count"], page_table=table_d, kv_page_size=w.kv_page,
+                        out=O[l], lse=LSE[l], workspace=ws_attn)
+    e[2].record()
+    torch.cuda.synchronize()
+    idx_ms, attn_ms = e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]) / w.layers
+    graph = None
+    if args.graph:
+        s_cap = torch.cuda.Stream()
+        s_cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s_cap):
+            step()                               # one more warm call on the capture stream
+        torch.cuda.current_stream().wait_stream(s_cap)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+    run = graph.replay if graph is not None else step
+    for _ in range(max(1, args.warmup)):
+        run()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    cnt = out["count"].cpu().numpy().astype(np.int64)
+    sum_s = int(cnt.sum())
+    attn_bytes = sum_s * (dqk * 2 + 4) + B * H * (dqk + dv) * 2 + B * H * 4 + B * 4
+    attn_gbs = attn_bytes / (attn_ms * 1e-3) / 1e9
+    res = {
+        "metric": f"LSA decode tokens/s, {B} sequences of {w.ctx_lo // 1024}K-{w.ctx_hi // 1024}K context (indexer+attn)",
+        "value": B / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "context": [int(ctx.min()), int(ctx.max())],
+                   "kv_page": w.kv_page, "layers": w.layers, "hip_graph": bool(graph is not None),
+                   "indexer": {"heads": w.n_heads, "head_dim": w.head_dim, "page": w.page, "keep_pages": w.keep_pages,
+                               "k_sparse": w.k_sparse, "k_sink": w.k_sink, "k_swa": w.k_swa}},
+        "roofline": {"kernel": "mla_attn_kernel (split over the list) + attn_combine_kernel", "bound": "hbm",
+                     "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_ms},
+        "breakdown": {"index_ms_eager": idx_ms, "attn_ms_per_layer_eager": attn_ms,
+                      "mean_index_list_len": sum_s / B},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def make_inputs(w, dev, n_q):
     """Indexer and attention inputs: the key caches of all L tokens, the queries of the n_q rows
     of one step."""
@@ -191,9 +287,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL if not w.decode],
+    ap.add_argument("--workload", default=W.L128K_CLI4.name, choices=[w.name for w in W.FULL],
                     help="single-call prefill workloads time the whole prefill; chunked ones time the last "
-                         "chunk (its block-cache update, indexer and attention) against the full cache")
+                         "chunk (its block-cache update, indexer and attention) against the full cache; "
+                         "the decode workload times one batched decode step")
+    ap.add_argument("--graph", action="store_true", help="decode: replay the step as a captured HIP graph")
     ap.add_argument("--pooling", default="mean", choices=["mean", "minmax"],
                     help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
     ap.add_argument("--attn", default="fused", choices=["fused", "split"],
@@ -223,6 +321,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = W.BY_NAME[args.workload]
+    if w.decode:
+        bench_decode(w, args)
+        return
     if args.pooling != w.pooling:
         from dataclasses import replace
         w = replace(w, name=f"{w.name}_{args.pooling}", pooling=args.pooling)

@@ -188,14 +188,20 @@ struct AttnPlan {
   size_t off_rows, off_po, off_ml, total;
 };
 
+// Workgroups a split attention call aims for: one per CU (the MLA kernel's LDS admits one per CU).
+// Every split re-loads its row's 73 KB of Q and writes 128 KB of fp32 partials, so more, shorter
+// splits cost more than they add in parallelism (64-sequence decode: 0.067 ms per layer at 256
+// workgroups, 0.166 ms at 2048).
+constexpr int64_t kSplitTarget = 256;
+
 AttnPlan plan_attn(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int32_t paged) {
   AttnPlan pl{};
   pl.n_split = 1;
   pl.split_len = k_cap;
   const bool mla = p->latent != 0;
-  if (mla && n_rows > 0 && n_rows < 2048) {
+  if (mla && n_rows > 0 && n_rows < kSplitTarget) {
     // too few rows to fill 256 CUs: split every row's list into 32-token-aligned pieces
-    int64_t want = cdiv(2048, n_rows);
+    int64_t want = cdiv(kSplitTarget, n_rows);
     int64_t max_split = cdiv(k_cap, 32);
     int64_t ns = want < max_split ? want : max_split;
     if (ns > 1) {
