@@ -446,9 +446,14 @@ def main():
             "attn_mfma_frac": attn_flops / (attn_avg * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
             "attn_gather_gbs": sum_s * row_kv_bytes / (attn_avg * 1e-3) / 1e9,
             "attn_tokens_per_s_per_layer": n_q / (attn_avg * 1e-3),
+            "tokens_per_s_layer_equivalent": n_q * w.layers / (ms_per_step * 1e-3),
             "mean_index_list_len": sum_s / n_q,
         },
     }
+    tr = res["roofline"]["traffic"]
+    if tr is not None:   # HBM (data-fabric) bytes from the committed counter passes over this launch time
+        res["breakdown"]["attn_fabric_gbs"] = tr / (attn_avg * 1e-3) / 1e9
+        res["breakdown"]["attn_fabric_frac"] = res["breakdown"]["attn_fabric_gbs"] / HBM_PEAK_GBS
     if not args.no_cpu_baseline:
         log(f"[bench] timing the oracle for ~{args.cpu_seconds:.0f} s on the host")
         res["cpu_baseline"] = cpu_baseline(w, t, args.cpu_seconds, q_start)
