@@ -191,6 +191,25 @@ def test_adaptive_dispatch():
     assert not np.array_equal(hi["idx"], flat["idx"])      # the two modes do differ here
 
 
+@pytest.mark.parametrize("head_dim,fp8", [(128, False), (64, True)])
+@pytest.mark.parametrize("keep_pages", [8, 0])
+def test_index_prefill_other_key_formats(head_dim, fp8, keep_pages):
+    """The kernel instances the five workloads do not reach: bf16 keys with d_I = 128 and fp8 keys
+    with d_I = 64, hierarchical (coarse, page select, fine_xcd) and flat (flat_dense), against the
+    oracle on sampled rows."""
+    from dataclasses import replace
+    w = replace(W.SMALL_CLI, name=f"small_d{head_dim}_{'fp8' if fp8 else 'bf16'}_m{keep_pages}", head_dim=head_dim,
+                fp8=fp8, keep_pages=keep_pages, seq_len=4096)
+    inp = P.prefill_inputs(w)
+    out, _ = _run_prefill(w, inp, pages=keep_pages > 0)
+    rows = _sample_rows(w.seq_len, 11, [w.k_sink + w.k_swa, w.k_sink + w.k_swa + w.page, w.seq_len - 2])
+    res = _oracle_rows(w, inp, rows)
+    stats = P.check_index_rows(w, rows, out["idx"][rows], out["count"][rows],
+                               out["pages"][rows] if "pages" in out else None, res)
+    P.check_runs(out["runs"][rows], out["run_count"][rows], out["idx"][rows], out["count"][rows], w.run_align)
+    print(w.name, stats)
+
+
 def test_keep_all_equals_flat_on_gpu():
     """With M >= #pages the hierarchical kernels must return exactly the flat selection."""
     w = W.SMALL_MLA
