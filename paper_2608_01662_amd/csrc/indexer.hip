@@ -827,42 +827,47 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
   for (int i = threadIdx.x; i < k_cap; i += NT) orow[i] = i < cnt ? lidx[i] : -1;
   if (threadIdx.x == 0) count[row] = cnt;
   if (!runs) return;
-  // a run starts at i = 0, after a gap, or at a position divisible by C
+  // A run starts at i = 0, after a gap, or at a position divisible by C. Thread x scans the
+  // contiguous slice [x E, x E + E) of the list; one block-wide prefix of the per-thread start
+  // counts numbers the runs, and each run is stored as one 8-byte (start, length) pair.
   const int C = g.C;
-  int base = 0;
-  for (int c = 0; c < cnt; c += NT) {
-    const int i = c + threadIdx.x;
-    bool st = false;
-    if (i < cnt) {
-      const int32_t s = lidx[i];
-      st = i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0;
-    }
-    const uint64_t bs = __ballot(st);
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    if (lane == 0) wsum[wv] = __popcll(bs);
-    __syncthreads();
-    int pre = 0, tot = 0;
-    for (int x = 0; x < NT / 64; ++x) {
-      const int v = wsum[x];
-      pre += x < wv ? v : 0;
-      tot += v;
-    }
-    if (st) rstart[base + pre + __popcll(bs & lanemask_lt())] = i;
-    base += tot;
-    __syncthreads();
+  const int E = (cnt + NT - 1) / NT;
+  const int b = (int)threadIdx.x * E, e = b + E < cnt ? b + E : cnt;
+  int mine = 0;
+  for (int i = b; i < e; ++i) {
+    const int32_t s = lidx[i];
+    mine += (i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0) ? 1 : 0;
   }
-  const int nr = base;
-  int32_t* rrow = runs + row * (int64_t)k_cap * 2;
-  for (int r = threadIdx.x; r < k_cap; r += NT) {
-    if (r < nr) {
-      const int s = rstart[r];
-      const int e = r + 1 < nr ? rstart[r + 1] : cnt;
-      rrow[2 * r] = lidx[s];
-      rrow[2 * r + 1] = e - s;
-    } else {
-      rrow[2 * r] = -1;
-      rrow[2 * r + 1] = 0;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int inc = mine;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
+  }
+  if (lane == 63) wsum[wv] = inc;
+  __syncthreads();
+  int r = inc - mine, nr = 0;
+#pragma unroll
+  for (int x = 0; x < NT / 64; ++x) {
+    const int v = wsum[x];
+    r += x < wv ? v : 0;
+    nr += v;
+  }
+  for (int i = b; i < e; ++i) {
+    const int32_t s = lidx[i];
+    if (i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0) rstart[r++] = i;
+  }
+  __syncthreads();
+  int2* rrow = reinterpret_cast<int2*>(runs + row * (int64_t)k_cap * 2);  // 8-byte aligned (checked on the host)
+  for (int q = threadIdx.x; q < k_cap; q += NT) {
+    int2 v = make_int2(-1, 0);
+    if (q < nr) {
+      const int s0 = rstart[q];
+      const int s1 = q + 1 < nr ? rstart[q + 1] : cnt;
+      v = make_int2(lidx[s0], s1 - s0);
     }
+    rrow[q] = v;
   }
   if (threadIdx.x == 0) run_count[row] = nr;
 }

@@ -315,9 +315,9 @@ static lsa_status check_index_io(const lsa_index_params* p, const void* q, const
               "runs and run_count must be both NULL or both non-NULL");
   LSA_REQUIRE(aligned(q, 16) && aligned(k, 16) && aligned(block_keys, 16), LSA_ERR_INVALID_ARG,
               "q, k and block_keys must be 16-byte aligned");
-  LSA_REQUIRE(aligned(w, 4) && aligned(k_scale, 4) && aligned(idx, 4) && aligned(count, 4) && aligned(runs, 4) &&
-                  aligned(run_count, 4),
-              LSA_ERR_INVALID_ARG, "w, k_scale, idx, count, runs, run_count must be 4-byte aligned");
+  LSA_REQUIRE(aligned(w, 4) && aligned(k_scale, 4) && aligned(idx, 4) && aligned(count, 4) && aligned(run_count, 4),
+              LSA_ERR_INVALID_ARG, "w, k_scale, idx, count, run_count must be 4-byte aligned");
+  LSA_REQUIRE(aligned(runs, 8), LSA_ERR_INVALID_ARG, "runs must be 8-byte aligned");
   LSA_REQUIRE(need == 0 || (workspace != nullptr && aligned(workspace, 256)), LSA_ERR_WORKSPACE,
               "workspace must be non-NULL and 256-byte aligned");
   LSA_REQUIRE(ws_bytes >= need, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, need);

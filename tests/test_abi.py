@@ -117,6 +117,7 @@ def test_bad_index_arguments():
     assert prefill(P(fp8=False)) == INVALID                                   # bf16 must not get scales
     assert prefill(prm, bk=None) == INVALID                                   # HI needs mean keys
     assert prefill(prm, runs=FAKE, rc=None) == INVALID
+    assert prefill(prm, runs=ctypes.c_void_p(0x100004), rc=FAKE) == INVALID   # runs: 8-byte (start, len) stores
     assert prefill(prm, q=MISALIGNED) == INVALID
     assert prefill(prm, ws=None) == WORKSPACE
     assert prefill(prm, wsb=16) == WORKSPACE
