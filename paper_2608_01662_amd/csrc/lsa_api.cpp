@@ -332,8 +332,9 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
   lsa_status s = check_index_params(p);
   if (s != LSA_OK) return s;
   LSA_REQUIRE(q_start >= 0 && n_q >= 0 && n_kv >= 0, LSA_ERR_INVALID_ARG, "negative q_start / n_q / n_kv");
-  LSA_REQUIRE(q_start + n_q <= n_kv, LSA_ERR_INVALID_ARG, "q_start + n_q = %lld exceeds n_kv = %lld",
-              (long long)(q_start + n_q), (long long)n_kv);
+  LSA_REQUIRE(q_start <= n_kv && n_q <= n_kv - q_start, LSA_ERR_INVALID_ARG,
+              "rows [q_start, q_start + n_q) = [%lld, +%lld) exceed n_kv = %lld", (long long)q_start, (long long)n_q,
+              (long long)n_kv);
   LSA_REQUIRE(n_kv < (1LL << 31), LSA_ERR_UNSUPPORTED, "n_kv must be < 2^31 (int32 positions)");
   LSA_REQUIRE(n_q < (1LL << 28), LSA_ERR_UNSUPPORTED, "n_q must be < 2^28 per call (chunk longer prefills)");
   LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
@@ -495,10 +496,17 @@ hipError_t hfa_streams(HfaStreams** out) {
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> lk(g_hfa_mu);
   HfaStreams& h = g_hfa[dev];
-  if (h.side == nullptr) {
-    if ((e = hipStreamCreateWithFlags(&h.side, hipStreamNonBlocking)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&h.fork, hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&h.join, hipEventDisableTiming)) != hipSuccess) return e;
+  if (h.side == nullptr) {  // all three objects, or none (a failed call leaves nothing half-made)
+    HfaStreams n;
+    if ((e = hipStreamCreateWithFlags(&n.side, hipStreamNonBlocking)) == hipSuccess &&
+        (e = hipEventCreateWithFlags(&n.fork, hipEventDisableTiming)) == hipSuccess &&
+        (e = hipEventCreateWithFlags(&n.join, hipEventDisableTiming)) == hipSuccess) {
+      h = n;
+    } else {
+      if (n.fork) (void)hipEventDestroy(n.fork);
+      if (n.side) (void)hipStreamDestroy(n.side);
+      return e;
+    }
   }
   *out = &h;
   return hipSuccess;
@@ -518,9 +526,10 @@ lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q,
   if (n_rows == 0) return LSA_OK;  // nothing to read or write
   LSA_REQUIRE(n_kv_rows >= 1 && n_kv_rows < (1LL << 31), LSA_ERR_INVALID_ARG, "n_kv_rows=%lld not in [1, 2^31)",
               (long long)n_kv_rows);
-  LSA_REQUIRE(q_start + n_rows <= n_kv_rows, LSA_ERR_INVALID_ARG,
-              "q_start + n_rows = %lld exceeds n_kv_rows = %lld (the window reads the cache up to the query)",
-              (long long)(q_start + n_rows), (long long)n_kv_rows);
+  LSA_REQUIRE(q_start <= n_kv_rows && n_rows <= n_kv_rows - q_start, LSA_ERR_INVALID_ARG,
+              "rows [q_start, q_start + n_rows) = [%lld, +%lld) exceed n_kv_rows = %lld (the window reads the "
+              "cache up to the query)",
+              (long long)q_start, (long long)n_rows, (long long)n_kv_rows);
   LSA_REQUIRE(q && kv && idx && count && out, LSA_ERR_INVALID_ARG, "q, kv, idx, count and out must be non-NULL");
   LSA_REQUIRE(aligned(q, 16) && aligned(kv, 16) && aligned(out, 16), LSA_ERR_INVALID_ARG,
               "q, kv and out must be 16-byte aligned");

@@ -111,6 +111,7 @@ def test_bad_block_cache_arguments():
 def test_bad_index_arguments():
     prm = P()
     assert prefill(prm, q_start=4090, n_q=16, n_kv=4096) == INVALID           # rows past the cache
+    assert prefill(prm, q_start=(1 << 63) - 8, n_q=16) == INVALID               # no signed overflow in the bound
     assert prefill(prm, n_q=-1) == INVALID
     assert prefill(prm, q=None) == INVALID
     assert prefill(prm, ks=None) == INVALID                                   # fp8 needs scales
@@ -163,6 +164,30 @@ def test_bad_attention_arguments():
     assert attn(q=MISALIGNED) == INVALID
     assert attn(table=FAKE, max_pages=0) == INVALID
     assert attn(n_rows=8, table=FAKE, max_pages=4, kv_page=64, ws=None) == WORKSPACE
+
+
+def test_bad_split_attention_arguments():
+    """lsa_hfa_attn validates on the host before touching streams or events."""
+    L = lsa.lib()
+    mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+
+    def hfa(prm=mla, n_rows=8, q=FAKE, kv=FAKE, n_kv=4096, idx=FAKE, cnt=FAKE, k_cap=64, q_start=0, k_swa=32,
+            out=FAKE, lse=None, ws=FAKE, wsb=1 << 40):
+        return L.lsa_hfa_attn(ctypes.byref(prm.c()), n_rows, q, kv, n_kv, idx, cnt, k_cap, q_start, k_swa, out, lse,
+                              ws, wsb, None)
+    assert hfa(prm=lsa.AttnParams(sm_scale=0.1, **lsa.MQA)) == UNSUPPORTED     # MLA latent cache only
+    assert hfa(q_start=4090) == INVALID                                        # window past the cache
+    assert hfa(q_start=(1 << 63) - 4) == INVALID                               # no signed overflow
+    assert hfa(k_swa=-1) == INVALID
+    assert hfa(k_cap=0) == INVALID
+    assert hfa(q=MISALIGNED) == INVALID
+    assert hfa(idx=None) == INVALID
+    assert hfa(ws=None) == WORKSPACE
+    assert hfa(wsb=16) == WORKSPACE
+    assert hfa(n_rows=0, q=None, idx=None, cnt=None, out=None, ws=None, wsb=0) == OK
+    # two fp32 partials (O and (m, l)) per row and head, for at most 16384 rows per pass
+    assert L.lsa_hfa_attn_workspace_size(ctypes.byref(mla.c()), 100) == 100 * 2 * 64 * (512 + 2) * 4
+    assert L.lsa_hfa_attn_workspace_size(ctypes.byref(mla.c()), 131072) == 16384 * 2 * 64 * (512 + 2) * 4
 
 
 def test_workspace_sizes():
