@@ -56,10 +56,13 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 //
 // The row's index list is validated once into LDS (-1 for entries to skip). Tiles of 32 gathered
 // latent rows are moved by direct global->LDS loads into NBUF rotating buffers (NBUF - 1 tiles in
-// flight while one is consumed); waves 0..3 issue them. Tile layout is chunk-major: 16-byte chunk
-// c (dims 8c..8c+7) of token t sits at c*512 + (t ^ kMlaSwz*(c&1))*16, so the K-operand reads are
-// 256 contiguous bytes per 16 lanes and the transposed V reads of two neighbouring chunks land in
-// disjoint bank halves (the LDS bank-conflict counter reads zero for this kernel).
+// flight while one is consumed); waves 0..3 issue them. Tile layout: 1 KB blocks of 8 tokens x 8
+// chunks (chunk c = dims 8c..8c+7): token t = 8o + j, chunk c sits in block 9o + c / 8 at 16-byte
+// slot 8j + ((c % 8) ^ mla_swz(o, j)), mla_swz(o, j) = (j & 6) | (o & 1). One direct load fills
+// one block, eight consecutive lanes taking one whole 128-byte line of one row (8 rows per load;
+// a load of 2 lanes per row touched 32 rows and cost about 4% more time at L = 128K), and the XOR
+// keeps the K-operand reads (16 tokens, one chunk) and the transposed V reads (4 tokens x 4 chunks
+// per half-wave) free of LDS bank conflicts (checked exhaustively on the host when it was chosen).
 //
 // Schedules that were measured and not kept: running the two wave groups half a tile apart
 // (ping-pong) is slower here, because the 36 KB of LDS writes a tile refill makes hold up the
@@ -70,7 +73,8 @@ constexpr int kMlaTile = 36 * 1024;  // 72 chunks x 32 tokens x 16 bytes
 constexpr int kMlaXch = 8 * 2048;    // partial-score exchange, 2 KB per wave
 constexpr int kMlaLoaders = 4;       // waves that issue the direct loads
 constexpr int kMlaLoads = 9;         // direct loads per loader wave per tile (36 x 1 KB)
-constexpr int kMlaSwz = 12;
+__device__ __forceinline__ int mla_swz(int o, int j) { return (j & 6) | (o & 1); }
+constexpr int kMlaHalf = 18 * 1024;  // the second 16 tokens of a tile start 18 blocks later
 constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
 
 template <bool SPLIT, int NBUF>
@@ -118,22 +122,34 @@ void mla_attn_kernel(AttnGeom a) {
   for (int c = 0; c < 16; ++c) o[c] = f32x4{};
   float m = -INFINITY, l = 0.f;
 
-  // K operand (token 16mt + i16, chunk 36kw + 4s + g; chunk parity = g & 1)
-  const int k_off = (36 * kw + g) * 512 + (i16 ^ (kMlaSwz * (g & 1))) * 16;
+  // K operand of k-step s, M-tile mt: token 16mt + i16 = 8(2mt + i16/8) + (i16 % 8), chunk
+  // 36kw + 4s + g = 8 (s'/2) + 4 (s' % 2) + g with s' = s + 9kw. Two base offsets, for even and odd
+  // s; the rest is an immediate (s/2 blocks, mt * 18 blocks).
+  const int ksw = mla_swz(i16 >> 3, i16 & 7);
+  const int k_row = 9 * (i16 >> 3) * 1024 + 8 * (i16 & 7) * 16;
+  const int k_p0 = k_row + ((0 + g) ^ ksw) * 16, k_p1 = k_row + ((4 + g) ^ ksw) * 16;
+  const int k_even = kw ? k_p1 + 4 * 1024 : k_p0;       // s even: s' % 2 = kw, block s'/2 = s/2 + 4kw
+  const int k_odd = kw ? k_p0 + 5 * 1024 : k_p1;        // s odd: s' % 2 = 1 - kw, block (s-1)/2 + 5kw
   // V^T operand of value block c: source lane (vq, gq) supplies token 4g + vq (and +16), dims
-  // 256kw + 16c + 4gq .. +3, i.e. chunk 32kw + 2c + gq/2 (parity gq/2), byte 8(gq&1).
+  // 256kw + 16c + 4gq .. +3, i.e. token 8(g/2) + 4(g % 2) + vq, chunk 32kw + 2c + gq/2 = block
+  // 4kw + c/4, chunk 2(c % 4) + gq/2 of it, byte 8(gq % 2): one base offset per c % 4.
   const int vq = i16 >> 2, gq = i16 & 3;
-  const int v_off = (32 * kw + (gq >> 1)) * 512 + ((4 * g + vq) ^ (kMlaSwz * (gq >> 1))) * 16 + (gq & 1) * 8;
-  // Direct load K (= 9 wv + k) moves chunks (2K, 2K+1) of the 32 tokens: lane (j, h) fills slot j
-  // of chunk 2K + h, i.e. token j ^ kMlaSwz*h, from bytes 16h + 32K of that token's row.
-  const int lj = lane & 31, lh = lane >> 5;
-  const int dma_tok = lj ^ (kMlaSwz * lh);
-  const int64_t dma_col = 16 * lh + 32 * (kMlaLoads * wv);
+  const int vj = 4 * (g & 1) + vq, vsw = mla_swz(g >> 1, vj);
+  int v_off[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    v_off[u] = (9 * (g >> 1) + 4 * kw) * 1024 + (8 * vj + ((2 * u + (gq >> 1)) ^ vsw)) * 16 + (gq & 1) * 8;
+  // Direct load k of loader wave w fills block 9w + k (tokens 8w.., chunks 8k..): lane 8j + u takes
+  // token 8w + j, chunk 8k + (u ^ mla_swz(w, j)), 16 bytes of one 128-byte line per lane.
+  const int lj = lane & 31;  // token of this lane's validity bit in the softmax mask
+  const int dj = lane >> 3;
+  const int dma_tok = 8 * wv + dj;
+  const int64_t dma_col = ((lane & 7) ^ mla_swz(wv, dj)) * 16;
   auto issue = [&](int tile, int buf) {
     const int r = ids[tile * kMlaT + dma_tok];
     const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
-    const uint8_t* const srcs[kMlaLoads] = {src,       src + 32,  src + 64,  src + 96, src + 128,
-                                            src + 160, src + 192, src + 224, src + 256};
+    const uint8_t* const srcs[kMlaLoads] = {src,       src + 128, src + 256, src + 384,  src + 512,
+                                            src + 640, src + 768, src + 896, src + 1024};
     lds_dma16x9(srcs, lds_addr(lds + buf * kMlaTile + wv * (kMlaLoads * 1024)));
   };
 
@@ -188,7 +204,8 @@ void mla_attn_kernel(AttnGeom a) {
 #pragma unroll
       for (int s = 0; s < 9; ++s)
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) ka[2 * s + mt] = *reinterpret_cast<const u32x4*>(tb + k_off + s * 2048 + mt * 256);
+        for (int mt = 0; mt < 2; ++mt)
+          ka[2 * s + mt] = *reinterpret_cast<const u32x4*>(tb + ((s & 1) ? k_odd : k_even) + (s >> 1) * 1024 + mt * kMlaHalf);
       __builtin_amdgcn_sched_barrier(0);  // keep the scheduler from sinking the reads again
       f32x4 sacc[2] = {f32x4{}, f32x4{}};
 #pragma unroll
@@ -243,12 +260,14 @@ void mla_attn_kernel(AttnGeom a) {
                         pack_bf16x2(p[6], p[7])};
       // ---- O^T += V^T P^T over this wave's 256 value columns; V^T via transposed LDS reads
       // (V operands requested in two batches of eight, again to pay the LDS latency rarely)
-      const uint8_t* vb = tb + v_off;
 #pragma unroll
       for (int c8 = 0; c8 < 16; c8 += 8) {
         u32x4 va[8];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) va[c] = tr16_pair(vb + (c8 + c) * 1024, vb + (c8 + c) * 1024 + 256);
+        for (int c = 0; c < 8; ++c) {
+          const uint8_t* vb = tb + v_off[(c8 + c) & 3] + ((c8 + c) >> 2) * 1024;
+          va[c] = tr16_pair(vb, vb + kMlaHalf);
+        }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int c = 0; c < 8; ++c) o[c8 + c] = mfma16(va[c], pb, o[c8 + c]);
