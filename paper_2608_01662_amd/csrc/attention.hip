@@ -463,9 +463,10 @@ __global__ __launch_bounds__(256) void translate_rows_kernel(const int32_t* __re
 }
 
 // ============================================================================ host launchers
-// Three tile buffers: two tiles in flight while one is consumed (0.7% faster than two buffers at
-// the L = 128K shape, measured back to back on one GPU).
-constexpr int kMlaBufs = 3;
+// Two tile buffers: one tile in flight while one is consumed. With whole-line loads this measured
+// 2% faster than three buffers (two tiles in flight) at the L = 128K shape; with the earlier
+// 32-byte-per-row loads three buffers had been 0.7% faster.
+constexpr int kMlaBufs = 2;
 template <bool SPLIT>
 static void launch_mla_kernel(dim3 grid, const AttnGeom& a, hipStream_t st) {
   hipLaunchKernelGGL((mla_attn_kernel<SPLIT, kMlaBufs>), grid, dim3(512), 0, st, a);
