@@ -153,7 +153,7 @@ def sub_block_mean_keys(k_hat, sub_block: int) -> np.ndarray:
     """
     k_hat = np.asarray(k_hat, np.float64)
     n_sub = k_hat.shape[0] // sub_block
-    means = k_hat[: n_sub * sub_block].reshape(n_sub, sub_block, -1).mean(axis=1)
+    means = k_hat[: n_sub * sub_block].reshape(n_sub, sub_block, k_hat.shape[1]).mean(axis=1)
     return bf16_bits_to_f64(f64_to_bf16_bits(means))
 
 
@@ -167,7 +167,10 @@ def sub_block_minmax_keys(k_hat, sub_block: int):
     """
     k_hat = np.asarray(k_hat, np.float64)
     n_sub = k_hat.shape[0] // sub_block
-    blocks = k_hat[: n_sub * sub_block].reshape(n_sub, sub_block, -1)
+    blocks = k_hat[: n_sub * sub_block].reshape(n_sub, sub_block, k_hat.shape[1])
+    if n_sub == 0:  # a cache shorter than one sub-block has no block keys
+        empty = np.zeros((0, k_hat.shape[1]))
+        return empty, empty.copy()
     k_max = bf16_bits_to_f64(f64_to_bf16_bits(blocks.max(axis=1)))
     k_min = bf16_bits_to_f64(f64_to_bf16_bits(blocks.min(axis=1)))
     return k_max, k_min

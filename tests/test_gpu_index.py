@@ -371,3 +371,56 @@ def test_decode_bad_rows_are_skipped():
     torch.cuda.synchronize()
     assert out["count"][0].item() == 0 and out["count"][1].item() == 0
     assert out["count"][2].item() > 0
+
+
+@pytest.mark.parametrize("w", [W.SMALL_DECODE, W.SMALL_DECODE_MINMAX], ids=lambda w: w.name)
+def test_decode_short_contexts(w):
+    """Paged decode at the context lengths where the streaming split changes shape: one token,
+    shorter than sink + window, exactly sink + window (E_t empty), one past it, page edges, and
+    just above M * P eligible tokens (the first context whose pages are not all recalled). Indexer
+    and paged attention against the oracle, row by row."""
+    P_ = w.kv_page
+    kw = w.k_sink + w.k_swa
+    ctx = np.array([1, 2, w.k_sink + 1, kw - 1, kw, kw + 1, P_, P_ + 1, 2 * P_ + kw, 3 * P_,
+                    w.keep_pages * P_ + kw, w.keep_pages * P_ + kw + P_ + 1], np.int32)
+    B = ctx.size
+    n_pages = (ctx + P_ - 1) // P_
+    n_phys = int(n_pages.sum())
+    perm = np.random.default_rng(11).permutation(n_phys).astype(np.int32)
+    table = np.full((B, int(n_pages.max())), -1, np.int32)
+    off = 0
+    for b in range(B):
+        table[b, :n_pages[b]] = perm[off:off + n_pages[b]]
+        off += n_pages[b]
+    inp = synth.indexer_inputs(w.seed + 7, B, n_phys * P_, w.n_heads, w.head_dim, w.fp8)
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_keys(prm, k, ks)
+    out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), P_, n_phys, q, wt, k, ks, bk, pages=True)
+    torch.cuda.synchronize()
+    res_dev = {key: v for key, v in out.items()}
+    out = {key: v.cpu().numpy() for key, v in out.items()}
+    prmo = P.oracle_params(w)
+    k_hat_pool = P.oracle_keys(inp).reshape(n_phys, P_, -1)
+    qf = orc.bf16_bits_to_f64(inp["q"])
+    rows_t, res = [], []
+    for b in range(B):
+        t = int(ctx[b]) - 1
+        k_log = orc.logical_rows(k_hat_pool, table[b], t + 1, P_)
+        res.append(orc.index_row(t, qf[b], inp["w"][b], k_log, P.oracle_block_cache(w, k_log), prmo))
+        rows_t.append(t)
+    P.check_index_rows(w, rows_t, out["idx"], out["count"], out["pages"], res)
+    P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
+    assert out["count"][0] == 1 and out["idx"][0, 0] == 0
+    # paged attention over those index lists
+    H, dqk, dv = w.attn_dims
+    a = synth.attention_inputs(w.seed + 7, 0, B, n_phys * P_, H, dqk, dv, latent=True)
+    o, lse = lsa.sparse_attn(w.attn_params(), P.bf16_dev(a["q"]), P.bf16_dev(a["kv"]).view(n_phys, P_, dqk), None,
+                             res_dev["idx"], res_dev["count"], page_table=P.to_dev(table), kv_page_size=P_)
+    torch.cuda.synchronize()
+    pool = a["kv"].reshape(n_phys, P_, dqk)
+    for b in range(B):
+        t = int(ctx[b]) - 1
+        kv_log = orc.logical_rows(pool, table[b], t + 1, P_)
+        oref, lref = orc.attention_for_set(a["q"][b], kv_log, None, out["idx"][b, :out["count"][b]], dv, w.sm_scale)
+        P.check_attention_row(o[b].float().cpu().numpy(), lse[b].cpu().numpy(), oref, lref, f"seq {b} (ctx {ctx[b]})")
