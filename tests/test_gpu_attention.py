@@ -125,6 +125,28 @@ def test_closed_forms_and_edge_lists(attn):
         P.check_attention_row(o[i], l[i], oref, lref, f"row {i}")
 
 
+def test_long_lists_beyond_one_staging_pass():
+    """MLA index lists longer than the 8192 entries the kernel stages in LDS at a time: the list is
+    walked in several passes (8192 = exactly one pass, 8193 = one entry into the second, and two
+    longer ones), against the oracle."""
+    from dataclasses import replace
+    w = replace(W.SMALL_MLA, seq_len=20000)
+    n_kv = w.seq_len
+    a = _attn_inputs(w, 0, 4, n_kv)
+    k_cap = 16448
+    counts = [8192, 8193, 12345, 16448]
+    g = np.random.default_rng(5)
+    idx = np.full((4, k_cap), -1, np.int32)
+    cnt = np.array(counts, np.int32)
+    for i, c in enumerate(counts):
+        idx[i, :c] = np.sort(g.choice(n_kv, c, replace=False))
+    o, l = _gpu_attn(w, a, list(range(4)), idx, cnt)
+    H, dqk, dv = w.attn_dims
+    for i in range(4):
+        oref, lref = orc.attention_for_set(a["q"][i], a["kv"], a["v"], idx[i, :cnt[i]], dv, w.sm_scale)
+        P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({cnt[i]} entries)")
+
+
 def test_cross_layer_reuse():
     """One index list feeds several layers (Sec. 3.2): each layer's output matches the oracle on
     its own Q and KV, and the shared list is left byte-identical."""
