@@ -136,3 +136,29 @@ def test_mutant_is_caught(name, monkeypatch):
         except Exception:  # an assertion or a crash both count as the pin catching the mutant
             failed.append(pin.__name__)
     assert failed, f"mutant {name} passed every pin"
+
+
+def test_worked_example_fixture():
+    """The oracle reproduces a worked example derived by hand from Eq. (1), (3), (6)-(7) and
+    (9)-(12) (tests/golden/worked_example.json, derivations inside)."""
+    import json
+    import os
+    fx = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")))
+    q, w, keys, t = np.array(fx["q"], float), np.array(fx["w"], float), np.array(fx["keys"], float), fx["t"]
+    c = fx["cases"]
+    assert np.array_equal(orc.indexer_scores(q, w, keys), np.array(c["scores"]["expected"], float))
+    for name in ("flat", "flat_tie", "hierarchical"):
+        prm = orc.IndexParams(**c[name]["params"])
+        k_mean = orc.sub_block_mean_keys(keys, prm.sub_block)
+        r = orc.index_row(t, q, w, keys, k_mean, prm)
+        assert r["S"].tolist() == c[name]["S"], name
+        if "runs" in c[name]:
+            assert [list(x) for x in orc.runs_of(r["S"], prm.run_align)] == c[name]["runs"], name
+        if "pages" in c[name]:
+            assert r["pages"].tolist() == c[name]["pages"]
+            assert r["page_ids"].tolist() == c[name]["page_ids"]
+            assert np.array_equal(r["page_score"], np.array(c[name]["page_score"], float))
+    a = c["attention"]
+    o, lse = orc.sparse_attention_row(np.array(a["q"], float), np.array(a["keys"], float), np.array(a["values"], float),
+                                      a["scale"])
+    assert np.allclose(o, np.array(a["o"]), rtol=1e-14, atol=0) and np.allclose(lse, np.array(a["lse"]), rtol=1e-14)
