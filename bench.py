@@ -301,9 +301,10 @@ def main():
     ap.add_argument("--graph", action="store_true", help="decode: replay the step as a captured HIP graph")
     ap.add_argument("--pooling", default="mean", choices=["mean", "minmax"],
                     help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
-    ap.add_argument("--attn", default="fused", choices=["fused", "split"],
-                    help="sparse attention as one fused pass over S_t (lsa_sparse_attn), or split into the "
-                         "listed part and the contiguous window on two streams, merged by log-sum-exp "
+    ap.add_argument("--attn", default="fused", choices=["fused", "runs", "split"],
+                    help="sparse attention as one fused pass over S_t (lsa_sparse_attn), the same pass "
+                         "reading S_t from its run encoding (lsa_sparse_attn_runs, MLA only), or split into "
+                         "the listed part and the contiguous window on two streams, merged by log-sum-exp "
                          "(lsa_hfa_attn)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -351,6 +352,9 @@ def main():
                run_count=torch.empty((n_q,), dtype=torch.int32, device=dev))
     ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n_q, n)), dtype=torch.uint8, device=dev)
     split_attn = args.attn == "split"
+    runs_attn = args.attn == "runs"
+    if runs_attn and w.attn != "mla":
+        sys.exit("bench.py: --attn runs needs an MLA workload (the run form is an MLA entry point)")
     ws_attn_n = (lsa.hfa_workspace_size(aprm, n_q) if split_attn else lsa.attn_workspace_size(aprm, n_q, w.k_cap, False))
     ws_attn = torch.empty(max(1, ws_attn_n), dtype=torch.uint8, device=dev)
     O = [torch.empty((n_q, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
@@ -375,6 +379,9 @@ def main():
             if split_attn:
                 lsa.hfa_attn(aprm, t["Q"][l], t["KV"][l], out["idx"], out["count"], q_start, w.k_swa, out=O[l],
                              lse=LSE[l], workspace=ws_attn)
+            elif runs_attn:
+                lsa.sparse_attn_runs(aprm, t["Q"][l], t["KV"][l], out["runs"], out["run_count"], out=O[l],
+                                     lse=LSE[l], workspace=ws_attn if ws_attn_n else None)
             else:
                 lsa.sparse_attn(aprm, t["Q"][l], t["KV"][l], t["V"][l], out["idx"], out["count"], out=O[l],
                                 lse=LSE[l], workspace=ws_attn if ws_attn_n else None)
@@ -438,12 +445,13 @@ def main():
                                "k_sparse": w.k_sparse, "k_sink": w.k_sink, "k_swa": w.k_swa,
                                "run_align": w.run_align, "pooling": w.pooling},
                    "attention": {"kind": w.attn, "heads": H, "d_qk": dqk, "d_v": dv,
-                                 "operator": "split (listed part + window, two streams)" if split_attn else "fused"}},
+                                 "operator": ("split (listed part + window, two streams)" if split_attn else
+                                              "fused, list read as runs" if runs_attn else "fused")}},
         "roofline": {"kernel": ("lsa_hfa_attn (two mla_attn_kernel parts + attn_combine_kernel)" if split_attn
                                 else "mla_attn_kernel"),
                      "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS,
-                     "traffic": None if split_attn else measured_traffic(),
+                     "traffic": None if (split_attn or runs_attn) else measured_traffic(),
                      "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_avg},
         "breakdown": {
             "block_cache_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,

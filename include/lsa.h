@@ -213,6 +213,23 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
                            void* out, float* lse, void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Sparse attention, Eq. (3), over the run encoding of the index lists instead of idx/count: row
+ * r attends to the concatenation of runs[r, 0..run_count[r]), run j covering cache rows
+ * [start, start + len) (lsa_index_prefill's runs output). The kernel expands the runs itself while
+ * staging a row's list, so the result equals lsa_sparse_attn over the same list, bit for bit.
+ * MLA latent cache only, contiguous cache only.
+ *   runs       [n_rows, k_cap] lsa_run, 8-byte aligned; run_count [n_rows] int32
+ *   k_cap      row stride of runs and the list capacity: entries past k_cap are not attended;
+ *              negative lengths count as 0; entries outside [0, n_kv_rows) are skipped
+ *   workspace  >= lsa_sparse_attn_workspace_size(p, n_rows, k_cap, 0)
+ * Other arguments as lsa_sparse_attn.
+ */
+lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const void* q,
+                                const void* kv, int64_t n_kv_rows, const lsa_run* runs,
+                                const int32_t* run_count, int32_t k_cap, void* out, float* lse,
+                                void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * Split sparse attention of prefill (Sec. 4.1.1, the hybrid operator): the same result as
  * lsa_sparse_attn over S_t, computed as two partial attentions merged by online-softmax
  * (log-sum-exp) rescaling: the listed part of S_t without its sliding window (sink and sparse

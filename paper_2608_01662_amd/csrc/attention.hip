@@ -81,6 +81,45 @@ __device__ __forceinline__ int mla_swz(int o, int j) { return (j & 6) | (o & 1);
 constexpr int kMlaHalf = 18 * 1024;  // the second 16 tokens of a tile start 18 blocks later
 constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
 
+// Run form of an index list: runs [start, start + len) of cache rows, in list order. Thread t of
+// the 512 takes the contiguous block of runs [t U, t U + U), U = ceil(n_runs / 512).
+struct RunBlock {
+  const int32_t* base;  // this row's runs (int32 pairs)
+  int b, e;             // this thread's runs
+};
+__device__ __forceinline__ RunBlock run_block(const AttnGeom& a, int64_t row) {
+  int nr = a.run_count[row];
+  nr = nr < 0 ? 0 : (nr > a.k_cap ? a.k_cap : nr);
+  const int u = (nr + 511) / 512;
+  const int b = (int)threadIdx.x * u;
+  return RunBlock{a.runs + row * a.k_cap * 2, b < nr ? b : nr, b + u < nr ? b + u : nr};
+}
+__device__ __forceinline__ int run_len(const int32_t* r) {
+  const int l = r[1];
+  return l < 0 ? 0 : (l > (1 << 24) ? (1 << 24) : l);  // a length is at most the list capacity anyway
+}
+// Exclusive prefix over the 512 threads of v (list entries before this thread's runs) and the total.
+__device__ __forceinline__ int64_t block_prefix512(int64_t v, int64_t* wtot, int64_t& total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int64_t inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
+  }
+  if (lane == 63) wtot[wv] = inc;
+  __syncthreads();
+  int64_t base = 0;
+  total = 0;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    base += x < wv ? wtot[x] : 0;
+    total += wtot[x];
+  }
+  __syncthreads();
+  return base + inc - v;
+}
+
 template <bool SPLIT, int NBUF>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void mla_attn_kernel(AttnGeom a) {
@@ -94,8 +133,19 @@ void mla_attn_kernel(AttnGeom a) {
   const bool loader = wv < kMlaLoaders;
   const int64_t row = xcd_band(blockIdx.x, a.n_rows);
   const int split = SPLIT ? (a.part >= 0 ? a.part : (int)blockIdx.y) : 0;
-  int cnt = a.count[row];
-  cnt = cnt < 0 ? 0 : (cnt > a.k_cap ? a.k_cap : cnt);
+  __shared__ int64_t rtot[8];
+  int cnt;
+  if (a.runs) {  // the list length is the sum of the run lengths (at most k_cap entries are used)
+    const RunBlock rb = run_block(a, row);
+    int64_t mine = 0;
+    for (int r = rb.b; r < rb.e; ++r) mine += run_len(rb.base + 2 * r);
+    int64_t total;
+    (void)block_prefix512(mine, rtot, total);
+    cnt = (int)(total > a.k_cap ? a.k_cap : total);
+  } else {
+    cnt = a.count[row];
+    cnt = cnt < 0 ? 0 : (cnt > a.k_cap ? a.k_cap : cnt);
+  }
   int s0 = SPLIT && a.part < 0 ? split * a.split_len : 0;
   int s1 = SPLIT && a.part < 0 ? (cnt < s0 + a.split_len ? cnt : s0 + a.split_len) : cnt;
   int64_t win0 = -1;  // first cache row of the window part (contiguous rows, no list)
@@ -110,7 +160,7 @@ void mla_attn_kernel(AttnGeom a) {
     }
   }
   const int n = s1 > s0 ? s1 - s0 : 0;
-  const int32_t* slots = a.rows + row * a.k_cap + s0;
+  const int32_t* slots = a.rows ? a.rows + row * a.k_cap + s0 : nullptr;  // list form (unused with runs)
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
   uint8_t* xch = lds + NBUF * kMlaTile;
 
@@ -162,7 +212,27 @@ void mla_attn_kernel(AttnGeom a) {
     const int ntiles = (nc + kMlaT - 1) / kMlaT;
     // list entries -> LDS, validated (-1 = skip; the last tile is padded with -1)
     __syncthreads();  // the previous chunk's readers of `ids` are done
-    {
+    if (a.runs) {
+      // list entries [s0 + c0, s0 + c0 + nc) from the runs: each thread writes the entries of its
+      // own runs that fall in this chunk (runs partition the list, so every entry is written once)
+      const RunBlock rb = run_block(a, row);
+      int64_t mine = 0;
+      for (int r = rb.b; r < rb.e; ++r) mine += run_len(rb.base + 2 * r);
+      int64_t total;
+      int64_t off = block_prefix512(mine, rtot, total);
+      const int64_t lo = (int64_t)s0 + c0, hi = lo + nc;
+      for (int r = rb.b; r < rb.e && off < hi; ++r) {
+        const int64_t start = rb.base[2 * r];
+        const int64_t len = run_len(rb.base + 2 * r);
+        const int64_t p0 = off > lo ? off : lo, p1 = off + len < hi ? off + len : hi;
+        for (int64_t pp = p0; pp < p1; ++pp) {
+          const int64_t v = start + (pp - off);
+          ids[pp - lo] = (v >= 0 && v < a.n_kv_rows) ? (int)v : -1;
+        }
+        off += len;
+      }
+      for (int i = nc + (int)threadIdx.x; i < ntiles * kMlaT; i += 512) ids[i] = -1;  // pad the last tile
+    } else {
       constexpr int U = kMlaIdCap / 512;
       int v[U];
 #pragma unroll

@@ -66,6 +66,10 @@ struct AttnGeom {
   int part;
   int k_swa;
   int64_t q_pos0;          // position t of row 0
+  // Run form of the lists (MLA only; nullptr = use rows/count): row r's list is the concatenation
+  // of the runs (start, length) runs[r, 0..run_count[r]), int32 pairs with row stride k_cap.
+  const int32_t* runs;
+  const int32_t* run_count;
 };
 
 hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st);

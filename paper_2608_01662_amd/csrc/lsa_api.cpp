@@ -466,6 +466,52 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
   return LSA_OK;
 }
 
+lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv,
+                                int64_t n_kv_rows, const lsa_run* runs, const int32_t* run_count, int32_t k_cap,
+                                void* out, float* lse, void* workspace, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  lsa_status s = check_attn_params(p);
+  if (s != LSA_OK) return s;
+  LSA_REQUIRE(p->latent != 0, LSA_ERR_UNSUPPORTED, "the run form is implemented for the MLA latent cache");
+  LSA_REQUIRE(n_rows >= 0 && k_cap >= 1, LSA_ERR_INVALID_ARG, "n_rows < 0 or k_cap < 1");
+  LSA_REQUIRE(n_rows < (1LL << 31) && k_cap < (1 << 30), LSA_ERR_UNSUPPORTED, "n_rows must be < 2^31, k_cap < 2^30");
+  if (n_rows == 0) return LSA_OK;  // nothing to read or write
+  LSA_REQUIRE(n_kv_rows >= 1 && n_kv_rows < (1LL << 31), LSA_ERR_INVALID_ARG, "n_kv_rows=%lld not in [1, 2^31)",
+              (long long)n_kv_rows);
+  LSA_REQUIRE(q && kv && runs && run_count && out, LSA_ERR_INVALID_ARG,
+              "q, kv, runs, run_count and out must be non-NULL");
+  LSA_REQUIRE(aligned(q, 16) && aligned(kv, 16) && aligned(out, 16), LSA_ERR_INVALID_ARG,
+              "q, kv and out must be 16-byte aligned");
+  LSA_REQUIRE(aligned(runs, 8) && aligned(run_count, 4) && aligned(lse, 4), LSA_ERR_INVALID_ARG,
+              "runs must be 8-byte aligned, run_count and lse 4-byte aligned");
+  const AttnPlan pl = plan_attn(p, n_rows, k_cap, 0);
+  LSA_REQUIRE(pl.total == 0 || (workspace != nullptr && aligned(workspace, 256)), LSA_ERR_WORKSPACE,
+              "workspace must be non-NULL and 256-byte aligned");
+  LSA_REQUIRE(ws_bytes >= pl.total, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, pl.total);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  lsa::AttnGeom a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.kv = static_cast<const uint16_t*>(kv);
+  a.n_kv_rows = n_kv_rows;
+  a.runs = reinterpret_cast<const int32_t*>(runs);
+  a.run_count = run_count;
+  a.k_cap = k_cap;
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.n_rows = n_rows;
+  a.n_split = pl.n_split;
+  a.split_len = pl.split_len;
+  a.scale_log2 = p->sm_scale * 1.4426950408889634f;
+  a.part = -1;
+  if (pl.n_split > 1) {
+    a.part_o = reinterpret_cast<float*>(ws + pl.off_po);
+    a.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
+  }
+  const hipError_t e = lsa::launch_mla_attn(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sparse attention (run form)");
+  return LSA_OK;
+}
+
 // ---------------------------------------------------------------- split attention (HFA)
 // Rows per pass of lsa_hfa_attn: the two fp32 partials of a row take 2 * 64 * (512 + 2) * 4 bytes.
 constexpr int64_t kHfaRowsPerPass = 16384;

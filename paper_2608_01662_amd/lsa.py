@@ -117,6 +117,8 @@ def lib() -> ctypes.CDLL:
         L.lsa_sparse_attn.argtypes = [A, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _i32, _i32, _i32, _vp,
                                       _vp, _vp, _sz, _vp]
         L.lsa_sparse_attn.restype = _i32
+        L.lsa_sparse_attn_runs.argtypes = [A, _i64, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _vp, _vp, _sz, _vp]
+        L.lsa_sparse_attn_runs.restype = _i32
         L.lsa_hfa_attn_workspace_size.argtypes = [A, _i64]
         L.lsa_hfa_attn_workspace_size.restype = _sz
         L.lsa_hfa_attn.argtypes = [A, _i64, _vp, _vp, _i64, _vp, _vp, _i32, _i64, _i32, _vp, _vp, _vp, _sz, _vp]
@@ -277,6 +279,26 @@ def sparse_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, v: torch.Ten
                                  _p(count), k_cap, _p(page_table), max_pages, kv_page_size, rows_per_seq,
                                  _p(out), _p(lse), _p(ws), wsb, _stream(q.device)),
            "lsa_sparse_attn")
+    return out, lse
+
+
+def sparse_attn_runs(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, runs: torch.Tensor, run_count: torch.Tensor,
+                     out: torch.Tensor | None = None, lse: torch.Tensor | bool | None = True,
+                     workspace: torch.Tensor | None = None):
+    """Sparse attention over the run form of the lists (lsa_sparse_attn_runs): runs [n_rows, k_cap, 2]
+    int32 (start, length) as index_prefill returns them, run_count [n_rows]. Returns (out, lse or None)."""
+    n_rows = q.shape[0]
+    k_cap = runs.shape[1]
+    if out is None:
+        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=q.device)
+    if lse is True:
+        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=q.device)
+    elif lse is False:
+        lse = None
+    ws, wsb = _workspace(attn_workspace_size(prm, n_rows, k_cap, False), q.device, workspace)
+    _check(lib().lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), kv.shape[0], _p(runs),
+                                      _p(run_count), k_cap, _p(out), _p(lse), _p(ws), wsb, _stream(q.device)),
+           "lsa_sparse_attn_runs")
     return out, lse
 
 

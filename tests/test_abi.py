@@ -166,6 +166,26 @@ def test_bad_attention_arguments():
     assert attn(n_rows=8, table=FAKE, max_pages=4, kv_page=64, ws=None) == WORKSPACE
 
 
+def test_bad_run_form_attention_arguments():
+    """lsa_sparse_attn_runs validates on the host before any launch."""
+    L = lsa.lib()
+    mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+
+    def att(prm=mla, n_rows=8, q=FAKE, kv=FAKE, n_kv=4096, runs=FAKE, rc=FAKE, k_cap=64, out=FAKE, lse=None,
+            ws=FAKE, wsb=1 << 40):
+        return L.lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, q, kv, n_kv, runs, rc, k_cap, out, lse, ws, wsb,
+                                      None)
+    assert att(prm=lsa.AttnParams(sm_scale=0.1, **lsa.MQA)) == UNSUPPORTED     # MLA latent cache only
+    assert att(runs=None) == INVALID
+    assert att(rc=None) == INVALID
+    assert att(runs=ctypes.c_void_p(0x100004)) == INVALID                      # 8-byte (start, len) pairs
+    assert att(k_cap=0) == INVALID
+    assert att(n_kv=0) == INVALID
+    assert att(q=MISALIGNED) == INVALID
+    assert att(ws=None) == WORKSPACE                                           # 8 rows: split partials
+    assert att(n_rows=0, q=None, runs=None, rc=None, out=None, ws=None, wsb=0) == OK
+
+
 def test_bad_split_attention_arguments():
     """lsa_hfa_attn validates on the host before touching streams or events."""
     L = lsa.lib()

@@ -147,6 +147,61 @@ def test_long_lists_beyond_one_staging_pass():
         P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({cnt[i]} entries)")
 
 
+@pytest.mark.parametrize("n_rows", [None, 8], ids=["all_rows", "split_8_rows"])
+def test_run_form_equals_list_form(n_rows):
+    """Attention over the indexer's run encoding equals attention over its index lists, bit for bit
+    (the kernel expands the runs while staging a row's list); with 8 rows the call takes the split
+    path (partials merged by log-sum-exp)."""
+    w = W.SMALL_CLI
+    inp = synth.indexer_inputs(w.seed, w.seq_len, w.seq_len, w.n_heads, w.head_dim, w.fp8)
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_keys(prm, k, ks)
+    out = lsa.index_prefill(prm, q, wt, k, ks, bk, 0, n_kv=w.seq_len, runs=True)
+    rows = slice(None) if n_rows is None else slice(w.seq_len - n_rows, w.seq_len)
+    a = _attn_inputs(w, 0, w.seq_len, w.seq_len)
+    qa, kv = P.bf16_dev(a["q"][rows]), P.bf16_dev(a["kv"])
+    o1, l1 = lsa.sparse_attn(w.attn_params(), qa, kv, None, out["idx"][rows].contiguous(), out["count"][rows].contiguous())
+    o2, l2 = lsa.sparse_attn_runs(w.attn_params(), qa, kv, out["runs"][rows].contiguous(), out["run_count"][rows].contiguous())
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_run_form_edge_runs():
+    """Hand-made runs: out-of-range starts and runs crossing the cache end (those entries are
+    skipped), a negative length (counts as 0), an empty row, and lists longer than the capacity
+    (cut at k_cap); each row equals the list form over the same expanded list."""
+    from dataclasses import replace
+    w = replace(W.SMALL_MLA, seq_len=600)
+    n_kv, k_cap, B = w.seq_len, 96, 6
+    a = _attn_inputs(w, 0, B, n_kv)
+    runs = np.zeros((B, k_cap, 2), np.int32)
+    rc = np.zeros(B, np.int32)
+    spec = [[(0, 4), (100, 30), (590, 20)],             # the last run crosses the cache end
+            [(-5, 10), (40, 1), (41, 7)],                # starts below 0
+            [(10, 3), (20, -4), (30, 5)],                # a negative length
+            [],                                          # empty row
+            [(0, 50), (200, 50), (400, 50)],             # 150 entries: cut at k_cap = 96
+            [(i * 7, 1) for i in range(90)]]             # many single-entry runs
+    idx = np.full((B, k_cap), -1, np.int32)
+    cnt = np.zeros(B, np.int32)
+    for b, rs in enumerate(spec):
+        rc[b] = len(rs)
+        lst = []
+        for j, (st, ln) in enumerate(rs):
+            runs[b, j] = (st, ln)
+            lst += list(range(st, st + max(ln, 0)))
+        lst = lst[:k_cap]
+        cnt[b] = len(lst)
+        idx[b, :len(lst)] = lst
+    qa, kv = P.bf16_dev(a["q"][:B]), P.bf16_dev(a["kv"])
+    o1, l1 = lsa.sparse_attn(w.attn_params(), qa, kv, None, P.to_dev(idx), P.to_dev(cnt))
+    o2, l2 = lsa.sparse_attn_runs(w.attn_params(), qa, kv, P.to_dev(runs), P.to_dev(rc))
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert torch.all(o2[3] == 0) and torch.all(torch.isneginf(l2[3]))
+
+
 def test_cross_layer_reuse():
     """One index list feeds several layers (Sec. 3.2): each layer's output matches the oracle on
     its own Q and KV, and the shared list is left byte-identical."""
