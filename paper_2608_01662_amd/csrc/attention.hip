@@ -94,10 +94,17 @@ __device__ __forceinline__ RunBlock run_block(const AttnGeom& a, int64_t row) {
   const int b = (int)threadIdx.x * u;
   return RunBlock{a.runs + row * a.k_cap * 2, b < nr ? b : nr, b + u < nr ? b + u : nr};
 }
-__device__ __forceinline__ int run_len(const int32_t* r) {
-  const int l = r[1];
+__device__ __forceinline__ int run_len(int l) {
   return l < 0 ? 0 : (l > (1 << 24) ? (1 << 24) : l);  // a length is at most the list capacity anyway
 }
+// Runs [r0, r0 + 4) of this thread's block, loaded together (zero-length past the block's end).
+__device__ __forceinline__ void load_runs4(const RunBlock& rb, int r0, int2 (&x)[4]) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    x[k] = r0 + k < rb.e ? *reinterpret_cast<const int2*>(rb.base + 2 * (r0 + k)) : int2{0, 0};
+}
+constexpr int kRunShort = 4;   // runs longer than this are expanded by the whole block
+constexpr int kRunQueue = 128; // long runs queued per staging pass (more are expanded by their owner)
 // Exclusive prefix over the 512 threads of v (list entries before this thread's runs) and the total.
 __device__ __forceinline__ int64_t block_prefix512(int64_t v, int64_t* wtot, int64_t& total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -134,13 +141,22 @@ void mla_attn_kernel(AttnGeom a) {
   const int64_t row = xcd_band(blockIdx.x, a.n_rows);
   const int split = SPLIT ? (a.part >= 0 ? a.part : (int)blockIdx.y) : 0;
   __shared__ int64_t rtot[8];
+  __shared__ int32_t roff[512];   // run form: list position of each thread's first run (clamped)
+  __shared__ int4 rq[kRunQueue];  // run form: (start, offset into the run, ids slot, entries)
+  __shared__ int rq_n;
   int cnt;
   if (a.runs) {  // the list length is the sum of the run lengths (at most k_cap entries are used)
     const RunBlock rb = run_block(a, row);
     int64_t mine = 0;
-    for (int r = rb.b; r < rb.e; ++r) mine += run_len(rb.base + 2 * r);
+    for (int r0 = rb.b; r0 < rb.e; r0 += 4) {
+      int2 x[4];
+      load_runs4(rb, r0, x);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) mine += run_len(x[k].y);
+    }
     int64_t total;
-    (void)block_prefix512(mine, rtot, total);
+    const int64_t off = block_prefix512(mine, rtot, total);
+    roff[threadIdx.x] = (int)(off < 0x7fffffff ? off : 0x7fffffff);  // read back by this thread only
     cnt = (int)(total > a.k_cap ? a.k_cap : total);
   } else {
     cnt = a.count[row];
@@ -211,27 +227,47 @@ void mla_attn_kernel(AttnGeom a) {
     const int nc = n - c0 < kMlaIdCap ? n - c0 : kMlaIdCap;
     const int ntiles = (nc + kMlaT - 1) / kMlaT;
     // list entries -> LDS, validated (-1 = skip; the last tile is padded with -1)
+    if (a.runs && threadIdx.x == 0) rq_n = 0;  // the previous pass's readers passed a barrier since
     __syncthreads();  // the previous chunk's readers of `ids` are done
     if (a.runs) {
-      // list entries [s0 + c0, s0 + c0 + nc) from the runs: each thread writes the entries of its
-      // own runs that fall in this chunk (runs partition the list, so every entry is written once)
+      // list entries [s0 + c0, s0 + c0 + nc) from the runs (runs partition the list, so every entry
+      // is written once): each thread writes the entries of its own short runs that fall in this
+      // chunk and queues the longer ones, which the whole block then writes, 512 entries at a time
       const RunBlock rb = run_block(a, row);
-      int64_t mine = 0;
-      for (int r = rb.b; r < rb.e; ++r) mine += run_len(rb.base + 2 * r);
-      int64_t total;
-      int64_t off = block_prefix512(mine, rtot, total);
       const int64_t lo = (int64_t)s0 + c0, hi = lo + nc;
-      for (int r = rb.b; r < rb.e && off < hi; ++r) {
-        const int64_t start = rb.base[2 * r];
-        const int64_t len = run_len(rb.base + 2 * r);
-        const int64_t p0 = off > lo ? off : lo, p1 = off + len < hi ? off + len : hi;
-        for (int64_t pp = p0; pp < p1; ++pp) {
-          const int64_t v = start + (pp - off);
-          ids[pp - lo] = (v >= 0 && v < a.n_kv_rows) ? (int)v : -1;
+      int64_t off = roff[threadIdx.x];
+      for (int r0 = rb.b; r0 < rb.e && off < hi; r0 += 4) {
+        int2 x[4];
+        load_runs4(rb, r0, x);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int64_t len = run_len(x[k].y);
+          const int64_t p0 = off > lo ? off : lo, p1 = off + len < hi ? off + len : hi;
+          if (p1 > p0) {
+            int q = kRunQueue;
+            if (p1 - p0 > kRunShort) q = atomicAdd(&rq_n, 1);
+            if (q < kRunQueue) {
+              rq[q] = int4{x[k].x, (int)(p0 - off), (int)(p0 - lo), (int)(p1 - p0)};
+            } else {
+              for (int64_t pp = p0; pp < p1; ++pp) {
+                const int64_t v = (int64_t)x[k].x + (pp - off);
+                ids[pp - lo] = (v >= 0 && v < a.n_kv_rows) ? (int)v : -1;
+              }
+            }
+          }
+          off += len;
         }
-        off += len;
       }
       for (int i = nc + (int)threadIdx.x; i < ntiles * kMlaT; i += 512) ids[i] = -1;  // pad the last tile
+      __syncthreads();
+      const int nq = rq_n < kRunQueue ? rq_n : kRunQueue;
+      for (int qi = 0; qi < nq; ++qi) {
+        const int4 e = rq[qi];
+        for (int i = (int)threadIdx.x; i < e.w; i += 512) {
+          const int64_t v = (int64_t)e.x + e.y + i;
+          ids[e.z + i] = (v >= 0 && v < a.n_kv_rows) ? (int)v : -1;
+        }
+      }
     } else {
       constexpr int U = kMlaIdCap / 512;
       int v[U];

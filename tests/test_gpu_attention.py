@@ -202,6 +202,45 @@ def test_run_form_edge_runs():
     assert torch.all(o2[3] == 0) and torch.all(torch.isneginf(l2[3]))
 
 
+def test_run_form_long_and_many_runs():
+    """Run form over lists of up to 16448 entries (several LDS staging passes, runs straddling a
+    pass boundary), with thousands of runs per row (several batches per thread), more long runs
+    than the block-wide queue holds, run lengths around the short-run cut, and one run cut at
+    k_cap that crosses the cache end; each row equals the list form bit for bit."""
+    from dataclasses import replace
+    w = replace(W.SMALL_MLA, seq_len=20000)
+    n_kv, k_cap = w.seq_len, 16448
+    spec = [[(13 * i, 6) for i in range(1500)],
+            [(2 * i, 1) for i in range(2500)] + [(6000, 9000)],
+            [],
+            [(5000, 20000)],
+            [(6 * i, 5) for i in range(3000)]]
+    st = 0
+    while sum(n for _, n in spec[2]) < 12000:
+        ln = 1 + len(spec[2]) % 9
+        spec[2].append((st, ln))
+        st += ln + 1
+    B = len(spec)
+    a = _attn_inputs(w, 0, B, n_kv)
+    runs = np.zeros((B, k_cap, 2), np.int32)
+    rc = np.zeros(B, np.int32)
+    idx = np.full((B, k_cap), -1, np.int32)
+    cnt = np.zeros(B, np.int32)
+    for b, rs in enumerate(spec):
+        rc[b] = len(rs)
+        runs[b, :len(rs)] = rs
+        lst = np.concatenate([np.arange(s0, s0 + n) for s0, n in rs])[:k_cap]
+        cnt[b] = len(lst)
+        idx[b, :len(lst)] = np.where(lst < n_kv, lst, -1)
+    assert cnt.tolist() == [9000, 11500, 12006, 16448, 15000]
+    qa, kv = P.bf16_dev(a["q"][:B]), P.bf16_dev(a["kv"])
+    o1, l1 = lsa.sparse_attn(w.attn_params(), qa, kv, None, P.to_dev(idx), P.to_dev(cnt))
+    o2, l2 = lsa.sparse_attn_runs(w.attn_params(), qa, kv, P.to_dev(runs), P.to_dev(rc))
+    torch.cuda.synchronize()
+    for b in range(B):
+        assert torch.equal(o1[b], o2[b]) and torch.equal(l1[b], l2[b]), f"row {b} ({cnt[b]} entries, {rc[b]} runs)"
+
+
 def test_cross_layer_reuse():
     """One index list feeds several layers (Sec. 3.2): each layer's output matches the oracle on
     its own Q and KV, and the shared list is left byte-identical."""
