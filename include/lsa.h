@@ -218,7 +218,8 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
  * [start, start + len) (lsa_index_prefill's runs output). The kernel expands the runs itself while
  * staging a row's list, so the result equals lsa_sparse_attn over the same list, bit for bit.
  * MLA latent cache only, contiguous cache only.
- *   runs       [n_rows, k_cap] lsa_run, 8-byte aligned; run_count [n_rows] int32
+ *   runs       [n_rows, k_cap] lsa_run, 8-byte aligned; run_count [n_rows] int32, clamped to
+ *              [0, k_cap]
  *   k_cap      row stride of runs and the list capacity: entries past k_cap are not attended;
  *              negative lengths count as 0; entries outside [0, n_kv_rows) are skipped
  *   workspace  >= lsa_sparse_attn_workspace_size(p, n_rows, k_cap, 0)

@@ -94,9 +94,8 @@ __device__ __forceinline__ RunBlock run_block(const AttnGeom& a, int64_t row) {
   const int b = (int)threadIdx.x * u;
   return RunBlock{a.runs + row * a.k_cap * 2, b < nr ? b : nr, b + u < nr ? b + u : nr};
 }
-__device__ __forceinline__ int run_len(int l) {
-  return l < 0 ? 0 : (l > (1 << 24) ? (1 << 24) : l);  // a length is at most the list capacity anyway
-}
+// Length of a run, clamped to [0, cap]: a run longer than the list capacity ends the list anyway.
+__device__ __forceinline__ int run_len(int l, int cap) { return l < 0 ? 0 : (l > cap ? cap : l); }
 // Runs [r0, r0 + 4) of this thread's block, loaded together (zero-length past the block's end).
 __device__ __forceinline__ void load_runs4(const RunBlock& rb, int r0, int2 (&x)[4]) {
 #pragma unroll
@@ -152,7 +151,7 @@ void mla_attn_kernel(AttnGeom a) {
       int2 x[4];
       load_runs4(rb, r0, x);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) mine += run_len(x[k].y);
+      for (int k = 0; k < 4; ++k) mine += run_len(x[k].y, a.k_cap);
     }
     int64_t total;
     const int64_t off = block_prefix512(mine, rtot, total);
@@ -241,7 +240,7 @@ void mla_attn_kernel(AttnGeom a) {
         load_runs4(rb, r0, x);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const int64_t len = run_len(x[k].y);
+          const int64_t len = run_len(x[k].y, a.k_cap);
           const int64_t p0 = off > lo ? off : lo, p1 = off + len < hi ? off + len : hi;
           if (p1 > p0) {
             int q = kRunQueue;

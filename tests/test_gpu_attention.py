@@ -170,10 +170,11 @@ def test_run_form_equals_list_form(n_rows):
 def test_run_form_edge_runs():
     """Hand-made runs: out-of-range starts and runs crossing the cache end (those entries are
     skipped), a negative length (counts as 0), an empty row, and lists longer than the capacity
-    (cut at k_cap); each row equals the list form over the same expanded list."""
+    (cut at k_cap, also after a run of 2^31 - 1 entries); each row equals the list form over the
+    same expanded list."""
     from dataclasses import replace
     w = replace(W.SMALL_MLA, seq_len=600)
-    n_kv, k_cap, B = w.seq_len, 96, 6
+    n_kv, k_cap, B = w.seq_len, 96, 7
     a = _attn_inputs(w, 0, B, n_kv)
     runs = np.zeros((B, k_cap, 2), np.int32)
     rc = np.zeros(B, np.int32)
@@ -182,7 +183,8 @@ def test_run_form_edge_runs():
             [(10, 3), (20, -4), (30, 5)],                # a negative length
             [],                                          # empty row
             [(0, 50), (200, 50), (400, 50)],             # 150 entries: cut at k_cap = 96
-            [(i * 7, 1) for i in range(90)]]             # many single-entry runs
+            [(i * 7, 1) for i in range(90)],             # many single-entry runs
+            [(3, 2 ** 31 - 1), (10, 5)]]                 # a length beyond any capacity: cut at k_cap
     idx = np.full((B, k_cap), -1, np.int32)
     cnt = np.zeros(B, np.int32)
     for b, rs in enumerate(spec):
@@ -190,7 +192,7 @@ def test_run_form_edge_runs():
         lst = []
         for j, (st, ln) in enumerate(rs):
             runs[b, j] = (st, ln)
-            lst += list(range(st, st + max(ln, 0)))
+            lst += list(range(st, st + min(max(ln, 0), k_cap)))
         lst = lst[:k_cap]
         cnt[b] = len(lst)
         idx[b, :len(lst)] = lst
