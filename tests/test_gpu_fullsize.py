@@ -61,9 +61,11 @@ def _check_attention(w, Q, KV, rows, idx, cnt, o, lse):
     return worst
 
 
-def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed, split_attn=False):
+def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed, split_attn=False, runs_layers=()):
     """Indexer + sparse attention for query rows [q_start, q_start + n_q) of one sequence with
-    n_kv cached tokens, as the library runs them; checks the sampled rows against the oracle."""
+    n_kv cached tokens, as the library runs them; checks the sampled rows against the oracle. For
+    the layers in runs_layers, attention over the run encoding must equal the list form on every
+    row, bit for bit."""
     H, dqk, dv = w.attn_dims
     prm = w.index_params()
     qI = synth.device_normal_bf16((n_q, w.n_heads, w.head_dim), w.seed, synth.T_QI, DEV,
@@ -90,6 +92,11 @@ def _prefill_case(w, q_start, n_q, n_kv, layers, n_random, seed, split_attn=Fals
             o, lse = lsa.hfa_attn(w.attn_params(), Q, KV, out["idx"], out["count"], q_start, w.k_swa)
         else:
             o, lse = lsa.sparse_attn(w.attn_params(), Q, KV, None, out["idx"], out["count"])
+        if layer in runs_layers:
+            o2, lse2 = lsa.sparse_attn_runs(w.attn_params(), Q, KV, out["runs"], out["run_count"])
+            torch.cuda.synchronize()
+            assert torch.equal(o, o2) and torch.equal(lse, lse2), f"{w.name} layer {layer}: run form differs"
+            del o2, lse2
         worst = _check_attention(w, Q, KV, rows, g_idx, g_cnt, o[sel].float().cpu().numpy(),
                                  lse[sel].cpu().numpy())
         print(f"{w.name} layer {layer}: index {stats}, attention worst max|d| {worst[0]:.2e} rel {worst[1]:.2e}")
@@ -104,7 +111,7 @@ def test_fullsize_prefill_L32768():
 
 def test_fullsize_prefill_L131072_cross_layer():
     w = W.L128K_CLI4
-    _prefill_case(w, 0, w.seq_len, w.seq_len, layers=[0, w.layers - 1], n_random=32, seed=102)
+    _prefill_case(w, 0, w.seq_len, w.seq_len, layers=[0, w.layers - 1], n_random=32, seed=102, runs_layers=[0])
 
 
 def test_fullsize_split_attention_L131072():
@@ -118,7 +125,7 @@ def test_fullsize_prefill_L1M_last_chunk():
     """The last 8192-row chunk of the 1M-token prefill, against the whole 1M-token prefix."""
     w = W.L1M_CHUNKED
     q_start = w.seq_len - w.chunk
-    _prefill_case(w, q_start, w.chunk, w.seq_len, layers=[0], n_random=16, seed=103)
+    _prefill_case(w, q_start, w.chunk, w.seq_len, layers=[0], n_random=16, seed=103, runs_layers=[0])
 
 
 def test_fullsize_prefill_L1M_paper_hi_setting():
