@@ -314,11 +314,13 @@ def main():
                     help="only run a plain device copy of BYTES (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build measures the single-GPU hot path "
-              "(multi-GPU sharding is a design note, not implemented); use --gpus 1", file=sys.stderr)
+        print("bench.py measures the hot path on one GPU; running across several GPUs is not "
+              "implemented (how it would shard is a design note); use --gpus 1", file=sys.stderr)
         sys.exit(2)
     if args.steps < 1 or args.warmup < 0:
         sys.exit("--steps must be >= 1 and --warmup >= 0")
+    if args.attn == "runs" and W.BY_NAME[args.workload].attn != "mla":
+        sys.exit("bench.py: --attn runs needs an MLA workload (the run form is an MLA entry point)")
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
@@ -353,8 +355,6 @@ def main():
     ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n_q, n)), dtype=torch.uint8, device=dev)
     split_attn = args.attn == "split"
     runs_attn = args.attn == "runs"
-    if runs_attn and w.attn != "mla":
-        sys.exit("bench.py: --attn runs needs an MLA workload (the run form is an MLA entry point)")
     ws_attn_n = (lsa.hfa_workspace_size(aprm, n_q) if split_attn else lsa.attn_workspace_size(aprm, n_q, w.k_cap, False))
     ws_attn = torch.empty(max(1, ws_attn_n), dtype=torch.uint8, device=dev)
     O = [torch.empty((n_q, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
