@@ -154,6 +154,28 @@ def test_flat_short_window_partial_page(base):
     print(w.name, stats)
 
 
+@pytest.mark.parametrize("keep_pages,k_sink,k_swa,k_sparse", [
+    (0, 0, 0, 1),       # flat, no sink, no window (E_t = [0, t]), one sparse token
+    (0, 0, 0, 300),     # flat, a budget above the early rows' candidate count
+    (1, 0, 64, 1),      # hierarchical with one recalled page, the shortest window (K_swa = P)
+    (1, 0, 64, 64),     # the whole recalled page selected
+    (2, 1, 64, 100),    # one sink token, two pages, a budget above one page
+], ids=["flat_1", "flat_300", "hi_m1_k1", "hi_m1_kP", "hi_m2_sink1"])
+def test_degenerate_budgets(keep_pages, k_sink, k_swa, k_sparse):
+    """Smallest legal budgets and windows: no sink, no window (flat mode), one recalled page,
+    one sparse token, and budgets at or above the candidate count; every row against the oracle."""
+    from dataclasses import replace
+    w = replace(W.L2K_MQA, name=f"degenerate_{keep_pages}_{k_sink}_{k_swa}_{k_sparse}", seq_len=700,
+                keep_pages=keep_pages, k_sink=k_sink, k_swa=k_swa, k_sparse=k_sparse)
+    inp = P.prefill_inputs(w)
+    out, _ = _run_prefill(w, inp, pages=keep_pages > 0)
+    rows = list(range(w.seq_len))
+    res = _oracle_rows(w, inp, rows)
+    stats = P.check_index_rows(w, rows, out["idx"], out["count"], out["pages"] if keep_pages > 0 else None, res)
+    P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
+    print(w.name, stats)
+
+
 @pytest.mark.parametrize("keep_pages", [0, 600])
 def test_select_from_global_keys(keep_pages):
     """Rows with more candidates than the LDS holds (here 45056 in flat mode, 38400 with M = 600
