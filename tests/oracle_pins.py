@@ -432,6 +432,23 @@ def pin_attention_scale_and_log(orc):
     assert np.allclose(o, [[7.0]], rtol=1e-14) and np.allclose(lse, [np.log(4.0)], rtol=1e-14)
 
 
+def pin_attention_for_set_value_columns(orc):
+    """One selected row has softmax weight 1, so the output is that row's value vector: with a
+    latent cache V is its first d_v columns (MLA absorbed mode), otherwise the separate V row.
+    Every other row and column holds distinct values, so a wrong row or column shows."""
+    n, d_qk, d_v = 6, 8, 4
+    vals = np.arange(n * d_qk, dtype=np.float64).reshape(n, d_qk) / 8.0 - 2.0   # exact in bf16
+    kv_bits = orc.f64_to_bf16_bits(vals)
+    q_bits = orc.f64_to_bf16_bits(np.full((2, d_qk), 0.25))
+    o, lse = orc.attention_for_set(q_bits, kv_bits, None, [3], d_v, 0.5)
+    assert np.array_equal(o, np.tile(vals[3, :d_v], (2, 1))), "latent V is not the first d_v columns"
+    v_sep = np.arange(n * d_v, dtype=np.float64).reshape(n, d_v) + 100.0
+    o2, _ = orc.attention_for_set(q_bits, kv_bits, orc.f64_to_bf16_bits(v_sep), [4], d_v, 0.5)
+    assert np.array_equal(o2, np.tile(v_sep[4], (2, 1))), "separate V row not used"
+    z = 0.5 * 0.25 * vals[3].sum()
+    assert np.allclose(lse, [z, z], rtol=1e-14)
+
+
 def pin_logical_rows(orc):
     page = 4
     paged = np.arange(6 * page * 2).reshape(6, page, 2)

@@ -103,6 +103,28 @@ def _pages_shifted(lo, hi, prm):
     return np.arange(lo // prm.page, hi // prm.page)
 
 
+def _latent_v_last_columns(q_t_bits, kv_bits, v_bits, S, d_v, scale):
+    S = np.asarray(S, np.int64)
+    k = orc.bf16_bits_to_f64(kv_bits[S])
+    v = k[:, -d_v:] if v_bits is None else orc.bf16_bits_to_f64(v_bits[S])
+    return orc.sparse_attention_row(orc.bf16_bits_to_f64(q_t_bits), k, v, scale)
+
+
+def _runs_without_align_cut(S, align):
+    runs = []
+    for s in np.asarray(S, np.int64).tolist():
+        if runs and s == runs[-1][0] + runs[-1][1]:
+            runs[-1][1] += 1
+        else:
+            runs.append([s, 1])
+    return [(a, n) for a, n in runs]
+
+
+def _key_scale_ignored(k, k_scale=None):
+    k = np.asarray(k)
+    return orc.e4m3fn_to_f64(k) if k.dtype == np.uint8 else orc.bf16_bits_to_f64(k)
+
+
 MUTANTS = {
     "no_relu": ("indexer_scores", _no_relu),
     "relu_after_head_sum": ("indexer_scores", _relu_after_sum),
@@ -119,6 +141,9 @@ MUTANTS = {
     "last_eligible_page_dropped": ("eligible_pages", _pages_shifted),
     "minmax_min_of_products": ("page_scores_minmax", _minmax_min_of_products),
     "minmax_extrema_swapped": ("sub_block_minmax_keys", _minmax_keys_swapped),
+    "latent_v_from_last_columns": ("attention_for_set", _latent_v_last_columns),
+    "runs_not_cut_at_multiples_of_c": ("runs_of", _runs_without_align_cut),
+    "key_scale_ignored": ("dequantized_keys", _key_scale_ignored),
 }
 
 
