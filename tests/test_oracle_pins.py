@@ -103,6 +103,24 @@ def _pages_shifted(lo, hi, prm):
     return np.arange(lo // prm.page, hi // prm.page)
 
 
+def _candidates_ignore_pages(pages, lo, hi, prm):
+    return np.arange(lo, hi + 1, dtype=np.int64)
+
+
+def _mean_keys_not_rounded(k_hat, sub_block):
+    k_hat = np.asarray(k_hat, np.float64)
+    n = k_hat.shape[0] // sub_block
+    return k_hat[: n * sub_block].reshape(n, sub_block, -1).mean(axis=1)
+
+
+def _scores_on_value_columns(q_t_bits, kv_bits, v_bits, S, d_v, scale):
+    S = np.asarray(S, np.int64)
+    k = orc.bf16_bits_to_f64(kv_bits[S])
+    v = k[:, :d_v] if v_bits is None else orc.bf16_bits_to_f64(v_bits[S])
+    q = orc.bf16_bits_to_f64(q_t_bits)
+    return orc.sparse_attention_row(q[:, :d_v], k[:, :d_v], v, scale)
+
+
 def _latent_v_last_columns(q_t_bits, kv_bits, v_bits, S, d_v, scale):
     S = np.asarray(S, np.int64)
     k = orc.bf16_bits_to_f64(kv_bits[S])
@@ -144,6 +162,9 @@ MUTANTS = {
     "latent_v_from_last_columns": ("attention_for_set", _latent_v_last_columns),
     "runs_not_cut_at_multiples_of_c": ("runs_of", _runs_without_align_cut),
     "key_scale_ignored": ("dequantized_keys", _key_scale_ignored),
+    "candidates_ignore_recalled_pages": ("candidates_of_pages", _candidates_ignore_pages),
+    "mean_keys_not_rounded_to_bf16": ("sub_block_mean_keys", _mean_keys_not_rounded),
+    "attention_scores_on_value_columns_only": ("attention_for_set", _scores_on_value_columns),
 }
 
 
