@@ -144,6 +144,37 @@ def _p(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+_BF16, _F32, _I32, _I64, _U8 = (torch.bfloat16,), (torch.float32,), (torch.int32,), (torch.int64,), (torch.uint8,)
+
+
+def _need(name: str, t, dtypes, shape=None, device=None, min_rows: int | None = None):
+    """The C ABI receives bare pointers, so the sizes it is told must match the tensors behind
+    them: `t` must be a contiguous CUDA tensor of one of `dtypes` on `device`, of exactly `shape`
+    (None entries match any size), with at least `min_rows` rows. Raises ValueError otherwise."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if not t.is_cuda or (device is not None and t.device != torch.device(device)):
+        raise ValueError(f"{name} must be a CUDA tensor on {device or 'a GPU'} (got {t.device})")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {' or '.join(str(d) for d in dtypes)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and (t.dim() != len(shape) or any(s is not None and d != s for d, s in zip(t.shape, shape))):
+        want = tuple("*" if s is None else s for s in shape)
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {want}")
+    if min_rows is not None and t.shape[0] < min_rows:
+        raise ValueError(f"{name} has {t.shape[0]} rows, at least {min_rows} needed")
+    return t
+
+
+def _need_opt(name: str, t, *args, **kw):
+    return None if t is None else _need(name, t, *args, **kw)
+
+
+def _key_dtypes(prm: "IndexParams"):
+    return _U8 if prm.fp8 else _BF16
+
+
 def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
@@ -158,6 +189,7 @@ def _workspace(nbytes: int, device, ws):
     if nbytes == 0:
         return None, 0
     if ws is not None:
+        _need("workspace", ws, tuple({ws.dtype}), device=device)
         return ws, ws.numel() * ws.element_size()
     return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
 
@@ -173,10 +205,12 @@ def attn_workspace_size(prm: AttnParams, n_rows: int, k_cap: int, paged: bool) -
 def block_means(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None = None,
                 out: torch.Tensor | None = None) -> torch.Tensor:
     """Mean-key cache of the coarse stage: [n_tok // sub_block, head_dim] bf16."""
-    k = _keys_u8_or_bf16(k)
+    k = _need("k", _keys_u8_or_bf16(k), _key_dtypes(prm), (None, prm.head_dim))
     n_tok = k.shape[0]
+    _need_opt("k_scale", k_scale, _F32, (n_tok,), k.device)
     if out is None:
         out = torch.empty((n_tok // prm.sub_block, prm.head_dim), dtype=torch.bfloat16, device=k.device)
+    _need("out", out, _BF16, (n_tok // prm.sub_block, prm.head_dim), k.device)
     _check(lib().lsa_block_means(ctypes.byref(prm.c()), n_tok, _p(k), _p(k_scale), _p(out), _stream(k.device)),
            "lsa_block_means")
     return out
@@ -185,10 +219,12 @@ def block_means(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None 
 def block_minmax(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None = None,
                  out: torch.Tensor | None = None) -> torch.Tensor:
     """Min-max block cache (Eq. 13): [n_tok // sub_block, 2 * head_dim] bf16 rows [k_max | k_min]."""
-    k = _keys_u8_or_bf16(k)
+    k = _need("k", _keys_u8_or_bf16(k), _key_dtypes(prm), (None, prm.head_dim))
     n_tok = k.shape[0]
+    _need_opt("k_scale", k_scale, _F32, (n_tok,), k.device)
     if out is None:
         out = torch.empty((n_tok // prm.sub_block, 2 * prm.head_dim), dtype=torch.bfloat16, device=k.device)
+    _need("out", out, _BF16, (n_tok // prm.sub_block, 2 * prm.head_dim), k.device)
     _check(lib().lsa_block_minmax(ctypes.byref(prm.c()), n_tok, _p(k), _p(k_scale), _p(out), _stream(k.device)),
            "lsa_block_minmax")
     return out
@@ -203,8 +239,10 @@ def block_keys(prm: IndexParams, k: torch.Tensor, k_scale: torch.Tensor | None =
 def block_keys_update(prm: IndexParams, rows: torch.Tensor, k: torch.Tensor, k_scale: torch.Tensor | None,
                       block: torch.Tensor) -> torch.Tensor:
     """Recompute, in place, the block-cache rows of the sub-blocks holding token rows `rows` (int64)."""
-    k = _keys_u8_or_bf16(k)
-    assert rows.dtype == torch.int64
+    k = _need("k", _keys_u8_or_bf16(k), _key_dtypes(prm), (None, prm.head_dim))
+    _need("rows", rows, _I64, (None,), k.device)
+    _need_opt("k_scale", k_scale, _F32, (k.shape[0],), k.device)
+    _need("block", block, _BF16, (k.shape[0] // prm.sub_block, prm.block_width), k.device)
     _check(lib().lsa_block_keys_update(ctypes.byref(prm.c()), rows.numel(), _p(rows), k.shape[0], _p(k),
                                        _p(k_scale), _p(block), _stream(k.device)), "lsa_block_keys_update")
     return block
@@ -220,6 +258,10 @@ def _index_outputs(prm: IndexParams, n_rows: int, device, runs: bool, pages: boo
         out.setdefault("run_count", torch.empty((n_rows,), dtype=torch.int32, device=device))
     if pages and prm.keep_pages > 0:
         out.setdefault("pages", torch.empty((n_rows, prm.keep_pages), dtype=torch.int32, device=device))
+    shapes = {"idx": (n_rows, kc), "count": (n_rows,), "runs": (n_rows, kc, 2), "run_count": (n_rows,),
+              "pages": (n_rows, prm.keep_pages)}
+    for key, t in out.items():
+        _need(f"out[{key!r}]", t, _I32, shapes[key], device)
     return out
 
 
@@ -229,8 +271,14 @@ def index_prefill(prm: IndexParams, q: torch.Tensor, w: torch.Tensor, k: torch.T
                   workspace: torch.Tensor | None = None, out: dict | None = None) -> dict:
     """LSA indexer for query rows at positions q_start .. q_start + n_q - 1 (lsa_index_prefill)."""
     k = _keys_u8_or_bf16(k)
-    n_q = q.shape[0]
+    _need("q", q, _BF16, (None, prm.n_heads, prm.head_dim))
+    n_q, dev = q.shape[0], q.device
     n_kv = k.shape[0] if n_kv is None else n_kv
+    _need("w", w, _F32, (n_q, prm.n_heads), dev)
+    _need("k", k, _key_dtypes(prm), (None, prm.head_dim), dev, min_rows=n_kv)
+    if prm.fp8:
+        _need("k_scale", k_scale, _F32, (None,), dev, min_rows=n_kv)
+    _need_opt("block_keys", block_keys, _BF16, (None, prm.block_width), dev, min_rows=n_kv // prm.sub_block)
     o = _index_outputs(prm, n_q, q.device, runs, pages, out)
     ws, wsb = _workspace(index_workspace_size(prm, n_q, n_kv), q.device, workspace)
     _check(lib().lsa_index_prefill(ctypes.byref(prm.c()), q_start, n_q, n_kv, _p(q), _p(w), _p(k), _p(k_scale),
@@ -246,7 +294,21 @@ def index_decode(prm: IndexParams, ctx_len: torch.Tensor, page_table: torch.Tens
                  workspace: torch.Tensor | None = None, out: dict | None = None) -> dict:
     """LSA indexer for one new token per sequence over a paged key cache (lsa_index_decode)."""
     k = _keys_u8_or_bf16(k)
+    _need("page_table", page_table, _I32, (None, None))
     batch, max_pages = page_table.shape
+    dev = page_table.device
+    _need("ctx_len", ctx_len, _I32, (batch,), dev)
+    _need("q", q, _BF16, (batch, prm.n_heads, prm.head_dim), dev)
+    _need("w", w, _F32, (batch, prm.n_heads), dev)
+    n_cached = n_phys * kv_page_size
+    _need("k", k, _key_dtypes(prm), None, dev)
+    if k.shape[-1] != prm.head_dim or k.numel() < n_cached * prm.head_dim:
+        raise ValueError(f"k must hold n_phys * kv_page_size = {n_cached} key rows of {prm.head_dim}")
+    if prm.fp8:
+        _need("k_scale", k_scale, _F32, None, dev)
+        if k_scale.numel() < n_cached:
+            raise ValueError(f"k_scale must hold {n_cached} scales")
+    _need_opt("block_keys", block_keys, _BF16, (None, prm.block_width), dev, min_rows=n_cached // prm.sub_block)
     o = _index_outputs(prm, batch, q.device, runs, pages, out)
     ws, wsb = _workspace(index_workspace_size(prm, batch, max_pages * kv_page_size), q.device, workspace)
     _check(lib().lsa_index_decode(ctypes.byref(prm.c()), batch, _p(ctx_len), _p(page_table), max_pages,
@@ -257,6 +319,23 @@ def index_decode(prm: IndexParams, ctx_len: torch.Tensor, page_table: torch.Tens
     return o
 
 
+def _attn_io(prm: AttnParams, q, kv, out, lse, paged: bool):
+    """Checks q and kv, allocates out / lse when asked to; returns (n_rows, n_kv_rows, out, lse)."""
+    _need("q", q, _BF16, (None, prm.n_heads, prm.d_qk))
+    n_rows, dev = q.shape[0], q.device
+    _need("kv", kv, _BF16, (None, None, prm.d_qk) if paged else (None, prm.d_qk), dev)
+    n_kv_rows = kv.shape[0] * (kv.shape[1] if paged else 1)
+    if out is None:
+        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=dev)
+    _need("out", out, _BF16, (n_rows, prm.n_heads, prm.d_v), dev)
+    if lse is True:
+        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=dev)
+    elif lse is False:
+        lse = None
+    _need_opt("lse", lse, _F32, (n_rows, prm.n_heads), dev)
+    return n_rows, n_kv_rows, out, lse
+
+
 def sparse_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, v: torch.Tensor | None,
                 idx: torch.Tensor, count: torch.Tensor, page_table: torch.Tensor | None = None,
                 kv_page_size: int = 0, rows_per_seq: int = 1, out: torch.Tensor | None = None,
@@ -264,16 +343,24 @@ def sparse_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, v: torch.Ten
     """Sparse attention over idx (lsa_sparse_attn). Returns (out [n_rows, H, d_v] bf16, lse or None).
 
     kv: contiguous [n_kv_rows, d_qk] or paged [n_phys, page, d_qk] (then page_table is required)."""
-    n_rows = q.shape[0]
+    paged = page_table is not None
+    n_rows, n_kv_rows, out, lse = _attn_io(prm, q, kv, out, lse, paged)
+    dev = q.device
+    if prm.latent:
+        if v is not None:
+            raise ValueError("v must be None with a latent cache (V is the first d_v columns of kv)")
+    else:
+        _need("v", v, _BF16, tuple(kv.shape[:-1]) + (prm.d_v,), dev)
+    _need("idx", idx, _I32, (n_rows, None), dev)
     k_cap = idx.shape[1]
-    n_kv_rows = kv.shape[0] * (kv.shape[1] if page_table is not None else 1)
-    if out is None:
-        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=q.device)
-    if lse is True:
-        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=q.device)
-    elif lse is False:
-        lse = None
-    max_pages = page_table.shape[1] if page_table is not None else 0
+    _need("count", count, _I32, (n_rows,), dev)
+    if paged:
+        if kv.shape[1] != kv_page_size:
+            raise ValueError(f"paged kv has pages of {kv.shape[1]} rows, kv_page_size is {kv_page_size}")
+        if rows_per_seq < 1:
+            raise ValueError("rows_per_seq must be >= 1")
+        _need("page_table", page_table, _I32, (None, None), dev, min_rows=-(-n_rows // rows_per_seq))
+    max_pages = page_table.shape[1] if paged else 0
     ws, wsb = _workspace(attn_workspace_size(prm, n_rows, k_cap, page_table is not None), q.device, workspace)
     _check(lib().lsa_sparse_attn(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), _p(v), n_kv_rows, _p(idx),
                                  _p(count), k_cap, _p(page_table), max_pages, kv_page_size, rows_per_seq,
@@ -287,16 +374,12 @@ def sparse_attn_runs(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, runs: t
                      workspace: torch.Tensor | None = None):
     """Sparse attention over the run form of the lists (lsa_sparse_attn_runs): runs [n_rows, k_cap, 2]
     int32 (start, length) as index_prefill returns them, run_count [n_rows]. Returns (out, lse or None)."""
-    n_rows = q.shape[0]
+    n_rows, n_kv_rows, out, lse = _attn_io(prm, q, kv, out, lse, False)
+    _need("runs", runs, _I32, (n_rows, None, 2), q.device)
     k_cap = runs.shape[1]
-    if out is None:
-        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=q.device)
-    if lse is True:
-        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=q.device)
-    elif lse is False:
-        lse = None
+    _need("run_count", run_count, _I32, (n_rows,), q.device)
     ws, wsb = _workspace(attn_workspace_size(prm, n_rows, k_cap, False), q.device, workspace)
-    _check(lib().lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), kv.shape[0], _p(runs),
+    _check(lib().lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), n_kv_rows, _p(runs),
                                       _p(run_count), k_cap, _p(out), _p(lse), _p(ws), wsb, _stream(q.device)),
            "lsa_sparse_attn_runs")
     return out, lse
@@ -311,16 +394,12 @@ def hfa_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, idx: torch.Tens
              workspace: torch.Tensor | None = None):
     """Split attention (lsa_hfa_attn): listed non-window part and contiguous window on two streams,
     merged by log-sum-exp rescaling. Returns (out, lse or None) as sparse_attn."""
-    n_rows = q.shape[0]
+    n_rows, n_kv_rows, out, lse = _attn_io(prm, q, kv, out, lse, False)
+    _need("idx", idx, _I32, (n_rows, None), q.device)
     k_cap = idx.shape[1]
-    if out is None:
-        out = torch.empty((n_rows, prm.n_heads, prm.d_v), dtype=torch.bfloat16, device=q.device)
-    if lse is True:
-        lse = torch.empty((n_rows, prm.n_heads), dtype=torch.float32, device=q.device)
-    elif lse is False:
-        lse = None
+    _need("count", count, _I32, (n_rows,), q.device)
     ws, wsb = _workspace(hfa_workspace_size(prm, n_rows), q.device, workspace)
-    _check(lib().lsa_hfa_attn(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), kv.shape[0], _p(idx), _p(count), k_cap,
+    _check(lib().lsa_hfa_attn(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), n_kv_rows, _p(idx), _p(count), k_cap,
                               q_start, k_swa, _p(out), _p(lse), _p(ws), wsb, _stream(q.device)), "lsa_hfa_attn")
     return out, lse
 

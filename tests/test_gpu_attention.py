@@ -333,3 +333,43 @@ def test_split_attention_parity(w):
     assert np.max(np.abs(l - lf)) <= 2e-3, np.max(np.abs(l - lf))
     print(w.name, "worst vs oracle", worst, "max |hfa - fused|", float(np.max(np.abs(o - of))))
 
+
+
+def test_binding_rejects_mismatched_tensors():
+    """The C ABI sees bare pointers, so the binding checks every tensor against the sizes it passes
+    (dtype, device, contiguity, shape) and raises before anything is launched."""
+    w = W.SMALL_MLA
+    n, k_cap = 64, 96
+    prm = w.attn_params()
+    a = _attn_inputs(w, 0, n, 300)
+    q, kv = P.bf16_dev(a["q"][:n]), P.bf16_dev(a["kv"])
+    idx = torch.zeros((n, k_cap), dtype=torch.int32, device=q.device)
+    cnt = torch.ones((n,), dtype=torch.int32, device=q.device)
+    lsa.sparse_attn(prm, q, kv, None, idx, cnt)   # the well-formed call works
+    bad = {
+        "idx dtype": lambda: lsa.sparse_attn(prm, q, kv, None, idx.long(), cnt),
+        "idx rows": lambda: lsa.sparse_attn(prm, q, kv, None, idx[: n - 1], cnt),
+        "count rows": lambda: lsa.sparse_attn(prm, q, kv, None, idx, cnt[: n - 1]),
+        "q not contiguous": lambda: lsa.sparse_attn(prm, q.transpose(0, 1).contiguous().transpose(0, 1), kv, None,
+                                                    idx, cnt),
+        "kv width": lambda: lsa.sparse_attn(prm, q, kv[:, :512].contiguous(), None, idx, cnt),
+        "out shape": lambda: lsa.sparse_attn(prm, q, kv, None, idx, cnt,
+                                             out=torch.empty((n - 1, 64, 512), dtype=torch.bfloat16, device=q.device)),
+        "kv on host": lambda: lsa.sparse_attn(prm, q, kv.cpu(), None, idx, cnt),
+        "runs shape": lambda: lsa.sparse_attn_runs(prm, q, kv, torch.zeros((n, k_cap), dtype=torch.int32,
+                                                                           device=q.device), cnt),
+    }
+    for name, call in bad.items():
+        with pytest.raises(ValueError):
+            call()
+            pytest.fail(name)
+    wi = W.SMALL_CLI
+    iprm = wi.index_params()
+    inp = synth.indexer_inputs(wi.seed, 256, 256, wi.n_heads, wi.head_dim, wi.fp8)
+    qi, wt, k, ks = P.gpu_index_inputs(inp, wi)
+    bk = lsa.block_keys(iprm, k, ks)
+    with pytest.raises(ValueError):   # more cached tokens claimed than the key tensor holds
+        lsa.index_prefill(iprm, qi, wt, k, ks, bk, 0, n_kv=k.shape[0] + 1)
+    with pytest.raises(ValueError):   # head weights of the wrong dtype
+        lsa.index_prefill(iprm, qi, wt.double(), k, ks, bk, 0)
+    torch.cuda.synchronize()
