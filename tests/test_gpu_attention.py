@@ -147,6 +147,27 @@ def test_long_lists_beyond_one_staging_pass():
         P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({cnt[i]} entries)")
 
 
+def test_mqa_long_lists():
+    """MQA (16 x 128, separate K and V) over lists far longer than the L = 2048 workload's (1, 31,
+    32, 33, 4097 and 9000 entries, the last tile partial), against the oracle."""
+    from dataclasses import replace
+    w = replace(W.L2K_MQA, seq_len=12000)
+    n_kv = w.seq_len
+    counts = [1, 31, 32, 33, 4097, 9000]
+    a = _attn_inputs(w, 0, len(counts), n_kv)
+    k_cap = max(counts)
+    g = np.random.default_rng(11)
+    idx = np.full((len(counts), k_cap), -1, np.int32)
+    cnt = np.array(counts, np.int32)
+    for i, c in enumerate(counts):
+        idx[i, :c] = np.sort(g.choice(n_kv, c, replace=False))
+    o, l = _gpu_attn(w, a, list(range(len(counts))), idx, cnt)
+    H, dqk, dv = w.attn_dims
+    for i in range(len(counts)):
+        oref, lref = orc.attention_for_set(a["q"][i], a["kv"], a["v"], idx[i, :cnt[i]], dv, w.sm_scale)
+        P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({cnt[i]} entries)")
+
+
 @pytest.mark.parametrize("n_rows", [None, 8], ids=["all_rows", "split_8_rows"])
 def test_run_form_equals_list_form(n_rows):
     """Attention over the indexer's run encoding equals attention over its index lists, bit for bit
