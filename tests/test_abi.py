@@ -6,6 +6,7 @@ import os
 import re
 
 import pytest
+import torch
 
 from paper_2608_01662_amd import lsa
 
@@ -237,3 +238,22 @@ def test_zero_sized_calls_accept_null_buffers():
     mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
     assert L.lsa_sparse_attn(ctypes.byref(mla.c()), 0, None, FAKE, None, 10, None, None, 8, None, 0, 0, 1,
                              None, None, None, 0, None) == OK
+
+
+def test_binding_refuses_host_tensors():
+    """The product path never computes on the CPU: host tensors are refused by the binding before
+    the library is called (there is no CPU fallback)."""
+    mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+    q = torch.zeros((2, 64, 576), dtype=torch.bfloat16)
+    kv = torch.zeros((8, 576), dtype=torch.bfloat16)
+    idx = torch.zeros((2, 4), dtype=torch.int32)
+    cnt = torch.ones((2,), dtype=torch.int32)
+    with pytest.raises(ValueError, match="CUDA"):
+        lsa.sparse_attn(mla, q, kv, None, idx, cnt)
+    with pytest.raises(ValueError, match="CUDA"):
+        lsa.sparse_attn_runs(mla, q, kv, torch.zeros((2, 4, 2), dtype=torch.int32), cnt)
+    prm = P()
+    with pytest.raises(ValueError, match="CUDA"):
+        lsa.index_prefill(prm, torch.zeros((2, prm.n_heads, prm.head_dim), dtype=torch.bfloat16),
+                          torch.zeros((2, prm.n_heads)), torch.zeros((8, prm.head_dim), dtype=torch.uint8),
+                          torch.ones(8), None, 0)
