@@ -303,7 +303,7 @@ def main():
                     help="coarse-stage block summary: mean keys (Eq. 9) or min-max extrema (Eq. 13)")
     ap.add_argument("--attn", default="fused", choices=["fused", "runs", "split"],
                     help="sparse attention as one fused pass over S_t (lsa_sparse_attn), the same pass "
-                         "reading S_t from its run encoding (lsa_sparse_attn_runs, MLA only), or split into "
+                         "reading S_t from its run encoding (lsa_sparse_attn_runs), or split into "
                          "the listed part and the contiguous window on two streams, merged by log-sum-exp "
                          "(lsa_hfa_attn)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -319,8 +319,6 @@ def main():
         sys.exit(2)
     if args.steps < 1 or args.warmup < 0:
         sys.exit("--steps must be >= 1 and --warmup >= 0")
-    if args.attn == "runs" and W.BY_NAME[args.workload].attn != "mla":
-        sys.exit("bench.py: --attn runs needs an MLA workload (the run form is an MLA entry point)")
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
@@ -355,7 +353,9 @@ def main():
     ws_idx = torch.empty(max(1, lsa.index_workspace_size(prm, n_q, n)), dtype=torch.uint8, device=dev)
     split_attn = args.attn == "split"
     runs_attn = args.attn == "runs"
-    ws_attn_n = (lsa.hfa_workspace_size(aprm, n_q) if split_attn else lsa.attn_workspace_size(aprm, n_q, w.k_cap, False))
+    ws_attn_n = (lsa.hfa_workspace_size(aprm, n_q) if split_attn else
+                 lsa.attn_runs_workspace_size(aprm, n_q, w.k_cap, False) if runs_attn else
+                 lsa.attn_workspace_size(aprm, n_q, w.k_cap, False))
     ws_attn = torch.empty(max(1, ws_attn_n), dtype=torch.uint8, device=dev)
     O = [torch.empty((n_q, H, dv), dtype=torch.bfloat16, device=dev) for _ in range(w.layers)]
     LSE = [torch.empty((n_q, H), dtype=torch.float32, device=dev) for _ in range(w.layers)]
@@ -381,7 +381,7 @@ def main():
                              lse=LSE[l], workspace=ws_attn)
             elif runs_attn:
                 lsa.sparse_attn_runs(aprm, t["Q"][l], t["KV"][l], out["runs"], out["run_count"], out=O[l],
-                                     lse=LSE[l], workspace=ws_attn if ws_attn_n else None)
+                                     lse=LSE[l], workspace=ws_attn if ws_attn_n else None, v=t["V"][l])
             else:
                 lsa.sparse_attn(aprm, t["Q"][l], t["KV"][l], t["V"][l], out["idx"], out["count"], out=O[l],
                                 lse=LSE[l], workspace=ws_attn if ws_attn_n else None)

@@ -214,21 +214,25 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
 
 /*
  * Sparse attention, Eq. (3), over the run encoding of the index lists instead of idx/count: row
- * r attends to the concatenation of runs[r, 0..run_count[r]), run j covering cache rows
- * [start, start + len) (lsa_index_prefill's runs output). The kernel expands the runs itself while
- * staging a row's list, so the result equals lsa_sparse_attn over the same list, bit for bit.
- * MLA latent cache only, contiguous cache only.
+ * r attends to the concatenation of runs[r, 0..run_count[r]), run j covering positions
+ * [start, start + len) (the runs output of lsa_index_prefill / lsa_index_decode). The result equals
+ * lsa_sparse_attn over the same list, bit for bit. With a contiguous MLA latent cache the kernel
+ * expands the runs itself while staging a row's list; otherwise (MQA, paged cache) the runs are
+ * first expanded into a position list at the head of the workspace.
  *   runs       [n_rows, k_cap] lsa_run, 8-byte aligned; run_count [n_rows] int32, clamped to
  *              [0, k_cap]
  *   k_cap      row stride of runs and the list capacity: entries past k_cap are not attended;
  *              negative lengths count as 0; entries outside [0, n_kv_rows) are skipped
- *   workspace  >= lsa_sparse_attn_workspace_size(p, n_rows, k_cap, 0)
- * Other arguments as lsa_sparse_attn.
+ *   workspace  >= lsa_sparse_attn_runs_workspace_size(p, n_rows, k_cap, page_table != NULL)
+ * Other arguments (v, page_table, max_pages, kv_page_size, rows_per_seq) as lsa_sparse_attn.
  */
+size_t lsa_sparse_attn_runs_workspace_size(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap,
+                                           int32_t paged);
 lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const void* q,
-                                const void* kv, int64_t n_kv_rows, const lsa_run* runs,
-                                const int32_t* run_count, int32_t k_cap, void* out, float* lse,
-                                void* workspace, size_t ws_bytes, void* stream);
+                                const void* kv, const void* v, int64_t n_kv_rows, const lsa_run* runs,
+                                const int32_t* run_count, int32_t k_cap, const int32_t* page_table,
+                                int32_t max_pages, int32_t kv_page_size, int32_t rows_per_seq,
+                                void* out, float* lse, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Split sparse attention of prefill (Sec. 4.1.1, the hybrid operator): the same result as

@@ -1369,6 +1369,63 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, 
   if (i < n) p[i] = v;
 }
 
+// Inverse of the run encoding: row r's runs [start, start + len) -> its position list
+// idx[r, 0..count[r]) (cut at k_cap entries; lengths clamped to [0, k_cap], run counts to
+// [0, k_cap]). One workgroup per row; thread t expands the contiguous block of runs
+// [t U, t U + U), U = ceil(n_runs / 256), at the list offset a block prefix over the run
+// lengths gives it. Positions outside [0, 2^31) are written as -1 (skipped by attention).
+__global__ __launch_bounds__(256) void expand_runs_kernel(const int32_t* __restrict__ runs,
+                                                          const int32_t* __restrict__ run_count, int k_cap,
+                                                          int32_t* __restrict__ idx, int32_t* __restrict__ count) {
+  __shared__ int64_t wtot[4];
+  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int nr = run_count[row];
+  nr = nr < 0 ? 0 : (nr > k_cap ? k_cap : nr);
+  const int u = (nr + 255) / 256;
+  const int b = (int)threadIdx.x * u < nr ? (int)threadIdx.x * u : nr;
+  const int e = b + u < nr ? b + u : nr;
+  const int32_t* rr = runs + row * k_cap * 2;
+  auto len_of = [&](int r) {
+    const int l = rr[2 * r + 1];
+    return (int64_t)(l < 0 ? 0 : (l > k_cap ? k_cap : l));
+  };
+  int64_t mine = 0;
+  for (int r = b; r < e; ++r) mine += len_of(r);
+  int64_t inc = mine;  // inclusive prefix over the block
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
+  }
+  if (lane == 63) wtot[wv] = inc;
+  __syncthreads();
+  int64_t off = inc - mine, total = 0;
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+    off += x < wv ? wtot[x] : 0;
+    total += wtot[x];
+  }
+  int32_t* out = idx + row * k_cap;
+  for (int r = b; r < e && off < k_cap; ++r) {
+    const int64_t start = rr[2 * r], len = len_of(r);
+    const int64_t p1 = off + len < k_cap ? off + len : k_cap;
+    for (int64_t p = off; p < p1; ++p) {
+      const int64_t v = start + (p - off);
+      out[p] = (v >= 0 && v < (1LL << 31)) ? (int32_t)v : -1;
+    }
+    off += len;
+  }
+  if (threadIdx.x == 0) count[row] = (int32_t)(total < k_cap ? total : k_cap);
+}
+
+hipError_t launch_expand_runs(const int32_t* runs, const int32_t* run_count, int64_t n_rows, int k_cap, int32_t* idx,
+                              int32_t* count, hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(expand_runs_kernel, dim3((unsigned)n_rows), dim3(256), 0, st, runs, run_count, k_cap, idx, count);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n, v);

@@ -43,6 +43,9 @@ hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_
 hipError_t prepare_index_kernels();
 // p[0..n) = v (a kernel, so that the call also records correctly inside a captured graph).
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st);
+// Run encoding -> position list: idx[r, 0..count[r]) from runs[r, 0..run_count[r]) (int32 pairs).
+hipError_t launch_expand_runs(const int32_t* runs, const int32_t* run_count, int64_t n_rows, int k_cap, int32_t* idx,
+                              int32_t* count, hipStream_t st);
 
 // Sparse attention over gathered rows.
 struct AttnGeom {

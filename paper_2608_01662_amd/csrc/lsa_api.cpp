@@ -466,13 +466,30 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
   return LSA_OK;
 }
 
-lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv,
+// The run form reads the runs inside the attention kernel for the contiguous MLA cache; any other
+// layout (MQA, paged cache) first expands them into a position list at the head of the workspace
+// and then runs the list form on it.
+static bool runs_fused(const lsa_attn_params* p, bool paged) { return p->latent != 0 && !paged; }
+
+static size_t runs_list_bytes(int64_t n_rows, int32_t k_cap) {
+  return round_up((size_t)n_rows * k_cap * 4, 256) + round_up((size_t)n_rows * 4, 256);
+}
+
+size_t lsa_sparse_attn_runs_workspace_size(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int32_t paged) {
+  if (check_attn_params(p) != LSA_OK || n_rows < 0 || k_cap < 1) return 0;
+  const size_t attn = plan_attn(p, n_rows, k_cap, paged).total;
+  return runs_fused(p, paged != 0) ? attn : runs_list_bytes(n_rows, k_cap) + attn;
+}
+
+lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv, const void* v,
                                 int64_t n_kv_rows, const lsa_run* runs, const int32_t* run_count, int32_t k_cap,
-                                void* out, float* lse, void* workspace, size_t ws_bytes, void* stream) {
+                                const int32_t* page_table, int32_t max_pages, int32_t kv_page_size,
+                                int32_t rows_per_seq, void* out, float* lse, void* workspace, size_t ws_bytes,
+                                void* stream) {
   g_err[0] = 0;
   lsa_status s = check_attn_params(p);
   if (s != LSA_OK) return s;
-  LSA_REQUIRE(p->latent != 0, LSA_ERR_UNSUPPORTED, "the run form is implemented for the MLA latent cache");
+  const bool mla = p->latent != 0, paged = page_table != nullptr;
   LSA_REQUIRE(n_rows >= 0 && k_cap >= 1, LSA_ERR_INVALID_ARG, "n_rows < 0 or k_cap < 1");
   LSA_REQUIRE(n_rows < (1LL << 31) && k_cap < (1 << 30), LSA_ERR_UNSUPPORTED, "n_rows must be < 2^31, k_cap < 2^30");
   if (n_rows == 0) return LSA_OK;  // nothing to read or write
@@ -480,15 +497,32 @@ lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const 
               (long long)n_kv_rows);
   LSA_REQUIRE(q && kv && runs && run_count && out, LSA_ERR_INVALID_ARG,
               "q, kv, runs, run_count and out must be non-NULL");
-  LSA_REQUIRE(aligned(q, 16) && aligned(kv, 16) && aligned(out, 16), LSA_ERR_INVALID_ARG,
-              "q, kv and out must be 16-byte aligned");
-  LSA_REQUIRE(aligned(runs, 8) && aligned(run_count, 4) && aligned(lse, 4), LSA_ERR_INVALID_ARG,
-              "runs must be 8-byte aligned, run_count and lse 4-byte aligned");
-  const AttnPlan pl = plan_attn(p, n_rows, k_cap, 0);
-  LSA_REQUIRE(pl.total == 0 || (workspace != nullptr && aligned(workspace, 256)), LSA_ERR_WORKSPACE,
+  LSA_REQUIRE(mla == (v == nullptr), LSA_ERR_INVALID_ARG, mla ? "v must be NULL for a latent cache" : "v is NULL");
+  LSA_REQUIRE(aligned(q, 16) && aligned(kv, 16) && aligned(v, 16) && aligned(out, 16), LSA_ERR_INVALID_ARG,
+              "q, kv, v and out must be 16-byte aligned");
+  LSA_REQUIRE(aligned(runs, 8) && aligned(run_count, 4) && aligned(lse, 4) && aligned(page_table, 4),
+              LSA_ERR_INVALID_ARG, "runs must be 8-byte aligned, run_count, lse and page_table 4-byte aligned");
+  if (paged)
+    LSA_REQUIRE(max_pages >= 1 && kv_page_size >= 1 && rows_per_seq >= 1, LSA_ERR_INVALID_ARG,
+                "paged cache needs max_pages, kv_page_size and rows_per_seq >= 1");
+  const size_t need = lsa_sparse_attn_runs_workspace_size(p, n_rows, k_cap, paged);
+  LSA_REQUIRE(need == 0 || (workspace != nullptr && aligned(workspace, 256)), LSA_ERR_WORKSPACE,
               "workspace must be non-NULL and 256-byte aligned");
-  LSA_REQUIRE(ws_bytes >= pl.total, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, pl.total);
+  LSA_REQUIRE(ws_bytes >= need, LSA_ERR_WORKSPACE, "workspace of %zu bytes < %zu needed", ws_bytes, need);
+  hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
+
+  if (!runs_fused(p, paged)) {
+    int32_t* idx = reinterpret_cast<int32_t*>(ws);
+    int32_t* count = reinterpret_cast<int32_t*>(ws + round_up((size_t)n_rows * k_cap * 4, 256));
+    const hipError_t e = lsa::launch_expand_runs(reinterpret_cast<const int32_t*>(runs), run_count, n_rows, k_cap,
+                                                 idx, count, st);
+    if (e != hipSuccess) return hip_fail(e, "run expansion");
+    const size_t head = runs_list_bytes(n_rows, k_cap);
+    return lsa_sparse_attn(p, n_rows, q, kv, v, n_kv_rows, idx, count, k_cap, page_table, max_pages, kv_page_size,
+                           rows_per_seq, out, lse, ws + head, ws_bytes - head, stream);
+  }
+  const AttnPlan pl = plan_attn(p, n_rows, k_cap, 0);
   lsa::AttnGeom a{};
   a.q = static_cast<const uint16_t*>(q);
   a.kv = static_cast<const uint16_t*>(kv);
@@ -507,7 +541,7 @@ lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const 
     a.part_o = reinterpret_cast<float*>(ws + pl.off_po);
     a.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   }
-  const hipError_t e = lsa::launch_mla_attn(a, static_cast<hipStream_t>(stream));
+  const hipError_t e = lsa::launch_mla_attn(a, st);
   if (e != hipSuccess) return hip_fail(e, "sparse attention (run form)");
   return LSA_OK;
 }

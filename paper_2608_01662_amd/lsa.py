@@ -117,7 +117,10 @@ def lib() -> ctypes.CDLL:
         L.lsa_sparse_attn.argtypes = [A, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _i32, _i32, _i32, _vp,
                                       _vp, _vp, _sz, _vp]
         L.lsa_sparse_attn.restype = _i32
-        L.lsa_sparse_attn_runs.argtypes = [A, _i64, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _vp, _vp, _sz, _vp]
+        L.lsa_sparse_attn_runs_workspace_size.argtypes = [A, _i64, _i32, _i32]
+        L.lsa_sparse_attn_runs_workspace_size.restype = _sz
+        L.lsa_sparse_attn_runs.argtypes = [A, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _i32, _i32, _i32,
+                                           _vp, _vp, _vp, _sz, _vp]
         L.lsa_sparse_attn_runs.restype = _i32
         L.lsa_hfa_attn_workspace_size.argtypes = [A, _i64]
         L.lsa_hfa_attn_workspace_size.restype = _sz
@@ -369,18 +372,39 @@ def sparse_attn(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, v: torch.Ten
     return out, lse
 
 
+def attn_runs_workspace_size(prm: AttnParams, n_rows: int, k_cap: int, paged: bool) -> int:
+    return int(lib().lsa_sparse_attn_runs_workspace_size(ctypes.byref(prm.c()), n_rows, k_cap, int(paged)))
+
+
 def sparse_attn_runs(prm: AttnParams, q: torch.Tensor, kv: torch.Tensor, runs: torch.Tensor, run_count: torch.Tensor,
                      out: torch.Tensor | None = None, lse: torch.Tensor | bool | None = True,
-                     workspace: torch.Tensor | None = None):
+                     workspace: torch.Tensor | None = None, v: torch.Tensor | None = None,
+                     page_table: torch.Tensor | None = None, kv_page_size: int = 0, rows_per_seq: int = 1):
     """Sparse attention over the run form of the lists (lsa_sparse_attn_runs): runs [n_rows, k_cap, 2]
-    int32 (start, length) as index_prefill returns them, run_count [n_rows]. Returns (out, lse or None)."""
-    n_rows, n_kv_rows, out, lse = _attn_io(prm, q, kv, out, lse, False)
-    _need("runs", runs, _I32, (n_rows, None, 2), q.device)
+    int32 (start, length) as the indexer returns them, run_count [n_rows]. Other arguments as
+    sparse_attn. Returns (out, lse or None)."""
+    paged = page_table is not None
+    n_rows, n_kv_rows, out, lse = _attn_io(prm, q, kv, out, lse, paged)
+    dev = q.device
+    if prm.latent:
+        if v is not None:
+            raise ValueError("v must be None with a latent cache (V is the first d_v columns of kv)")
+    else:
+        _need("v", v, _BF16, tuple(kv.shape[:-1]) + (prm.d_v,), dev)
+    _need("runs", runs, _I32, (n_rows, None, 2), dev)
     k_cap = runs.shape[1]
-    _need("run_count", run_count, _I32, (n_rows,), q.device)
-    ws, wsb = _workspace(attn_workspace_size(prm, n_rows, k_cap, False), q.device, workspace)
-    _check(lib().lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), n_kv_rows, _p(runs),
-                                      _p(run_count), k_cap, _p(out), _p(lse), _p(ws), wsb, _stream(q.device)),
+    _need("run_count", run_count, _I32, (n_rows,), dev)
+    if paged:
+        if kv.shape[1] != kv_page_size:
+            raise ValueError(f"paged kv has pages of {kv.shape[1]} rows, kv_page_size is {kv_page_size}")
+        if rows_per_seq < 1:
+            raise ValueError("rows_per_seq must be >= 1")
+        _need("page_table", page_table, _I32, (None, None), dev, min_rows=-(-n_rows // rows_per_seq))
+    max_pages = page_table.shape[1] if paged else 0
+    ws, wsb = _workspace(attn_runs_workspace_size(prm, n_rows, k_cap, paged), dev, workspace)
+    _check(lib().lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, _p(q), _p(kv), _p(v), n_kv_rows, _p(runs),
+                                      _p(run_count), k_cap, _p(page_table), max_pages, kv_page_size, rows_per_seq,
+                                      _p(out), _p(lse), _p(ws), wsb, _stream(dev)),
            "lsa_sparse_attn_runs")
     return out, lse
 

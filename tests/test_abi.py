@@ -171,19 +171,28 @@ def test_bad_run_form_attention_arguments():
     """lsa_sparse_attn_runs validates on the host before any launch."""
     L = lsa.lib()
     mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
+    mqa = lsa.AttnParams(sm_scale=0.1, **lsa.MQA)
 
-    def att(prm=mla, n_rows=8, q=FAKE, kv=FAKE, n_kv=4096, runs=FAKE, rc=FAKE, k_cap=64, out=FAKE, lse=None,
-            ws=FAKE, wsb=1 << 40):
-        return L.lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, q, kv, n_kv, runs, rc, k_cap, out, lse, ws, wsb,
-                                      None)
-    assert att(prm=lsa.AttnParams(sm_scale=0.1, **lsa.MQA)) == UNSUPPORTED     # MLA latent cache only
+    def att(prm=mla, n_rows=8, q=FAKE, kv=FAKE, v=None, n_kv=4096, runs=FAKE, rc=FAKE, k_cap=64, table=None,
+            max_pages=0, kv_page=0, rps=1, out=FAKE, lse=None, ws=FAKE, wsb=1 << 40):
+        return L.lsa_sparse_attn_runs(ctypes.byref(prm.c()), n_rows, q, kv, v, n_kv, runs, rc, k_cap, table, max_pages,
+                                      kv_page, rps, out, lse, ws, wsb, None)
+    assert att(prm=mqa) == INVALID                                             # MQA needs v
+    assert att(v=FAKE) == INVALID                                              # latent cache takes no v
     assert att(runs=None) == INVALID
     assert att(rc=None) == INVALID
     assert att(runs=ctypes.c_void_p(0x100004)) == INVALID                      # 8-byte (start, len) pairs
     assert att(k_cap=0) == INVALID
     assert att(n_kv=0) == INVALID
     assert att(q=MISALIGNED) == INVALID
+    assert att(table=FAKE, max_pages=0, kv_page=64) == INVALID                 # paged needs max_pages
     assert att(ws=None) == WORKSPACE                                           # 8 rows: split partials
+    # MQA and paged caches expand the runs into a list at the head of the workspace
+    need = L.lsa_sparse_attn_runs_workspace_size(ctypes.byref(mqa.c()), 8, 64, 0)
+    assert need >= 8 * 64 * 4 + 8 * 4
+    assert att(prm=mqa, v=FAKE, wsb=need - 1) == WORKSPACE
+    assert L.lsa_sparse_attn_runs_workspace_size(ctypes.byref(mla.c()), 131072, 3076, 0) == 0   # fused, no list
+    assert L.lsa_sparse_attn_runs_workspace_size(ctypes.byref(mla.c()), 64, 2308, 1) > 64 * 2308 * 4
     assert att(n_rows=0, q=None, runs=None, rc=None, out=None, ws=None, wsb=0) == OK
 
 

@@ -225,6 +225,74 @@ def test_run_form_edge_runs():
     assert torch.all(o2[3] == 0) and torch.all(torch.isneginf(l2[3]))
 
 
+def test_run_form_mqa_and_paged_equal_list_form():
+    """Run form where the runs are expanded into a list first: MQA over the L = 2048 workload's
+    indexer runs, and paged MLA decode over the decode indexer's runs (permuted page table);
+    each equals the list form bit for bit."""
+    w = W.L2K_MQA
+    inp = synth.indexer_inputs(w.seed, w.seq_len, w.seq_len, w.n_heads, w.head_dim, w.fp8)
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    out = lsa.index_prefill(prm, q, wt, k, ks, lsa.block_keys(prm, k, ks), 0, n_kv=w.seq_len, runs=True)
+    a = _attn_inputs(w, 0, w.seq_len, w.seq_len)
+    qa, kv, v = P.bf16_dev(a["q"]), P.bf16_dev(a["kv"]), P.bf16_dev(a["v"])
+    o1, l1 = lsa.sparse_attn(w.attn_params(), qa, kv, v, out["idx"], out["count"])
+    o2, l2 = lsa.sparse_attn_runs(w.attn_params(), qa, kv, out["runs"], out["run_count"], v=v)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2), "MQA run form differs"
+
+    wd = W.SMALL_DECODE
+    H, dqk, dv = wd.attn_dims
+    ctx, table, n_phys = synth.decode_layout(wd.seed, wd.batch, wd.ctx_lo, wd.ctx_hi, wd.kv_page)
+    inp = synth.indexer_inputs(wd.seed, wd.batch, n_phys * wd.kv_page, wd.n_heads, wd.head_dim, wd.fp8)
+    prm = wd.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, wd)
+    dtab = P.to_dev(table)
+    out = lsa.index_decode(prm, P.to_dev(ctx), dtab, wd.kv_page, n_phys, q, wt, k, ks, lsa.block_keys(prm, k, ks))
+    a = synth.attention_inputs(wd.seed, 0, wd.batch, n_phys * wd.kv_page, H, dqk, dv, latent=True)
+    qa, kv = P.bf16_dev(a["q"]), P.bf16_dev(a["kv"]).view(n_phys, wd.kv_page, dqk)
+    o1, l1 = lsa.sparse_attn(wd.attn_params(), qa, kv, None, out["idx"], out["count"], page_table=dtab,
+                             kv_page_size=wd.kv_page)
+    o2, l2 = lsa.sparse_attn_runs(wd.attn_params(), qa, kv, out["runs"], out["run_count"], page_table=dtab,
+                                  kv_page_size=wd.kv_page)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2), "paged run form differs"
+
+
+def test_run_expansion_edge_runs_mqa():
+    """The run expansion (MQA path) on hand-made runs: out-of-range starts, negative lengths, an
+    empty row, a length of 2^31 - 1 and a run count above k_cap; equal to the list form."""
+    from dataclasses import replace
+    w = replace(W.L2K_MQA, seq_len=600)
+    n_kv, k_cap, B = w.seq_len, 96, 6
+    a = _attn_inputs(w, 0, B, n_kv)
+    spec = [[(0, 4), (100, 30), (590, 20)],
+            [(-5, 10), (40, 1), (41, 7)],
+            [(10, 3), (20, -4), (30, 5)],
+            [],
+            [(3, 2 ** 31 - 1), (10, 5)],
+            [(i * 5, 1) for i in range(k_cap)]]
+    runs = np.zeros((B, k_cap, 2), np.int32)
+    rc = np.zeros(B, np.int32)
+    idx = np.full((B, k_cap), -1, np.int32)
+    cnt = np.zeros(B, np.int32)
+    for b, rs in enumerate(spec):
+        rc[b] = len(rs) if b != B - 1 else k_cap + 7     # the last row claims more runs than fit
+        lst = []
+        for j, (st, ln) in enumerate(rs):
+            runs[b, j] = (st, ln)
+            lst += list(range(st, st + min(max(ln, 0), k_cap)))
+        lst = lst[:k_cap]
+        cnt[b] = len(lst)
+        idx[b, :len(lst)] = lst
+    qa, kv, v = P.bf16_dev(a["q"][:B]), P.bf16_dev(a["kv"]), P.bf16_dev(a["v"])
+    o1, l1 = lsa.sparse_attn(w.attn_params(), qa, kv, v, P.to_dev(idx), P.to_dev(cnt))
+    o2, l2 = lsa.sparse_attn_runs(w.attn_params(), qa, kv, P.to_dev(runs), P.to_dev(rc), v=v)
+    torch.cuda.synchronize()
+    for b in range(B):
+        assert torch.equal(o1[b], o2[b]) and torch.equal(l1[b], l2[b]), f"row {b}"
+
+
 def test_run_form_long_and_many_runs():
     """Run form over lists of up to 16448 entries (several LDS staging passes, runs straddling a
     pass boundary), with thousands of runs per row (several batches per thread), more long runs
