@@ -1371,9 +1371,11 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, 
 
 // Inverse of the run encoding: row r's runs [start, start + len) -> its position list
 // idx[r, 0..count[r]) (cut at k_cap entries; lengths clamped to [0, k_cap], run counts to
-// [0, k_cap]). One workgroup per row; thread t expands the contiguous block of runs
+// [0, k_cap]). One workgroup per row; thread t takes the contiguous block of runs
 // [t U, t U + U), U = ceil(n_runs / 256), at the list offset a block prefix over the run
-// lengths gives it. Positions outside [0, 2^31) are written as -1 (skipped by attention).
+// lengths gives it, writes its short runs and queues the long ones (sink and window stretches),
+// which the whole block then writes. Positions outside [0, 2^31) are written as -1 (skipped by
+// attention).
 __global__ __launch_bounds__(256) void expand_runs_kernel(const int32_t* __restrict__ runs,
                                                           const int32_t* __restrict__ run_count, int k_cap,
                                                           int32_t* __restrict__ idx, int32_t* __restrict__ count) {
@@ -1406,16 +1408,41 @@ __global__ __launch_bounds__(256) void expand_runs_kernel(const int32_t* __restr
     off += x < wv ? wtot[x] : 0;
     total += wtot[x];
   }
+  // short runs are written by their thread; longer ones are queued and written by the whole block
+  constexpr int kShort = 8, kQueue = 64;
+  __shared__ int64_t qstart[kQueue];
+  __shared__ int32_t qoff[kQueue], qlen[kQueue];
+  __shared__ int qn;
+  if (threadIdx.x == 0) qn = 0;
+  __syncthreads();
   int32_t* out = idx + row * k_cap;
+  auto put = [&](int64_t start, int64_t p0, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) {
+      const int64_t v = start + i;
+      out[p0 + i] = (v >= 0 && v < (1LL << 31)) ? (int32_t)v : -1;
+    }
+  };
   for (int r = b; r < e && off < k_cap; ++r) {
     const int64_t start = rr[2 * r], len = len_of(r);
-    const int64_t p1 = off + len < k_cap ? off + len : k_cap;
-    for (int64_t p = off; p < p1; ++p) {
-      const int64_t v = start + (p - off);
-      out[p] = (v >= 0 && v < (1LL << 31)) ? (int32_t)v : -1;
+    const int64_t n = (off + len < k_cap ? off + len : k_cap) - off;
+    int slot = kQueue;
+    if (n > kShort) slot = atomicAdd(&qn, 1);
+    if (slot < kQueue) {
+      qstart[slot] = start;
+      qoff[slot] = (int32_t)off;
+      qlen[slot] = (int32_t)n;
+    } else {
+      put(start, off, n);
     }
     off += len;
   }
+  __syncthreads();
+  const int nq = qn < kQueue ? qn : kQueue;
+  for (int j = 0; j < nq; ++j)
+    for (int i = (int)threadIdx.x; i < qlen[j]; i += 256) {
+      const int64_t v = qstart[j] + i;
+      out[qoff[j] + i] = (v >= 0 && v < (1LL << 31)) ? (int32_t)v : -1;
+    }
   if (threadIdx.x == 0) count[row] = (int32_t)(total < k_cap ? total : k_cap);
 }
 
