@@ -266,3 +266,17 @@ def test_binding_refuses_host_tensors():
         lsa.index_prefill(prm, torch.zeros((2, prm.n_heads, prm.head_dim), dtype=torch.bfloat16),
                           torch.zeros((2, prm.n_heads)), torch.zeros((8, prm.head_dim), dtype=torch.uint8),
                           torch.ones(8), None, 0)
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/lsa.h is a C header: it compiles as C99 (pedantic) and as C++11."""
+    import shutil
+    import subprocess
+    for cc, std, ext in (("gcc", "-std=c99", "c"), ("g++", "-std=c++11", "cpp")):
+        if shutil.which(cc) is None:
+            pytest.skip(f"{cc} not available")
+        src = tmp_path / f"use.{ext}"
+        src.write_text('#include "lsa.h"\nint main(void) { return lsa_version() == 0; }\n')
+        r = subprocess.run([cc, std, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only",
+                            f"-I{os.path.join(ROOT, 'include')}", str(src)], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
