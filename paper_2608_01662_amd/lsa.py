@@ -264,6 +264,8 @@ def _index_outputs(prm: IndexParams, n_rows: int, device, runs: bool, pages: boo
     shapes = {"idx": (n_rows, kc), "count": (n_rows,), "runs": (n_rows, kc, 2), "run_count": (n_rows,),
               "pages": (n_rows, prm.keep_pages)}
     for key, t in out.items():
+        if key not in shapes:
+            raise ValueError(f"unknown output {key!r} (expected {', '.join(shapes)})")
         _need(f"out[{key!r}]", t, _I32, shapes[key], device)
     return out
 
