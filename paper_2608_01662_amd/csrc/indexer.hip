@@ -518,7 +518,7 @@ __device__ __forceinline__ int fine_swz(int t) {
 }
 
 constexpr int kFineChunk = 64;  // key rows staged in LDS at a time
-constexpr int kFineRowsPerWave = 4;  // query rows a fine-scoring wave takes in turn
+constexpr int kFineRowsPerWave = 8;  // query rows a fine-scoring wave takes in turn
 
 // One direct global->LDS load (16 or 4 bytes per lane; lane i writes LDS bytes [lds + SIZE*i, ..)),
 // issued from asm so that the compiler's wait insertion does not drain it before LDS reads that it
