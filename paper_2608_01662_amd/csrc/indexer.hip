@@ -502,9 +502,9 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
   }
 }
 
-// Prefill variant (contiguous keys): one wave per (row, XCD). Workgroup b runs on XCD b mod 8,
-// and the wave of XCD x scores only the recalled pages p with p mod 8 == x, so each XCD's L2
-// holds one eighth of the keys instead of streaming all of them. A page's keys are one contiguous
+// Prefill variant (contiguous keys): one wave per (group of rows, XCD), the rows taken in turn.
+// Workgroup b runs on XCD b mod 8, and the wave of XCD x scores only the recalled pages p with
+// p mod 8 == x, so each XCD's L2 holds one eighth of the keys instead of streaming all of them. A page's keys are one contiguous
 // block of P rows, copied into LDS 64 rows at a time by direct loads in which the 16-byte granules
 // of one key row go to consecutive lanes (a few cache lines per load instead of one line per
 // lane); granule c of row t is stored at slot c ^ swz(t) so that the operand reads are
