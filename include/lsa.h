@@ -83,7 +83,8 @@ typedef struct lsa_run {
   int32_t len;
 } lsa_run;
 
-/* K_cap = k_sink + k_swa + k_sparse: the row length of idx and runs. */
+/* K_cap = k_sink + k_swa + k_sparse: the index budget K of Sec. 3.1, split by Eq. (6) into sink,
+ * sliding window and sparse part; the row length of idx and runs. 0 for a NULL p. */
 int32_t lsa_index_k_cap(const lsa_index_params* p);
 
 /*
@@ -113,6 +114,9 @@ lsa_status lsa_block_means(const lsa_index_params* p, int64_t n_tok, const void*
 lsa_status lsa_block_minmax(const lsa_index_params* p, int64_t n_tok, const void* k,
                             const float* k_scale, void* block_keys, void* stream);
 /*
+ * Maintenance of the Stage-1 block cache of Sec. 3.3 (mean keys of Eq. 9, or the extrema of
+ * Eq. 13), which the paper computes once and keeps current as the sequence grows (the block-mean
+ * maintenance it names among the hierarchy's costs).
  * Keeps a block cache current while tokens are appended (decode): recomputes, from the keys in
  * the cache, the summary of every sub-block that contains one of the n_rows token rows in `rows`
  * (mean keys as lsa_block_means, or [k_max | k_min] as lsa_block_minmax, by p->pooling). The
@@ -132,7 +136,10 @@ lsa_status lsa_block_keys_update(const lsa_index_params* p, int64_t n_rows, cons
  * and n_q < 2^28; longer prefills are issued in chunks through q_start).
  *   q          [n_q, H^I, d_I] bf16 indexer queries
  *   w          [n_q, H^I] fp32 head weights (any sign)
- *   k, k_scale [n_kv, d_I] keys (+ [n_kv] fp32 scales for fp8, NULL for bf16)
+ *   k, k_scale [n_kv, d_I] keys (+ [n_kv] fp32 scales for fp8, NULL for bf16). Scales must be
+ *              finite and >= 0: a token's scale multiplies its score after the ReLU and the head
+ *              sum, which equals Eq. (1) on the dequantised key s*k only for s >= 0 (the
+ *              per-token quantiser's max|k|/448 always is)
  *   block_keys [n_kv / B, d_I] bf16 from lsa_block_means, or [n_kv / B, 2 d_I] from
  *              lsa_block_minmax when p->pooling is LSA_POOL_MINMAX (ignored in flat mode, may be
  *              NULL)
@@ -155,7 +162,8 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
                              size_t ws_bytes, void* stream);
 
 /*
- * Indexer for decode: one query per sequence b at position t_b = ctx_len[b] - 1 (the new token
+ * Indexer for decode (the decode setting of Table 1): Eq. (6)-(7) and, in hierarchical mode,
+ * Eq. (9)-(12) for one query per sequence b at position t_b = ctx_len[b] - 1 (the new token
  * is already in the cache). Keys live in pages of kv_page_size tokens: logical position s of
  * sequence b is row s % kv_page_size of physical page page_table[b * max_pages + s / kv_page_size].
  * Hierarchical mode needs page == kv_page_size (one coarse page = one cache page).
@@ -247,8 +255,9 @@ lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const 
  *   k_swa      the indexer's window size: idx must end with the whole window of each row, as
  *              lsa_index_prefill writes it (rows shorter than the window hold [0, t])
  *   workspace  >= lsa_hfa_attn_workspace_size(p, n_rows) bytes, 256-byte aligned (fp32 partials)
- * Other arguments as lsa_sparse_attn. Calls on one device share the side stream: concurrent calls
- * from several host threads on one device are serialised by it.
+ * Other arguments as lsa_sparse_attn. Calls on one device share the side stream and its two
+ * events; the library enqueues one call's whole sequence under a lock, so concurrent calls from
+ * several host threads are correct (their work on the side stream runs one call after the other).
  */
 size_t lsa_hfa_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows);
 lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q, const void* kv, int64_t n_kv_rows,

@@ -22,21 +22,6 @@ constexpr float kLazy = 8.0f;  // rescale when the max grows by more than this (
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// acc *= alpha on an MFMA accumulator kept in AGPRs, element by element through one VGPR. Written
-// as asm so that the accumulators never need VGPR copies outside this (rare) path.
-template <typename V, int N>
-__device__ __forceinline__ V scale_acc(V acc, float alpha) {
-#pragma unroll
-  for (int r = 0; r < N; ++r) {
-    float x = acc[r], t;
-    asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
-                 : "+a"(x), "=&v"(t)
-                 : "v"(alpha));
-    acc[r] = x;
-  }
-  return acc;
-}
-
 __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb) {
   const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pa));
   const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(pb));
@@ -619,7 +604,5 @@ hipError_t launch_translate_rows(const int32_t* idx, const int32_t* count, int64
                      page_table, max_pages, kv_page, rows_per_seq, n_kv_rows, out_rows);
   return hipGetLastError();
 }
-
-hipError_t prepare_attn_kernels() { return hipSuccess; }
 
 }  // namespace lsa

@@ -1308,15 +1308,11 @@ hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, co
     return fp8 ? launch_fine_xcd_t<64, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st)
                : launch_fine_xcd_t<64, false>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st);
   }
-#define LSA_FINE(D_, F_, P_) return launch_fine_t<D_, F_, P_>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
-  if (g.D == 128) {
-    if (fp8) { if (paged) LSA_FINE(128, true, true); else LSA_FINE(128, true, false); }
-    else { if (paged) LSA_FINE(128, false, true); else LSA_FINE(128, false, false); }
-  } else {
-    if (fp8) { if (paged) LSA_FINE(64, true, true); else LSA_FINE(64, true, false); }
-    else { if (paged) LSA_FINE(64, false, true); else LSA_FINE(64, false, false); }
-  }
-#undef LSA_FINE
+  // paged decode: per (sequence, page) through the page table
+  if (g.D == 128) return fp8 ? launch_fine_t<128, true, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
+                             : launch_fine_t<128, false, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st);
+  return fp8 ? launch_fine_t<64, true, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
+             : launch_fine_t<64, false, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st);
 }
 
 // Which selection kernel serves rows of slots_cap candidates: keys in registers, staged in LDS,

@@ -83,6 +83,5 @@ hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st);
 hipError_t launch_translate_rows(const int32_t* idx, const int32_t* count, int64_t n_rows, int k_cap,
                                  const int32_t* page_table, int max_pages, int kv_page, int rows_per_seq,
                                  int64_t n_kv_rows, int32_t* out_rows, hipStream_t st);
-hipError_t prepare_attn_kernels();
 
 }  // namespace lsa

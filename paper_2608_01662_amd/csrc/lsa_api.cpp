@@ -566,7 +566,8 @@ struct HfaStreams {
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
 };
-std::mutex g_hfa_mu;
+std::mutex g_hfa_mu;       // creation of the per-device streams and events
+std::mutex g_hfa_call_mu;  // one call's enqueue sequence at a time
 HfaStreams g_hfa[64];
 
 hipError_t hfa_streams(HfaStreams** out) {
@@ -624,6 +625,10 @@ lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q,
   HfaStreams* hs = nullptr;
   hipError_t e = hfa_streams(&hs);
   if (e != hipSuccess) return hip_fail(e, "split attention streams");
+  // the side stream and the fork/join events are shared by every call on this device: enqueue a
+  // whole call's record / wait / launch sequence under the lock, so that the side stream never
+  // interleaves the parts of two calls and each part waits on its own call's fork
+  std::lock_guard<std::mutex> call_lock(g_hfa_call_mu);
   const int64_t rpp = hfa_rows_per_pass(n_rows);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   float* part_o = reinterpret_cast<float*>(ws);

@@ -7,7 +7,8 @@ context lengths and page tables. It holds none of the method's arithmetic. Both 
 
 Distributions (stand-ins for the paper's workloads, which need model activations):
   * indexer queries and keys  ~ N(0, 1) / sqrt(d_I)
-  * indexer head weights w    ~ U(0, 1)
+  * indexer head weights w    ~ U(0, 1); with signed weights (the head weights are a learned
+    projection of either sign) ~ U(-1, 1), every fifth row with all weights <= 0
   * attention queries, latent KV, K, V ~ N(0, 1)
   * fp8 keys: per-token scale sigma = max|k| / 448 (1 for an all-zero key), code = e4m3fn(k / sigma)
     with round-to-nearest-even after clamping to the finite range +-448.
@@ -47,13 +48,18 @@ def quantize_fp8_per_token(k: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
     return codes, scale
 
 
-def indexer_inputs(seed: int, n_q: int, n_kv: int, n_heads: int, head_dim: int, fp8: bool):
+def indexer_inputs(seed: int, n_q: int, n_kv: int, n_heads: int, head_dim: int, fp8: bool,
+                   signed_weights: bool = False):
     """Indexer query q_I [n_q, H, d] (bf16 bits), weights w [n_q, H] (fp32), key cache
-    k_I [n_kv, d] (bf16 bits, or e4m3fn codes plus per-token scale [n_kv])."""
+    k_I [n_kv, d] (bf16 bits, or e4m3fn codes plus per-token scale [n_kv]). signed_weights: w ~
+    U(-1, 1), and rows 0, 5, 10, ... get -|w| (all of their scores are then <= 0)."""
     s = np.float32(1.0 / np.sqrt(head_dim))
     q = to_bf16_bits(rng(seed, T_QI).standard_normal((n_q, n_heads, head_dim), dtype=np.float32) * s)
     k32 = rng(seed, T_KI).standard_normal((n_kv, head_dim), dtype=np.float32) * s
     w = rng(seed, T_W).random((n_q, n_heads), dtype=np.float32)
+    if signed_weights:
+        w = (np.float32(2.0) * w - np.float32(1.0)).astype(np.float32)
+        w[::5] = -np.abs(w[::5])
     if fp8:
         k, k_scale = quantize_fp8_per_token(k32)
     else:

@@ -40,7 +40,7 @@ def _indexer_oracle(w, q_rows, w_rows, codes, scales, rows_t, n_kv):
     k_hat = orc.dequantized_keys(codes[:n_kv], scales[:n_kv])
     k_mean = P.oracle_block_cache(w, k_hat)
     qf = orc.bf16_bits_to_f64(q_rows)
-    return [orc.index_row(t, qf[i], w_rows[i], k_hat, k_mean, prm) for i, t in enumerate(rows_t)]
+    return [P.oracle_index_row(t, qf[i], w_rows[i], k_hat, k_mean, prm) for i, t in enumerate(rows_t)]
 
 
 def _bits(t: torch.Tensor) -> np.ndarray:
@@ -190,7 +190,7 @@ def test_fullsize_decode_b64():
         k_log = orc.dequantized_keys(orc.logical_rows(codes, table[b], t + 1, w.kv_page),
                                      orc.logical_rows(scales, table[b], t + 1, w.kv_page))
         k_mean = P.oracle_block_cache(w, k_log)
-        res.append(orc.index_row(t, orc.bf16_bits_to_f64(qb[b]), wb[b], k_log, k_mean, prmo))
+        res.append(P.oracle_index_row(t, orc.bf16_bits_to_f64(qb[b]), wb[b], k_log, k_mean, prmo))
         rows_t.append(t)
     stats = P.check_index_rows(w, rows_t, g["idx"][batch_rows], g["count"][batch_rows], g["pages"][batch_rows], res)
     P.check_runs(g["runs"][batch_rows], g["run_count"][batch_rows], g["idx"][batch_rows], g["count"][batch_rows],

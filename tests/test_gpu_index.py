@@ -6,6 +6,8 @@ import numpy as np
 import pytest
 import torch
 
+from dataclasses import replace
+
 import oracle.lsa_oracle as orc
 from paper_2608_01662_amd import lsa, synth
 from paper_2608_01662_amd import workloads as W
@@ -36,7 +38,7 @@ def _oracle_rows(w, inp, rows_t):
     k_hat = P.oracle_keys(inp)
     k_mean = P.oracle_block_cache(w, k_hat) if w.keep_pages > 0 else None
     qf = orc.bf16_bits_to_f64(inp["q"])
-    return [orc.index_row(t, qf[t], inp["w"][t], k_hat, k_mean, prm) for t in rows_t]
+    return [P.oracle_index_row(t, qf[t], inp["w"][t], k_hat, k_mean, prm) for t in rows_t]
 
 
 # ----------------------------------------------------------------------------- mean keys
@@ -213,15 +215,18 @@ def test_adaptive_dispatch():
     assert not np.array_equal(hi["idx"], flat["idx"])      # the two modes do differ here
 
 
-@pytest.mark.parametrize("head_dim,fp8", [(128, False), (64, True)])
-@pytest.mark.parametrize("keep_pages", [8, 0])
-def test_index_prefill_other_key_formats(head_dim, fp8, keep_pages):
+@pytest.mark.parametrize("head_dim,fp8,keep_pages,pooling", [
+    (128, False, 8, "mean"), (128, False, 0, "mean"), (64, True, 8, "mean"), (64, True, 0, "mean"),
+    (64, True, 8, "minmax"), (64, False, 8, "minmax")],
+    ids=["d128_bf16_hi", "d128_bf16_flat", "d64_fp8_hi", "d64_fp8_flat", "d64_fp8_minmax", "d64_bf16_minmax"])
+def test_index_prefill_other_key_formats(head_dim, fp8, keep_pages, pooling):
     """The kernel instances the five workloads do not reach: bf16 keys with d_I = 128 and fp8 keys
-    with d_I = 64, hierarchical (coarse, page select, fine_xcd) and flat (flat_dense), against the
-    oracle on sampled rows."""
+    with d_I = 64, hierarchical (coarse_kernel<D, 4, false, false>, page select, fine_xcd_kernel)
+    and flat (flat_dense_kernel), and min-max pooling at d_I = 64 (coarse_kernel<64, 2, false,
+    true>), against the oracle on sampled rows."""
     from dataclasses import replace
-    w = replace(W.SMALL_CLI, name=f"small_d{head_dim}_{'fp8' if fp8 else 'bf16'}_m{keep_pages}", head_dim=head_dim,
-                fp8=fp8, keep_pages=keep_pages, seq_len=4096)
+    w = replace(W.SMALL_CLI, name=f"small_d{head_dim}_{'fp8' if fp8 else 'bf16'}_m{keep_pages}_{pooling}",
+                head_dim=head_dim, fp8=fp8, keep_pages=keep_pages, pooling=pooling, seq_len=4096)
     inp = P.prefill_inputs(w)
     out, _ = _run_prefill(w, inp, pages=keep_pages > 0)
     rows = _sample_rows(w.seq_len, 11, [w.k_sink + w.k_swa, w.k_sink + w.k_swa + w.page, w.seq_len - 2])
@@ -230,6 +235,63 @@ def test_index_prefill_other_key_formats(head_dim, fp8, keep_pages):
                                out["pages"][rows] if "pages" in out else None, res)
     P.check_runs(out["runs"][rows], out["run_count"][rows], out["idx"][rows], out["count"][rows], w.run_align)
     print(w.name, stats)
+
+
+@pytest.mark.parametrize("base,keep_pages", [(W.L2K_MQA, 16), (W.L2K_MQA, 0), (W.SMALL_CLI, 8),
+                                             (W.SMALL_MINMAX, 8), (W.SMALL_CLI, 0)],
+                         ids=["mqa_hi", "mqa_flat", "cli_hi", "cli_minmax", "cli_flat"])
+def test_signed_head_weights(base, keep_pages):
+    """Head weights of either sign (Eq. 1: w is a learned projection): w ~ U(-1, 1), and every
+    fifth row with all weights <= 0, so that all of its scores are <= 0. This runs the sign-aware
+    order keys of the page and token selections and the ReLU of the coarse and fine stages on
+    negative sums. Every row (L = 2048) or every third row (L = 8192) against the oracle,
+    stage-wise."""
+    from dataclasses import replace
+    w = replace(base, keep_pages=keep_pages)
+    inp = P.prefill_inputs(w, signed_weights=True)
+    assert (inp["w"] < 0).any() and (inp["w"][::5] <= 0).all()
+    out, _ = _run_prefill(w, inp, pages=keep_pages > 0)
+    n = w.seq_len
+    rows = _sample_rows(n, 1 if n <= 2048 else 3, [w.k_sink + w.k_swa, n - 2])
+    res = _oracle_rows(w, inp, rows)
+    neg = [r for r in res if r["score"].size and r["score"].max() <= 0]
+    assert len(neg) >= len(res) // 6, "rows whose scores are all <= 0 must be part of the check"
+    stats = P.check_index_rows(w, rows, out["idx"][rows], out["count"][rows],
+                               out["pages"][rows] if "pages" in out else None, res)
+    P.check_runs(out["runs"][rows], out["run_count"][rows], out["idx"][rows], out["count"][rows], w.run_align)
+    print(w.name, keep_pages, stats, "all-non-positive rows", len(neg))
+
+
+def _slots(w, n_kv):
+    """Candidate slots per row of the fine-score workspace: M * P, or every page in flat mode."""
+    return (w.keep_pages if w.keep_pages > 0 else -(-n_kv // w.page)) * w.page
+
+
+@pytest.mark.parametrize("seq_len,lo,hi", [(12288, 8192, 16384), (36000, 32768, 36900)],
+                         ids=["reg_kpt32", "lds_staged"])
+def test_selection_instances(seq_len, lo, hi):
+    """The two selection kernels no workload reaches. Flat indexing (Eq. 7) with P = 128 and the
+    L = 128K budget (K_cap = 4 + 1024 + 2048):
+      * L = 12288: 96 pages = 12288 candidate slots per row, served by
+        token_select_reg_kernel<512, 32> (keys in registers, 8193..16384 slots);
+      * L = 36000: 282 pages = 36096 slots, served by token_select_kernel<512, false> (keys staged
+        in LDS: more than the 32768 register slots, and slots + K_cap within the 156 KB of LDS).
+    The last 256 rows of the cache, every third one against the oracle."""
+    from dataclasses import replace
+    w = replace(W.L128K_CLI4, name=f"flat_L{seq_len}", seq_len=seq_len, keep_pages=0, layers=1)
+    slots = _slots(w, seq_len)
+    assert lo < slots <= hi, slots
+    if seq_len > 32768:
+        assert (slots + w.k_cap) * 4 <= 160 * 1024 - 4096   # keys (reused for the run scratch) + list fit in LDS
+    inp = P.prefill_inputs(w)
+    q0 = seq_len - 256
+    out, _ = _run_prefill(w, inp, q_start=q0, pages=False)
+    rows = sorted(set(range(q0, seq_len, 3)) | {seq_len - 1})
+    res = _oracle_rows(w, inp, rows)
+    sel = [t - q0 for t in rows]
+    stats = P.check_index_rows(w, rows, out["idx"][sel], out["count"][sel], None, res)
+    P.check_runs(out["runs"][sel], out["run_count"][sel], out["idx"][sel], out["count"][sel], w.run_align)
+    print(w.name, slots, stats)
 
 
 def test_keep_all_equals_flat_on_gpu():
@@ -350,15 +412,24 @@ def test_empty_and_tiny():
 
 
 # ----------------------------------------------------------------------------- decode (paged)
-def _decode_case(w):
+def _decode_case(w, signed_weights=False):
     ctx, table, n_phys = synth.decode_layout(w.seed, w.batch, w.ctx_lo, w.ctx_hi, w.kv_page)
-    inp = synth.indexer_inputs(w.seed, w.batch, n_phys * w.kv_page, w.n_heads, w.head_dim, w.fp8)
+    inp = synth.indexer_inputs(w.seed, w.batch, n_phys * w.kv_page, w.n_heads, w.head_dim, w.fp8, signed_weights)
     return ctx, table, n_phys, inp
 
 
-@pytest.mark.parametrize("w", [W.SMALL_DECODE, W.SMALL_DECODE_MINMAX], ids=lambda w: w.name)
-def test_index_decode_parity(w):
-    ctx, table, n_phys, inp = _decode_case(w)
+_DECODE_D64 = replace(W.SMALL_DECODE, name="small_decode_b8_d64_fp8", head_dim=64)
+_DECODE_D64_MINMAX = replace(W.SMALL_DECODE_MINMAX, name="small_decode_b8_d64_bf16_minmax", head_dim=64, fp8=False)
+
+
+@pytest.mark.parametrize("w,signed", [(W.SMALL_DECODE, False), (W.SMALL_DECODE_MINMAX, False), (_DECODE_D64, False),
+                                      (_DECODE_D64_MINMAX, False), (W.SMALL_DECODE, True)],
+                         ids=["mean", "minmax", "d64_fp8", "d64_bf16_minmax", "signed_w"])
+def test_index_decode_parity(w, signed):
+    """Paged decode indexer against the oracle on every sequence. The d_I = 64 cases run the paged
+    coarse instances coarse_kernel<64, 1, true, false / true> and fine_kernel<64, fp8 / bf16>;
+    signed_w draws head weights of either sign (two of the eight sequences with all weights <= 0)."""
+    ctx, table, n_phys, inp = _decode_case(w, signed)
     prm = w.index_params()
     q, wt, k, ks = P.gpu_index_inputs(inp, w)
     bk = lsa.block_keys(prm, k, ks)
@@ -373,7 +444,7 @@ def test_index_decode_parity(w):
         t = int(ctx[b]) - 1
         k_log = orc.logical_rows(k_hat_pool, table[b], t + 1, w.kv_page)
         k_mean = P.oracle_block_cache(w, k_log)
-        res.append(orc.index_row(t, qf[b], inp["w"][b], k_log, k_mean, prmo))
+        res.append(P.oracle_index_row(t, qf[b], inp["w"][b], k_log, k_mean, prmo))
         rows_t.append(t)
     P.check_index_rows(w, rows_t, out["idx"], out["count"], out["pages"], res)
     P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
@@ -429,7 +500,7 @@ def test_decode_short_contexts(w):
     for b in range(B):
         t = int(ctx[b]) - 1
         k_log = orc.logical_rows(k_hat_pool, table[b], t + 1, P_)
-        res.append(orc.index_row(t, qf[b], inp["w"][b], k_log, P.oracle_block_cache(w, k_log), prmo))
+        res.append(P.oracle_index_row(t, qf[b], inp["w"][b], k_log, P.oracle_block_cache(w, k_log), prmo))
         rows_t.append(t)
     P.check_index_rows(w, rows_t, out["idx"], out["count"], out["pages"], res)
     P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
