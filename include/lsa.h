@@ -182,6 +182,27 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
                             int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out,
                             void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * lsa_index_decode without a workspace, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid allocation). The indexer's
+ * scratch (page-score keys, recalled pages and fine-score keys of a pass of rows) lives in a fixed
+ * device array of LSA_STATIC_SCRATCH_BYTES inside the library, one per device, held until the
+ * process ends; rows are processed in as many passes as that array requires. The call allocates
+ * and frees nothing. Arguments and outputs as lsa_index_decode without workspace / ws_bytes;
+ * the outputs are bit-identical to lsa_index_decode's.
+ * Returns LSA_ERR_WORKSPACE (before any HIP call) when one query row needs more than the array
+ * holds: 4 * (M * P + number of pages + M) bytes + 768 in hierarchical mode, 4 * (pages * P) + 768
+ * flat, with pages = ceil(max_pages * kv_page_size / P).
+ * Every call on one device shares that device's array: calls that overlap in time on one device
+ * (several host threads, or several streams) race and must be serialised by the caller.
+ */
+#define LSA_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+lsa_status lsa_index_decode_static(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
+                                   const int32_t* page_table, int32_t max_pages, int32_t kv_page_size,
+                                   int64_t n_phys, const void* q, const float* w, const void* k,
+                                   const float* k_scale, const void* block_keys, int32_t* idx, int32_t* count,
+                                   lsa_run* runs, int32_t* run_count, int32_t* pages_out, void* stream);
+
 /* Sparse attention shapes. Supported: MQA {n_heads 16, d_qk 128, d_v 128, latent 0} and
  * MLA absorbed {n_heads 64, d_qk 576, d_v 512, latent 1}. */
 typedef struct lsa_attn_params {

@@ -86,14 +86,31 @@ struct IndexPlan {
   size_t off_page_keys, off_pages, off_fine, total;
 };
 
-IndexPlan plan_index(const lsa_index_params* p, int64_t n_rows, int64_t max_kv) {
+// Workspace bytes one query row needs (page-score keys, recalled pages, fine-score keys).
+size_t index_row_bytes(const lsa_index_params* p, int64_t max_kv) {
+  const int64_t n_pages = cdiv(max_kv, p->page);
+  const bool hi = p->keep_pages > 0;
+  const int64_t slots = (hi ? (int64_t)p->keep_pages : n_pages) * p->page;
+  return (size_t)slots * 4 + (hi ? (size_t)(n_pages + p->keep_pages) * 4 : 0);
+}
+
+// budget == 0: passes of about kPassBytes in multiples of 8 rows (the caller's workspace is sized
+// from this plan); otherwise the plan fits within `budget` bytes (a fixed scratch array), in as
+// many rows per pass as fit, at least one (the caller checks that one row fits).
+IndexPlan plan_index(const lsa_index_params* p, int64_t n_rows, int64_t max_kv, size_t budget = 0) {
   IndexPlan pl{};
   pl.n_pages = cdiv(max_kv, p->page);
   const bool hi = p->keep_pages > 0;
   pl.slots = (hi ? (int64_t)p->keep_pages : pl.n_pages) * p->page;
-  const size_t per_row = (size_t)pl.slots * 4 + (hi ? (size_t)(pl.n_pages + p->keep_pages) * 4 : 0);
-  int64_t rpp = (int64_t)(kPassBytes / (per_row > 0 ? per_row : 1));
-  rpp = rpp < 8 ? 8 : rpp / 8 * 8;
+  const size_t per_row = index_row_bytes(p, max_kv);
+  int64_t rpp;
+  if (budget == 0) {
+    rpp = (int64_t)(kPassBytes / (per_row > 0 ? per_row : 1));
+    rpp = rpp < 8 ? 8 : rpp / 8 * 8;
+  } else {  // three areas, each rounded up to 256 bytes
+    rpp = budget > 768 ? (int64_t)((budget - 768) / (per_row > 0 ? per_row : 1)) : 0;
+    rpp = rpp < 1 ? 1 : rpp;
+  }
   pl.rows_per_pass = n_rows < rpp ? n_rows : rpp;
   const size_t r = (size_t)pl.rows_per_pass;
   size_t off = 0;
@@ -139,8 +156,8 @@ lsa::IndexGeom make_geom(const lsa_index_params* p) {
 lsa_status run_index(const lsa_index_params* p, const lsa::IndexGeom& g, int64_t n_rows, int64_t max_kv,
                      const void* q, const float* w, const void* k, const float* k_scale, const void* block_keys,
                      int32_t* idx, int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out,
-                     void* workspace, hipStream_t st) {
-  const IndexPlan pl = plan_index(p, n_rows, max_kv);
+                     void* workspace, hipStream_t st, size_t budget = 0) {
+  const IndexPlan pl = plan_index(p, n_rows, max_kv, budget);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint32_t* page_keys = reinterpret_cast<uint32_t*>(ws + pl.off_page_keys);
   uint32_t* fine = reinterpret_cast<uint32_t*>(ws + pl.off_fine);
@@ -357,12 +374,14 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
                    e.keep_pages > 0 ? pages_out : nullptr, workspace, static_cast<hipStream_t>(stream));
 }
 
-lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
-                            const int32_t* page_table, int32_t max_pages, int32_t kv_page_size, int64_t n_phys,
-                            const void* q, const float* w, const void* k, const float* k_scale, const void* block_keys,
-                            int32_t* idx, int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out,
-                            void* workspace, size_t ws_bytes, void* stream) {
-  g_err[0] = 0;
+// Checks and geometry shared by the two decode entry points. `budget` = 0: the caller's workspace
+// (ws_bytes must cover the plan); otherwise the fixed scratch array of that many bytes.
+static lsa_status decode_setup(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
+                               const int32_t* page_table, int32_t max_pages, int32_t kv_page_size, int64_t n_phys,
+                               const void* q, const float* w, const void* k, const float* k_scale,
+                               const void* block_keys, int32_t* idx, int32_t* count, lsa_run* runs,
+                               int32_t* run_count, int32_t* pages_out, void* workspace, size_t ws_bytes, size_t budget,
+                               lsa_index_params* e_out, lsa::IndexGeom* g_out) {
   lsa_status s = check_index_params(p);
   if (s != LSA_OK) return s;
   LSA_REQUIRE(batch >= 0, LSA_ERR_INVALID_ARG, "batch=%d < 0", batch);
@@ -378,14 +397,20 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
   LSA_REQUIRE(pages_out == nullptr || p->keep_pages > 0, LSA_ERR_INVALID_ARG, "pages_out needs keep_pages > 0");
   const int64_t max_kv = (int64_t)max_pages * kv_page_size;
   const lsa_index_params e = effective_params(p, max_kv);
-  const IndexPlan pl = plan_index(&e, batch, max_kv);
+  const IndexPlan pl = plan_index(&e, batch, max_kv, budget);
   s = check_lds(&e, pl);
   if (s != LSA_OK) return s;
+  if (budget != 0) {
+    const size_t row = index_row_bytes(&e, max_kv);
+    LSA_REQUIRE(row + 768 <= budget, LSA_ERR_WORKSPACE,
+                "one query row of this call needs %zu bytes of indexer workspace; the fixed scratch array holds "
+                "%zu (lower max_pages or keep_pages, or use lsa_index_decode with a workspace)",
+                row + 768, budget);
+  }
   if (batch == 0) return LSA_OK;  // nothing to read or write
+  // (with the fixed scratch array there is no caller workspace to check)
   s = check_index_io(&e, q, w, k, k_scale, block_keys, n_phys * kv_page_size / p->sub_block, idx, count, runs,
-                     run_count, workspace, ws_bytes, pl.total);
-  if (s != LSA_OK) return s;
-  s = clear_pages_if_flat(p, &e, pages_out, batch, static_cast<hipStream_t>(stream));
+                     run_count, workspace, ws_bytes, budget != 0 ? 0 : pl.total);
   if (s != LSA_OK) return s;
   lsa::IndexGeom g = make_geom(&e);
   g.ctx_len = ctx_len;
@@ -395,8 +420,85 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
   g.n_phys = n_phys;
   g.n_kv = n_phys * kv_page_size;
   g.n_sub = g.n_kv / p->sub_block;
-  return run_index(&e, g, batch, max_kv, q, w, k, k_scale, block_keys, idx, count, runs, run_count,
-                   e.keep_pages > 0 ? pages_out : nullptr, workspace, static_cast<hipStream_t>(stream));
+  *e_out = e;
+  *g_out = g;
+  return LSA_OK;
+}
+
+lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
+                            const int32_t* page_table, int32_t max_pages, int32_t kv_page_size, int64_t n_phys,
+                            const void* q, const float* w, const void* k, const float* k_scale, const void* block_keys,
+                            int32_t* idx, int32_t* count, lsa_run* runs, int32_t* run_count, int32_t* pages_out,
+                            void* workspace, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  lsa_index_params e{};
+  lsa::IndexGeom g{};
+  lsa_status s = decode_setup(p, batch, ctx_len, page_table, max_pages, kv_page_size, n_phys, q, w, k, k_scale,
+                              block_keys, idx, count, runs, run_count, pages_out, workspace, ws_bytes, 0, &e, &g);
+  if (s != LSA_OK || batch == 0) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = clear_pages_if_flat(p, &e, pages_out, batch, st);
+  if (s != LSA_OK) return s;
+  return run_index(&e, g, batch, (int64_t)max_pages * kv_page_size, q, w, k, k_scale, block_keys, idx, count, runs,
+                   run_count, e.keep_pages > 0 ? pages_out : nullptr, workspace, st);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- decode indexer without allocation
+// Scratch of lsa_index_decode_static: the indexer workspace (page-score keys, recalled pages,
+// fine-score keys) of one row pass lives in this fixed device array instead of a caller-owned
+// workspace. Each device holds its own copy until the process ends. Host code must not use the
+// array's name as an address: its device address is looked up once per device (first call there)
+// and only that pointer is passed to kernels. Nothing in it needs to start at zero (every entry a
+// kernel reads is written earlier in the same call), and it keeps the last call's contents.
+static __device__ __align__(256) uint8_t scratch[LSA_STATIC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {};
+
+// Device address of `scratch` on the current device (looked up on the first call there).
+hipError_t static_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (ptr == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+extern "C" {
+
+lsa_status lsa_index_decode_static(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
+                                   const int32_t* page_table, int32_t max_pages, int32_t kv_page_size,
+                                   int64_t n_phys, const void* q, const float* w, const void* k,
+                                   const float* k_scale, const void* block_keys, int32_t* idx, int32_t* count,
+                                   lsa_run* runs, int32_t* run_count, int32_t* pages_out, void* stream) {
+  g_err[0] = 0;
+  lsa_index_params e{};
+  lsa::IndexGeom g{};
+  lsa_status s = decode_setup(p, batch, ctx_len, page_table, max_pages, kv_page_size, n_phys, q, w, k, k_scale,
+                              block_keys, idx, count, runs, run_count, pages_out, nullptr, 0,
+                              LSA_STATIC_SCRATCH_BYTES, &e, &g);
+  if (s != LSA_OK || batch == 0) return s;
+  void* ws = nullptr;
+  hipError_t err = static_scratch(&ws);
+  if (err != hipSuccess) return hip_fail(err, "static scratch address");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = clear_pages_if_flat(p, &e, pages_out, batch, st);
+  if (s != LSA_OK) return s;
+  return run_index(&e, g, batch, (int64_t)max_pages * kv_page_size, q, w, k, k_scale, block_keys, idx, count, runs,
+                   run_count, e.keep_pages > 0 ? pages_out : nullptr, ws, st, LSA_STATIC_SCRATCH_BYTES);
 }
 
 size_t lsa_sparse_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int32_t paged) {

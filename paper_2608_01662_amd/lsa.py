@@ -112,6 +112,9 @@ def lib() -> ctypes.CDLL:
         L.lsa_index_decode.argtypes = [P, _i32, _vp, _vp, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _vp, _vp, _vp, _vp, _sz, _vp]
         L.lsa_index_decode.restype = _i32
+        L.lsa_index_decode_static.argtypes = [P, _i32, _vp, _vp, _i32, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                              _vp, _vp, _vp, _vp, _vp]
+        L.lsa_index_decode_static.restype = _i32
         L.lsa_sparse_attn_workspace_size.argtypes = [A, _i64, _i32, _i32]
         L.lsa_sparse_attn_workspace_size.restype = _sz
         L.lsa_sparse_attn.argtypes = [A, _i64, _vp, _vp, _vp, _i64, _vp, _vp, _i32, _vp, _i32, _i32, _i32, _vp,
@@ -321,6 +324,39 @@ def index_decode(prm: IndexParams, ctx_len: torch.Tensor, page_table: torch.Tens
                                   _p(o["idx"]), _p(o["count"]), _p(o.get("runs")), _p(o.get("run_count")),
                                   _p(o.get("pages")), _p(ws), wsb, _stream(q.device)),
            "lsa_index_decode")
+    return o
+
+
+def index_decode_static(prm: IndexParams, ctx_len: torch.Tensor, page_table: torch.Tensor, kv_page_size: int,
+                        n_phys: int, q: torch.Tensor, w: torch.Tensor, k: torch.Tensor, k_scale: torch.Tensor | None,
+                        block_keys: torch.Tensor | None, out: dict) -> dict:
+    """lsa_index_decode_static: the decode indexer with its scratch in the library's fixed device
+    array (no workspace). `out` holds preallocated outputs (idx, count, and optionally runs +
+    run_count and pages), so that this call allocates nothing either."""
+    k = _keys_u8_or_bf16(k)
+    _need("page_table", page_table, _I32, (None, None))
+    batch, max_pages = page_table.shape
+    dev = page_table.device
+    _need("ctx_len", ctx_len, _I32, (batch,), dev)
+    _need("q", q, _BF16, (batch, prm.n_heads, prm.head_dim), dev)
+    _need("w", w, _F32, (batch, prm.n_heads), dev)
+    n_cached = n_phys * kv_page_size
+    _need("k", k, _key_dtypes(prm), None, dev)
+    if k.shape[-1] != prm.head_dim or k.numel() < n_cached * prm.head_dim:
+        raise ValueError(f"k must hold n_phys * kv_page_size = {n_cached} key rows of {prm.head_dim}")
+    if prm.fp8:
+        _need("k_scale", k_scale, _F32, None, dev)
+        if k_scale.numel() < n_cached:
+            raise ValueError(f"k_scale must hold {n_cached} scales")
+    _need_opt("block_keys", block_keys, _BF16, (None, prm.block_width), dev, min_rows=n_cached // prm.sub_block)
+    if out is None or "idx" not in out or "count" not in out:
+        raise ValueError("index_decode_static needs preallocated outputs (out['idx'], out['count'])")
+    o = _index_outputs(prm, batch, q.device, "runs" in out, "pages" in out, out)
+    _check(lib().lsa_index_decode_static(ctypes.byref(prm.c()), batch, _p(ctx_len), _p(page_table), max_pages,
+                                         kv_page_size, n_phys, _p(q), _p(w), _p(k), _p(k_scale), _p(block_keys),
+                                         _p(o["idx"]), _p(o["count"]), _p(o.get("runs")), _p(o.get("run_count")),
+                                         _p(o.get("pages")), _stream(q.device)),
+           "lsa_index_decode_static")
     return o
 
 

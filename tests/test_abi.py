@@ -146,6 +146,25 @@ def test_bad_decode_arguments():
     assert dec(wsb=0) == WORKSPACE
 
 
+def test_static_decode_arguments():
+    """lsa_index_decode_static (scratch in the library's fixed array) validates like
+    lsa_index_decode and rejects, before any HIP call, a call whose single row needs more
+    scratch than the array holds (flat mode over 2^20 pages of 64 tokens: 256 MB per row)."""
+    L = lsa.lib()
+    hi = P(page=64, sub_block=64, keep_pages=128, k_swa=256)
+
+    def dec(prm=hi, batch=4, ctx=FAKE, table=FAKE, max_pages=2048, kv_page=64, n_phys=1000):
+        return L.lsa_index_decode_static(ctypes.byref(prm.c()), batch, ctx, table, max_pages, kv_page, n_phys, FAKE,
+                                         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None)
+    assert dec(kv_page=32) == UNSUPPORTED
+    assert dec(ctx=None) == INVALID
+    assert dec(max_pages=0) == INVALID
+    assert dec(batch=-1) == INVALID
+    assert dec(prm=P(page=64, sub_block=64, keep_pages=0, k_swa=256), max_pages=1 << 20) == WORKSPACE
+    assert b"scratch" in L.lsa_last_error()
+    assert dec(batch=0) == OK                                                  # nothing to do, nothing touched
+
+
 def test_bad_attention_arguments():
     L = lsa.lib()
     mla = lsa.AttnParams(sm_scale=0.07, **lsa.MLA)
