@@ -111,25 +111,41 @@ __device__ __forceinline__ int64_t block_prefix512(int64_t v, int64_t* wtot, int
   return base + inc - v;
 }
 
-template <bool SPLIT, int NBUF>
+// WIN: the window branch of the split attention as a query-tiled kernel (Sec. 4.1.1): a workgroup
+// takes two consecutive query rows t0, t0 + 1 and heads 32 blockIdx.y .. + 31, and walks the
+// contiguous cache rows of the union of their windows, [t0 - k_swa + 1, t0 + 1], once: every tile
+// is loaded once into LDS for both rows. Wave w works on row t0 + (w >> 2) with the per-wave code
+// of the list kernel (16 heads, half of the dims, half of the value columns); each row masks the
+// tokens outside its own window. Writes the fp32 partial of split a.part.
+// (Two rows of 64 heads would hold 2 x (73.7 KB of Q operand + 131 KB of fp32 accumulators), 80%
+// of a CU's 512 KB register file, before any operand; tiling 2 rows x 32 heads keeps the 64 query
+// vectors per tile of the list kernel.)
+template <bool SPLIT, int NBUF, bool WIN = false>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void mla_attn_kernel(AttnGeom a) {
   static_assert(NBUF >= 2 && NBUF <= 3, "two or three tile buffers");
+  static_assert(!WIN || SPLIT, "the window kernel writes partials");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[NBUF * kMlaTile + kMlaXch];
-  __shared__ int32_t ids[kMlaIdCap];
+  __shared__ int32_t ids[WIN ? 1 : kMlaIdCap];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int i16 = lane & 15, g = lane >> 4;
-  const int hq = wv >> 1, kw = wv & 1;
+  const int hq = WIN ? 2 * (int)blockIdx.y + ((wv >> 1) & 1) : wv >> 1, kw = wv & 1;
   const int head = 16 * hq + i16;
   const bool loader = wv < kMlaLoaders;
-  const int64_t row = xcd_band(blockIdx.x, a.n_rows);
+  // WIN: item = row pair; the second row of a pair past n_rows (odd count) computes nothing it writes
+  const int64_t item = xcd_band(blockIdx.x, WIN ? (a.n_rows + 1) / 2 : a.n_rows);
+  const int64_t wrow = WIN ? 2 * item + (wv >> 2) : item;
+  const bool row_ok = wrow < a.n_rows;
+  const int64_t row = row_ok ? wrow : a.n_rows - 1;
   const int split = SPLIT ? (a.part >= 0 ? a.part : (int)blockIdx.y) : 0;
   __shared__ int64_t rtot[8];
   __shared__ int32_t roff[512];   // run form: list position of each thread's first run (clamped)
   __shared__ int4 rq[kRunQueue];  // run form: (start, offset into the run, ids slot, entries)
   __shared__ int rq_n;
   int cnt;
-  if (a.runs) {  // the list length is the sum of the run lengths (at most k_cap entries are used)
+  if (WIN) {
+    cnt = 0;  // (unused: the window is generated)
+  } else if (a.runs) {  // the list length is the sum of the run lengths (at most k_cap entries are used)
     const RunBlock rb = run_block(a, row);
     int64_t mine = 0;
     for (int r0 = rb.b; r0 < rb.e; r0 += 4) {
@@ -149,7 +165,22 @@ void mla_attn_kernel(AttnGeom a) {
   int s0 = SPLIT && a.part < 0 ? split * a.split_len : 0;
   int s1 = SPLIT && a.part < 0 ? (cnt < s0 + a.split_len ? cnt : s0 + a.split_len) : cnt;
   int64_t win0 = -1;  // first cache row of the window part (contiguous rows, no list)
-  if (a.part >= 0) {
+  // WIN: this wave's row window [w_lo, w_hi] (empty for a skipped row) and the pair's union
+  int64_t w_lo = 0, w_hi = -1, u_last = -1;
+  if (WIN) {
+    const int64_t t0 = a.q_pos0 + 2 * item;
+    const int64_t t1 = a.q_pos0 + (2 * item + 1 < a.n_rows ? 2 * item + 1 : 2 * item);
+    const int64_t t = a.q_pos0 + row;
+    int c = a.count[row];
+    if (row_ok && c > 0) {  // an empty list (a skipped row) has no window either
+      w_hi = t;
+      w_lo = t - a.k_swa + 1 > 0 ? t - a.k_swa + 1 : 0;
+    }
+    win0 = t0 - a.k_swa + 1 > 0 ? t0 - a.k_swa + 1 : 0;
+    u_last = t1 < a.n_kv_rows - 1 ? t1 : a.n_kv_rows - 1;
+    s0 = 0;
+    s1 = (int)(t1 - win0 + 1);
+  } else if (a.part >= 0) {
     const int64_t t = a.q_pos0 + row;
     const int nwin = (int)(a.k_swa < t + 1 ? a.k_swa : t + 1);
     if (a.part == 0) {
@@ -200,20 +231,29 @@ void mla_attn_kernel(AttnGeom a) {
   const int dma_tok = 8 * wv + dj;
   const int64_t dma_col = ((lane & 7) ^ mla_swz(wv, dj)) * 16;
   auto issue = [&](int tile, int buf) {
-    const int r = ids[tile * kMlaT + dma_tok];
+    int r;
+    if (WIN) {  // contiguous rows; positions past the union re-read its last row (masked)
+      const int64_t p = win0 + (int64_t)tile * kMlaT + dma_tok;
+      r = (int)(p < u_last ? p : u_last);
+    } else {
+      r = ids[tile * kMlaT + dma_tok];
+    }
     const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
     const uint8_t* const srcs[kMlaLoads] = {src,       src + 128, src + 256, src + 384,  src + 512,
                                             src + 640, src + 768, src + 896, src + 1024};
     lds_dma16x9(srcs, lds_addr(lds + buf * kMlaTile + wv * (kMlaLoads * 1024)));
   };
 
-  for (int c0 = 0; c0 < n; c0 += kMlaIdCap) {
-    const int nc = n - c0 < kMlaIdCap ? n - c0 : kMlaIdCap;
+  constexpr int kPass = WIN ? (1 << 30) : kMlaIdCap;  // the window needs no staged list
+  for (int c0 = 0; c0 < n; c0 += kPass) {
+    const int nc = n - c0 < kPass ? n - c0 : kPass;
     const int ntiles = (nc + kMlaT - 1) / kMlaT;
     // list entries -> LDS, validated (-1 = skip; the last tile is padded with -1)
-    if (a.runs && threadIdx.x == 0) rq_n = 0;  // the previous pass's readers passed a barrier since
-    __syncthreads();  // the previous chunk's readers of `ids` are done
-    if (a.runs) {
+    if (!WIN && a.runs && threadIdx.x == 0) rq_n = 0;  // the previous pass's readers passed a barrier since
+    if (!WIN) __syncthreads();  // the previous chunk's readers of `ids` are done
+    if (WIN) {
+      // nothing to stage: tile rows are win0 + 32 it + 0..31
+    } else if (a.runs) {
       // list entries [s0 + c0, s0 + c0 + nc) from the runs (runs partition the list, so every entry
       // is written once): each thread writes the entries of its own short runs that fall in this
       // chunk and queues the longer ones, which the whole block then writes, 512 entries at a time
@@ -317,7 +357,13 @@ void mla_attn_kernel(AttnGeom a) {
         sacc[1] += other[64];
       }
       // ---- online softmax (base 2); lane holds tokens 16mt + 4g + r of head `head`
-      const uint32_t vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
+      uint32_t vmask;
+      if (WIN) {
+        const int64_t p = win0 + (int64_t)it * kMlaT + lj;
+        vmask = (uint32_t)__ballot(p >= w_lo && p <= w_hi);
+      } else {
+        vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
+      }
       if (vmask != 0xFFFFFFFFu) {  // partial or skipped tokens: mask them
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
@@ -381,7 +427,7 @@ void mla_attn_kernel(AttnGeom a) {
       *reinterpret_cast<u32x2*>(orow + 16 * c) = v;
     }
     if (a.lse && g == 0 && kw == 0) a.lse[row * 64 + head] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
-  } else {
+  } else if (row_ok) {
     const int64_t pi = (row * a.n_split + split) * 64 + head;
     float* po = a.part_o + pi * 512 + dv0;
 #pragma unroll
@@ -581,6 +627,13 @@ hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st) {
 hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st) {
   if (a.n_rows == 0) return hipSuccess;
   launch_mla_kernel<true>(dim3((unsigned)a.n_rows), a, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_mla_attn_window(const AttnGeom& a, hipStream_t st) {
+  if (a.n_rows == 0) return hipSuccess;
+  hipLaunchKernelGGL((mla_attn_kernel<true, kMlaBufs, true>), dim3((unsigned)((a.n_rows + 1) / 2), 2u), dim3(512), 0,
+                     st, a);
   return hipGetLastError();
 }
 

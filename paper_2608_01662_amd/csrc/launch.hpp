@@ -80,6 +80,9 @@ hipError_t launch_mqa_attn(const AttnGeom& a, hipStream_t st);
 hipError_t launch_attn_combine(const AttnGeom& a, int H, int d_v, hipStream_t st);
 // One part (a.part = 0 or 1) of the split attention into the partials a.part_o / a.part_ml.
 hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st);
+// The window part (a.part = 1) as the query-tiled kernel: two consecutive rows per workgroup
+// share each contiguous window tile.
+hipError_t launch_mla_attn_window(const AttnGeom& a, hipStream_t st);
 hipError_t launch_translate_rows(const int32_t* idx, const int32_t* count, int64_t n_rows, int k_cap,
                                  const int32_t* page_table, int max_pages, int kv_page, int rows_per_seq,
                                  int64_t n_kv_rows, int32_t* out_rows, hipStream_t st);

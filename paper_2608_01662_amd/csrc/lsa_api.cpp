@@ -762,7 +762,7 @@ lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q,
     a.part = 0;
     if ((e = lsa::launch_mla_attn_part(a, st)) != hipSuccess) return hip_fail(e, "split attention (listed part)");
     a.part = 1;
-    if ((e = lsa::launch_mla_attn_part(a, hs->side)) != hipSuccess) return hip_fail(e, "split attention (window)");
+    if ((e = lsa::launch_mla_attn_window(a, hs->side)) != hipSuccess) return hip_fail(e, "split attention (window)");
     if ((e = hipEventRecord(hs->join, hs->side)) != hipSuccess) return hip_fail(e, "split attention join");
     if ((e = hipStreamWaitEvent(st, hs->join, 0)) != hipSuccess) return hip_fail(e, "split attention join");
     if ((e = lsa::launch_attn_combine(a, 64, 512, st)) != hipSuccess) return hip_fail(e, "split attention merge");

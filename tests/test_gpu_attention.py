@@ -397,17 +397,24 @@ def test_attention_determinism():
     assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
 
 
-@pytest.mark.parametrize("w", [W.SMALL_MLA, W.SMALL_CLI], ids=lambda w: w.name)
-def test_split_attention_parity(w):
+@pytest.mark.parametrize("w,q0,n_q", [(W.SMALL_MLA, 0, 1536), (W.SMALL_CLI, 0, 1536), (W.SMALL_CLI, 777, 999)],
+                         ids=["small_mla", "small_cli", "small_cli_odd_chunk"])
+def test_split_attention_parity(w, q0, n_q):
     """Split attention (listed non-window part and contiguous window on two streams, merged by
-    log-sum-exp): every row of a chunk against the oracle's Eq. (3) over the whole list, and
-    against the fused kernel. The lists come from the oracle's indexer (the window part is read
-    from the cache, not from the list, so the lists must hold the whole window: they do), over a
-    chunk whose first rows are shorter than the window."""
+    log-sum-exp; the window part runs in the query-tiled kernel, two consecutive rows per
+    workgroup sharing each window tile): every seventh row of a chunk against the oracle's Eq. (3)
+    over the whole list, and every row against the fused kernel. The lists come from the oracle's
+    indexer (the window part is read from the cache, not from the list, so the lists must hold the
+    whole window: they do). Chunks: from position 0 (first rows shorter than the window), and an
+    odd count of rows from an odd position (the last row pair holds one row); one row's list is
+    emptied (count 0: no window either, o = 0 and lse = -inf as in the fused kernel)."""
     n = w.seq_len
-    q0, n_q = 0, min(n, 1536)
+    n_q = min(n - q0, n_q)
     rows = list(range(q0, q0 + n_q))
     idx, cnt = _oracle_index(w, rows, n)
+    skipped = n_q // 2
+    cnt = cnt.copy()
+    cnt[skipped] = 0
     a = _attn_inputs(w, 0, n, n)
     q = P.bf16_dev(a["q"][rows])
     kv = P.bf16_dev(a["kv"])
@@ -415,13 +422,15 @@ def test_split_attention_parity(w):
     of, lf = lsa.sparse_attn(w.attn_params(), q, kv, None, P.to_dev(idx), P.to_dev(cnt))
     torch.cuda.synchronize()
     o, l, of, lf = o.float().cpu().numpy(), l.cpu().numpy(), of.float().cpu().numpy(), lf.cpu().numpy()
-    sel = list(range(0, n_q, 7)) + [n_q - 1]
+    assert np.all(o[skipped] == 0) and np.all(np.isneginf(l[skipped])), "an empty list attends to nothing"
+    assert np.all(of[skipped] == 0) and np.all(np.isneginf(lf[skipped]))
+    sel = [i for i in list(range(0, n_q, 7)) + [n_q - 2, n_q - 1] if i != skipped]
     worst = _check_rows(w, a, [rows[i] for i in sel], idx[sel], cnt[sel], o[sel], l[sel])
     # against the fused kernel: two bf16 roundings of the same value apart at most
-    assert np.max(np.abs(o - of)) <= 2e-2, np.max(np.abs(o - of))
-    assert np.max(np.abs(l - lf)) <= 2e-3, np.max(np.abs(l - lf))
-    print(w.name, "worst vs oracle", worst, "max |hfa - fused|", float(np.max(np.abs(o - of))))
-
+    keep = np.arange(n_q) != skipped
+    assert np.max(np.abs(o[keep] - of[keep])) <= 2e-2, np.max(np.abs(o[keep] - of[keep]))
+    assert np.max(np.abs(l[keep] - lf[keep])) <= 2e-3, np.max(np.abs(l[keep] - lf[keep]))
+    print(w.name, q0, n_q, "worst vs oracle", worst, "max |hfa - fused|", float(np.max(np.abs(o[keep] - of[keep]))))
 
 
 def test_binding_rejects_mismatched_tensors():
