@@ -87,6 +87,26 @@ def copy_probe(nbytes: int):
     print(json.dumps({"copy_probe_bytes": nbytes, "copies": 3}), flush=True)
 
 
+def gather_probe(n_rows: int, table_rows: int):
+    """Random-row gather of known size, shaped like the attention's KV reads, run under rocprofv3
+    --pmc to check the FETCH_SIZE calibration on scattered 1152-byte rows: n_rows rows of 576 bf16
+    (1152 bytes) drawn at random from a table of table_rows rows (torch.index_select: every
+    gathered row is read once and written once)."""
+    dev = torch.device("cuda:0")
+    table = torch.ones((table_rows, 576), dtype=torch.bfloat16, device=dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    idx = torch.randint(0, table_rows, (n_rows,), generator=g, device=dev)
+    out = torch.empty((n_rows, 576), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.index_select(table, 0, idx, out=out)
+    torch.cuda.synchronize()
+    print(json.dumps({"gather_probe_rows": n_rows, "row_bytes": 1152, "table_rows": table_rows,
+                      "gathered_bytes": n_rows * 1152, "index_bytes": n_rows * 8,
+                      "table_bytes": table_rows * 1152, "gathers": 3}), flush=True)
+
+
 def index_sweep(lengths, pooling):
     """Indexer time of one whole prefill (every row) at each cache length, hierarchical (the
     benchmark workload's M and P) against flat (dense causal scoring of every eligible token): the
@@ -239,54 +259,113 @@ def make_inputs(w, dev, n_q):
     return t
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+_CPU = {}   # worker state: the oracle's inputs, memory-mapped from files the parent wrote
+
+
+def _cpu_worker_init(shm_dir, layers, prm_kw, dv, sm_scale):
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(1)                     # one BLAS thread per worker process
+    import oracle.lsa_oracle as orc
+    ld = lambda name: np.load(os.path.join(shm_dir, name + ".npy"), mmap_mode="r")
+    _CPU.update(orc=orc, k_hat=ld("k_hat"), k_mean=ld("k_mean"), q=ld("q"), w=ld("w"),
+                Q=[ld(f"Q{l}") for l in range(layers)], KV=[ld(f"KV{l}") for l in range(layers)],
+                V=[ld(f"V{l}") if os.path.exists(os.path.join(shm_dir, f"V{l}.npy")) else None for l in range(layers)],
+                prm=orc.IndexParams(**prm_kw), dv=dv, sm_scale=sm_scale)
+    if prm_kw["pooling"] == "minmax":
+        _CPU["k_mean"] = (ld("k_mean"), ld("k_min"))
+
+
+def _cpu_worker_rows(job):
+    """Oracle index row and every layer's attention for the sample rows job = [(i, t), ...]."""
+    c = _CPU
+    for i, t in job:
+        r = c["orc"].index_row(int(t), c["q"][i], c["w"][i], c["k_hat"], c["k_mean"], c["prm"])
+        for l in range(len(c["Q"])):
+            c["orc"].attention_for_set(c["Q"][l][i], c["KV"][l], c["V"][l], r["S"], c["dv"], c["sm_scale"])
+    return len(job)
+
+
 def cpu_baseline(w, t, seconds, q_start=0):
     """The float64 oracle on a bounded sample of query rows of the same workload (rows of the
-    step: positions q_start .. L-1)."""
+    step: positions q_start .. L-1), in a pool of one process per core this process may run on
+    (os.sched_getaffinity), each with one BLAS thread. The pool's processes are started fresh
+    (spawn: they never touch the GPU) and read the inputs memory-mapped from /dev/shm."""
+    import multiprocessing as mp
+    import shutil
+    import tempfile
     import oracle.lsa_oracle as orc
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        cores = 1
+    cores = len(os.sched_getaffinity(0))
     n = w.seq_len
     H, dqk, dv = w.attn_dims
     g = np.random.default_rng(1234)
     lo = max(w.k_cap, q_start)
-    rows = np.sort(g.choice(np.arange(lo, n), size=min(512, n - lo), replace=False))
+    rows = np.sort(g.choice(np.arange(lo, n), size=min(8192, n - lo), replace=False))
     kb = t["kI"].cpu().numpy() if w.fp8 else t["kI"].view(torch.int16).cpu().numpy().view(np.uint16)
     ks = t["ks"].cpu().numpy() if w.fp8 else None
     ridx = torch.from_numpy(rows - q_start).cuda()
-    qrows = t["qI"].index_select(0, ridx).float().cpu().numpy().astype(np.float64)
-    wrows = t["wI"].index_select(0, ridx).cpu().numpy()
-    Qrows = [q.index_select(0, ridx).view(torch.int16).cpu().numpy().view(np.uint16) for q in t["Q"]]
-    KVb = [kv.view(torch.int16).cpu().numpy().view(np.uint16) for kv in t["KV"]]
-    Vb = [None if v is None else v.view(torch.int16).cpu().numpy().view(np.uint16) for v in t["V"]]
-    prm = orc.IndexParams(page=w.page, sub_block=w.sub_block, keep_pages=w.keep_pages, k_sparse=w.k_sparse,
-                          k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align, pooling=w.pooling)
-    t0 = time.perf_counter()
-    k_hat = orc.dequantized_keys(kb, ks)
-    if w.pooling == "minmax":
-        k_mean = orc.sub_block_minmax_keys(k_hat, w.sub_block)
-    else:
-        k_mean = orc.sub_block_mean_keys(k_hat, w.sub_block)
-    t_once = time.perf_counter() - t0
-    done = 0
-    t1 = time.perf_counter()
-    for i, tpos in enumerate(rows):
-        r = orc.index_row(int(tpos), qrows[i], wrows[i], k_hat, k_mean, prm)
+    shm_dir = tempfile.mkdtemp(prefix="lsa_oracle_", dir="/dev/shm" if os.path.isdir("/dev/shm") else None)
+    try:
+        save = lambda name, arr: np.save(os.path.join(shm_dir, name + ".npy"), np.ascontiguousarray(arr))
+        save("q", t["qI"].index_select(0, ridx).float().cpu().numpy().astype(np.float64))
+        save("w", t["wI"].index_select(0, ridx).cpu().numpy())
         for l in range(w.layers):
-            orc.attention_for_set(Qrows[l][i], KVb[l], Vb[l], r["S"], dv, w.sm_scale)
-        done += 1
-        if time.perf_counter() - t1 > seconds:
-            break
-    per_row = (time.perf_counter() - t1) / done
+            save(f"Q{l}", t["Q"][l].index_select(0, ridx).view(torch.int16).cpu().numpy().view(np.uint16))
+            save(f"KV{l}", t["KV"][l].view(torch.int16).cpu().numpy().view(np.uint16))
+            if t["V"][l] is not None:
+                save(f"V{l}", t["V"][l].view(torch.int16).cpu().numpy().view(np.uint16))
+        # one-off work of the step, timed in this process: key decode and the block cache
+        t0 = time.perf_counter()
+        k_hat = orc.dequantized_keys(kb, ks)
+        if w.pooling == "minmax":
+            k_max, k_min = orc.sub_block_minmax_keys(k_hat, w.sub_block)
+        else:
+            k_max, k_min = orc.sub_block_mean_keys(k_hat, w.sub_block), None
+        t_once = time.perf_counter() - t0
+        save("k_hat", k_hat)
+        save("k_mean", k_max)
+        if k_min is not None:
+            save("k_min", k_min)
+        del k_hat, k_max, k_min
+        prm_kw = dict(page=w.page, sub_block=w.sub_block, keep_pages=w.keep_pages, k_sparse=w.k_sparse,
+                      k_sink=w.k_sink, k_swa=w.k_swa, run_align=w.run_align, pooling=w.pooling)
+        jobs = [[(i, int(rows[i])) for i in range(j, min(j + 4, len(rows)))] for j in range(0, len(rows), 4)]
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(cores, initializer=_cpu_worker_init,
+                      initargs=(shm_dir, w.layers, prm_kw, dv, w.sm_scale)) as pool:
+            pool.map(_cpu_worker_rows, [jobs[0]] * cores, chunksize=1)   # warm every worker (imports, page-in)
+            done = 0
+            t1 = time.perf_counter()
+            pending = [pool.apply_async(_cpu_worker_rows, (j,)) for j in jobs[:2 * cores]]
+            nxt = len(pending)
+            while pending:
+                done += pending.pop(0).get()
+                if time.perf_counter() - t1 < seconds and nxt < len(jobs):
+                    pending.append(pool.apply_async(_cpu_worker_rows, (jobs[nxt],)))
+                    nxt += 1
+            wall = time.perf_counter() - t1
+    finally:
+        shutil.rmtree(shm_dir, ignore_errors=True)
+    per_row = wall / done                    # pool wall time per row (all workers busy)
     n_q = n - q_start
     full = t_once + n_q * per_row
-    return {"value": n_q / full, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+    return {"value": n_q / full, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu": _cpu_model(),
             "sample": (f"{done} query rows at random positions in [{lo}, L) through the indexer and "
-                       f"{w.layers} attention layers, plus the one-off key decode and block cache "
-                       f"({t_once:.2f} s); tokens/s extrapolated to all {n_q} rows of the step "
-                       f"({per_row * 1e3:.1f} ms per row)")}
+                       f"{w.layers} attention layers in {cores} worker processes with one BLAS thread each "
+                       f"({wall:.1f} s wall), plus the one-off key decode and block cache ({t_once:.2f} s); "
+                       f"tokens/s extrapolated to all {n_q} rows of the step ({per_row * 1e3:.2f} ms of pool "
+                       f"wall time per row)")}
 
 
 def main():
@@ -312,6 +391,9 @@ def main():
                     help="only time the indexer, hierarchical against flat, at these cache lengths, and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration) and exit")
+    ap.add_argument("--gather-probe", default="", metavar="ROWS,TABLE_ROWS",
+                    help="only gather ROWS random 1152-byte rows from a table of TABLE_ROWS rows "
+                         "(counter calibration for scattered reads) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures the hot path on one GPU; running across several GPUs is not "
@@ -321,6 +403,10 @@ def main():
         sys.exit("--steps must be >= 1 and --warmup >= 0")
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.gather_probe:
+        n_rows, table_rows = (int(x) for x in args.gather_probe.split(","))
+        gather_probe(n_rows, table_rows)
         return
     if args.index_sweep:
         index_sweep([int(x) for x in args.index_sweep.split(",")], args.pooling)
@@ -469,6 +555,10 @@ def main():
     if tr is not None:   # HBM (data-fabric) bytes from the committed counter passes over this launch time
         res["breakdown"]["attn_fabric_gbs"] = tr / (attn_avg * 1e-3) / 1e9
         res["breakdown"]["attn_fabric_frac"] = res["breakdown"]["attn_fabric_gbs"] / HBM_PEAK_GBS
+    # beside the algorithmic fraction: the counter-measured HBM fraction (the L2 serves the window
+    # rows that neighbouring queries share) and the MFMA fraction of the same launch
+    res["roofline"]["traffic_frac"] = res["breakdown"].get("attn_fabric_frac")
+    res["roofline"]["mfma_frac"] = res["breakdown"]["attn_mfma_frac"]
     if not args.no_cpu_baseline:
         log(f"[bench] timing the oracle for ~{args.cpu_seconds:.0f} s on the host")
         res["cpu_baseline"] = cpu_baseline(w, t, args.cpu_seconds, q_start)
