@@ -486,18 +486,50 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
       }
     }
     uint32_t* dst = fine_keys + row * ldf + kk * g.P;
-    for (int tile = 0; tile < g.P / 32; ++tile) {
+    // key row of lane j in `tile` (row 0, not scored, outside E_t or the cache)
+    auto krow_of = [&](int tile, bool& ok) -> int64_t {
       const int64_t pos = page * g.P + tile * 32 + j;
-      const bool ok = kbase >= 0 && pos >= ri.lo && pos <= ri.hi;
-      const int64_t krow = ok ? kbase + tile * 32 + j : 0;
-      u32x4 b[KS];
-      load_key_operand<D, FP8>(k, krow, lane, b);
+      ok = kbase >= 0 && pos >= ri.lo && pos <= ri.hi;
+      return ok ? kbase + tile * 32 + j : 0;
+    };
+    constexpr int RAWN = FP8 ? D / 32 : D / 16;  // 16-byte loads per lane per tile
+    auto fetch = [&](int64_t kr, u32x4 (&r)[RAWN], float& scl) {
+      const u32x4* pp = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(k) + kr * (FP8 ? D : 2 * D) +
+                                                      (FP8 ? D / 2 : D) * (lane >> 5));
+#pragma unroll
+      for (int v = 0; v < RAWN; ++v) r[v] = pp[v];
+      scl = FP8 ? kscale[kr] : 1.f;
+    };
+    bool ok;
+    int64_t krow = krow_of(0, ok);
+    u32x4 raw[RAWN];
+    float sc;
+    fetch(krow, raw, sc);
+    for (int tile = 0; tile < g.P / 32; ++tile) {
+      bool nok = false;
+      u32x4 nraw[RAWN];
+      float nsc = 1.f;
+      if (tile + 1 < g.P / 32) fetch(krow_of(tile + 1, nok), nraw, nsc);  // in flight while this tile is scored
+      u32x4 bk[KS];
+#pragma unroll
+      for (int v = 0; v < RAWN; ++v) {
+        if (FP8) {
+          bk[2 * v] = fp8x8_to_bf16x8(raw[v].x, raw[v].y);
+          bk[2 * v + 1] = fp8x8_to_bf16x8(raw[v].z, raw[v].w);
+        } else {
+          bk[v] = raw[v];
+        }
+      }
       f32x16 acc = {};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) acc = mfma32(a[s], b[s], acc);
+      for (int s = 0; s < KS; ++s) acc = mfma32(a[s], bk[s], acc);
       float v = head_reduce(acc, wr);
-      if (FP8) v *= kscale[krow];
+      if (FP8) v *= sc;
       if (lane < 32) dst[tile * 32 + j] = ok ? score_key(v) : 0u;
+      ok = nok;
+      sc = nsc;
+#pragma unroll
+      for (int e = 0; e < RAWN; ++e) raw[e] = nraw[e];
     }
   }
 }
@@ -1342,7 +1374,10 @@ hipError_t launch_token_select(const IndexGeom& g, int64_t n_rows, const uint32_
   const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
   const size_t lds = token_select_lds_bytes(slots_cap, k_cap, g.M);
   const dim3 grid((unsigned)n_rows), block(512);
-  if (slots_cap <= 512 * 16)
+  if (slots_cap <= 1024 * 8 && n_rows <= kSelectFewRows)   // few rows (decode): more threads per row
+    hipLaunchKernelGGL((token_select_reg_kernel<1024, 8>), grid, dim3(1024), lds, st, g, n_rows, fine_keys, ldf, pages,
+                       idx, count, runs, run_count);
+  else if (slots_cap <= 512 * 16)
     hipLaunchKernelGGL((token_select_reg_kernel<512, 16>), grid, block, lds, st, g, n_rows, fine_keys, ldf, pages, idx,
                        count, runs, run_count);
   else if (slots_cap <= 512 * 32)
@@ -1466,7 +1501,7 @@ hipError_t prepare_index_kernels() {
   const int lim = (int)kSelectLdsLimit;
   const void* sel[] = {(const void*)token_select_kernel<512, false>, (const void*)token_select_kernel<1024, true>,
                        (const void*)token_select_reg_kernel<512, 16>, (const void*)token_select_reg_kernel<512, 32>,
-                       (const void*)token_select_reg_kernel<512, 64>};
+                       (const void*)token_select_reg_kernel<512, 64>, (const void*)token_select_reg_kernel<1024, 8>};
   for (const void* f : sel) {  // (the register-key kernels have 20 KB of static LDS, the others 4 KB)
     e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (f == sel[0] || f == sel[1]) ? lim : lim - 16 * 1024);
