@@ -148,7 +148,8 @@ lsa_status lsa_block_keys_update(const lsa_index_params* p, int64_t n_rows, cons
  *              largest score (ties to the smaller position), then the window; -1 after count[i]
  *   count      [n_q] int32: |S_t| = min(t+1, k_sink + k_swa + min(k_sparse, |candidates|))
  *   runs       [n_q, K_cap] lsa_run or NULL: idx re-encoded as maximal runs of consecutive
- *              positions, cut at multiples of run_align; unused entries are {-1, 0}; 8-byte aligned
+ *              positions, cut at multiples of run_align; entries past run_count[i] are not written
+ *              (they keep whatever the buffer held); 8-byte aligned
  *   run_count  [n_q] int32, required iff runs != NULL
  *   pages_out  [n_q, M] int32 or NULL (hierarchical mode only): the recalled pages P_t (Eq. 10)
  *              in ascending order, -1 padded

@@ -35,6 +35,18 @@ __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// v_mfma_scale_f32_32x32x64_f8f6f4 with both operands OCP e4m3 and unit block scales (E8M0 127):
+//   A[i][k]: lane l holds i = l%32, k = 32*(l/32) + 0..31 (byte t of its 8 dwords is k offset t)
+//   B[k][j]: lane l holds j = l%32, k = 32*(l/32) + 0..31
+//   D: as v_mfma_f32_32x32x16_bf16 (checked on gfx950 with an in-bounds probe)
+typedef __attribute__((ext_vector_type(8))) int i32x8;
+__device__ __forceinline__ f32x16 mfma32_fp8(i32x8 a, i32x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+}
+__device__ __forceinline__ i32x8 join_fp8x32(u32x4 lo, u32x4 hi) {
+  return i32x8{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
 // ---------------------------------------------------------------- number formats
 // Four OCP e4m3fn codes (one dword) -> four bf16, exactly: the hardware converter yields fp32
 // values with at most 4 significant bits, so keeping their upper halves loses nothing.

@@ -246,6 +246,69 @@ __device__ __forceinline__ void load_query_minmax(const uint16_t* __restrict__ q
   }
 }
 
+// fp8 keys are scored on the fp8 matrix cores (Eq. 1 / Eq. 11 with e4m3 key codes as they are
+// stored). The bf16 query of each head is scaled by a power of two 2^E (its largest |q| lands in
+// [2^7, 2^8)) and split into two e4m3 terms, q 2^E = hi + lo: the hi term keeps the leading 4
+// significant bits (round to nearest even), the lo term the remaining ones, so the split is exact
+// for every element of at least 2^-2 after scaling, i.e. within 2^10 of the head's largest;
+// smaller ones are off by at most half the e4m3 subnormal step, 2^-10 after scaling, 2^-18 of the
+// head's largest element. The factor 2^-E goes into the head weight: w ReLU(x) = (w 2^-E) ReLU(x 2^E).
+// Operand i of a lane holds dims (D/2) h + 32 i .. + 31, the order the key bytes have in LDS.
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
+
+// four bf16 values (two dwords) times sc -> the e4m3 codes of their hi and lo terms (one dword each)
+__device__ __forceinline__ void split_fp8x4(uint32_t w0, uint32_t w1, float sc, uint32_t& hi, uint32_t& lo) {
+  const float x0 = bf16_lo(w0) * sc, x1 = bf16_hi(w0) * sc, x2 = bf16_lo(w1) * sc, x3 = bf16_hi(w1) * sc;
+  int h = __builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
+  h = __builtin_amdgcn_cvt_pk_fp8_f32(x2, x3, h, true);
+  const f32x2 b01 = __builtin_amdgcn_cvt_pk_f32_fp8(h, false), b23 = __builtin_amdgcn_cvt_pk_f32_fp8(h, true);
+  int l = __builtin_amdgcn_cvt_pk_fp8_f32(x0 - b01.x, x1 - b01.y, 0, false);  // exact differences
+  l = __builtin_amdgcn_cvt_pk_fp8_f32(x2 - b23.x, x3 - b23.y, l, true);
+  hi = (uint32_t)h;
+  lo = (uint32_t)l;
+}
+
+// From the bf16 query operand a (as load_query_operand holds it) and the head weights wr (as
+// load_head_weights holds them): the fp8 operands qh, ql of the D/64 products per tile, and wr
+// multiplied by 2^-E of each head.
+template <int D>
+__device__ __forceinline__ void query_fp8(const u32x4 (&a)[D / 16], int lane, i32x8 (&qh)[D / 64],
+                                          i32x8 (&ql)[D / 64], float (&wr)[16]) {
+  // largest |q| of this lane's head (its D/2 dims here, the other half in lane ^ 32)
+  uint32_t mx = 0;  // bf16 magnitudes order like their bit patterns
+  auto mag2 = [](uint32_t d) { return max(d & 0x7FFFu, (d >> 16) & 0x7FFFu); };
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    const u32x4 v = a[s];
+    mx = max(mx, max(max(mag2(v.x), mag2(v.y)), max(mag2(v.z), mag2(v.w))));
+  }
+  mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
+  const int ex = (int)((mx >> 7) & 0xFF) - 127;  // floor(log2 max|q|) for a normal maximum
+  int E = mx == 0u ? 0 : 7 - ex;
+  E = E < -60 ? -60 : (E > 60 ? 60 : E);
+  const float sc = __uint_as_float((uint32_t)(E + 127) << 23);
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) {
+    uint32_t h[8], l[8];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {  // a[4i + u] holds dims (D/2) h + 32 i + 8 u .. + 7
+      const u32x4 v = a[4 * i + u];
+      split_fp8x4(v.x, v.y, sc, h[2 * u], l[2 * u]);
+      split_fp8x4(v.z, v.w, sc, h[2 * u + 1], l[2 * u + 1]);
+    }
+    qh[i] = i32x8{(int)h[0], (int)h[1], (int)h[2], (int)h[3], (int)h[4], (int)h[5], (int)h[6], (int)h[7]};
+    ql[i] = i32x8{(int)l[0], (int)l[1], (int)l[2], (int)l[3], (int)l[4], (int)l[5], (int)l[6], (int)l[7]};
+  }
+  // head of accumulator register r: 8 (r / 4) + 4 h + r % 4; lane `head` holds that head's exponent
+  const int hh = lane >> 5;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int Er = __shfl(E, 8 * (r / 4) + 4 * hh + (r % 4));
+    wr[r] *= __uint_as_float((uint32_t)(127 - Er) << 23);
+  }
+}
+
 // ============================================================================ Stage 1: coarse page scores
 // Eq. (9), or Eq. (13) with MINMAX. Grid: (ceil(n_rows / R), chunks). Each wave takes tiles of 32
 // block keys of the chunk; R query rows share each loaded tile (prefill). Output: order keys of
@@ -473,6 +536,8 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
   float wr[16];
   load_query_operand<D>(q, g.H, row, lane, a);
   load_head_weights(w, g.H, row, lane, wr);
+  i32x8 qh[D / 64], ql[D / 64];
+  if constexpr (FP8) query_fp8<D>(a, lane, qh, ql, wr);
 
   for (int64_t kk = k0 + wv; kk < k1; kk += 4) {
     const int64_t page = flat ? ri.p_lo + kk : (int64_t)pages[row * g.M + kk];
@@ -510,19 +575,18 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
       u32x4 nraw[RAWN];
       float nsc = 1.f;
       if (tile + 1 < g.P / 32) fetch(krow_of(tile + 1, nok), nraw, nsc);  // in flight while this tile is scored
-      u32x4 bk[KS];
-#pragma unroll
-      for (int v = 0; v < RAWN; ++v) {
-        if (FP8) {
-          bk[2 * v] = fp8x8_to_bf16x8(raw[v].x, raw[v].y);
-          bk[2 * v + 1] = fp8x8_to_bf16x8(raw[v].z, raw[v].w);
-        } else {
-          bk[v] = raw[v];
-        }
-      }
       f32x16 acc = {};
+      if constexpr (FP8) {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) acc = mfma32(a[s], bk[s], acc);
+        for (int i = 0; i < D / 64; ++i) {
+          const i32x8 b = join_fp8x32(raw[2 * i], raw[2 * i + 1]);
+          acc = mfma32_fp8(qh[i], b, acc);
+          acc = mfma32_fp8(ql[i], b, acc);
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) acc = mfma32(a[s], raw[s], acc);
+      }
       float v = head_reduce(acc, wr);
       if (FP8) v *= sc;
       if (lane < 32) dst[tile * 32 + j] = ok ? score_key(v) : 0u;
@@ -599,16 +663,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 
     float wr[16];
     load_query_operand<D>(q, g.H, row, lane, a);
     load_head_weights(w, g.H, row, lane, wr);
+    i32x8 qh[D / 64], ql[D / 64];
+    if constexpr (FP8) query_fp8<D>(a, lane, qh, ql, wr);
     const uint8_t* kb = reinterpret_cast<const uint8_t*>(k);
     uint32_t* const out_row = fine_keys + row * ldf;
-
-    auto widen = [&](const u32x4 (&raw)[LG], int s) -> u32x4 {
-      if (FP8) {
-        const u32x4 r = raw[s >> 1];
-        return (s & 1) ? fp8x8_to_bf16x8_pk(r.z, r.w) : fp8x8_to_bf16x8_pk(r.x, r.y);
-      }
-      return raw[s];
-    };
     auto tiles_of = [&](int c0) { return P - c0 < kFineChunk ? (P - c0) / 32 : kFineChunk / 32; };  // 1 or 2
     // LDS layout of a chunk: row-major key rows, 16-byte granule c of row t at granule c ^ swz(t)
     // (conflict-free reads of one granule by 8 consecutive rows). Load m fills slots 64 m + lane;
@@ -690,10 +748,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 
         lds_read_wait();  // the buffer may be refilled once every read of it has returned
         if (has_next) issue(page_of(nbit), nc0);
         f32x16 acc0 = {}, acc1 = {};
+        if constexpr (FP8) {
   #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          acc0 = mfma32(a[s], widen(raw0, s), acc0);
-          acc1 = mfma32(a[s], widen(raw1, s), acc1);
+          for (int i = 0; i < D / 64; ++i) {
+            const i32x8 b0 = join_fp8x32(raw0[2 * i], raw0[2 * i + 1]), b1 = join_fp8x32(raw1[2 * i], raw1[2 * i + 1]);
+            acc0 = mfma32_fp8(qh[i], b0, acc0);
+            acc1 = mfma32_fp8(qh[i], b1, acc1);
+            acc0 = mfma32_fp8(ql[i], b0, acc0);
+            acc1 = mfma32_fp8(ql[i], b1, acc1);
+          }
+        } else {
+  #pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            acc0 = mfma32(a[s], raw0[s], acc0);
+            acc1 = mfma32(a[s], raw1[s], acc1);
+          }
         }
         // key t of the chunk (position r0 + t) is scored iff lo <= t <= hi (32-bit, wave-uniform bounds)
         const int64_t r0 = page_of(bit) * P + c0;
@@ -758,16 +827,10 @@ __global__ __launch_bounds__(64 * kFlatRows) void flat_dense_kernel(IndexGeom g,
   float wr[16];
   load_query_operand<D>(q, g.H, have_row ? row : last, lane, a);
   load_head_weights(w, g.H, have_row ? row : last, lane, wr);
+  i32x8 qh[D / 64], ql[D / 64];
+  if constexpr (FP8) query_fp8<D>(a, lane, qh, ql, wr);
   const uint8_t* kb = reinterpret_cast<const uint8_t*>(k);
   uint32_t* const out_row = fine_keys + (have_row ? row : 0) * ldf;
-
-  auto widen = [&](const u32x4 (&raw)[LG], int s) -> u32x4 {
-    if (FP8) {
-      const u32x4 r = raw[s >> 1];
-      return (s & 1) ? fp8x8_to_bf16x8_pk(r.z, r.w) : fp8x8_to_bf16x8_pk(r.x, r.y);
-    }
-    return raw[s];
-  };
   // LDS layout of a chunk as in the fine stage (row-major rows, granule c of row t at c ^ swz(t));
   // load m fills slots 64 m + lane, which hold src_off(64 (m % 2) + lane) + 2048 (m / 2) bytes
   // into the chunk's rows
@@ -824,10 +887,21 @@ __global__ __launch_bounds__(64 * kFlatRows) void flat_dense_kernel(IndexGeom g,
       }
       const float sc0 = FP8 ? sb[j] : 1.f, sc1 = FP8 ? sb[32 + j] : 1.f;
       f32x16 acc0 = {}, acc1 = {};
+      if constexpr (FP8) {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        acc0 = mfma32(a[s], widen(raw0, s), acc0);
-        acc1 = mfma32(a[s], widen(raw1, s), acc1);
+        for (int i = 0; i < D / 64; ++i) {
+          const i32x8 b0 = join_fp8x32(raw0[2 * i], raw0[2 * i + 1]), b1 = join_fp8x32(raw1[2 * i], raw1[2 * i + 1]);
+          acc0 = mfma32_fp8(qh[i], b0, acc0);
+          acc1 = mfma32_fp8(qh[i], b1, acc1);
+          acc0 = mfma32_fp8(ql[i], b0, acc0);
+          acc1 = mfma32_fp8(ql[i], b1, acc1);
+        }
+      } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          acc0 = mfma32(a[s], raw0[s], acc0);
+          acc1 = mfma32(a[s], raw1[s], acc1);
+        }
       }
       // key t of the chunk (position base + s0 + t) is scored iff lo <= t <= hi
       const int64_t p0 = base + s0;
@@ -892,14 +966,10 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
   }
   __syncthreads();
   int2* rrow = reinterpret_cast<int2*>(runs + row * (int64_t)k_cap * 2);  // 8-byte aligned (checked on the host)
-  for (int q = threadIdx.x; q < k_cap; q += NT) {
-    int2 v = make_int2(-1, 0);
-    if (q < nr) {
-      const int s0 = rstart[q];
-      const int s1 = q + 1 < nr ? rstart[q + 1] : cnt;
-      v = make_int2(lidx[s0], s1 - s0);
-    }
-    rrow[q] = v;
+  for (int q = threadIdx.x; q < nr; q += NT) {  // entries past run_count are not written
+    const int s0 = rstart[q];
+    const int s1 = q + 1 < nr ? rstart[q + 1] : cnt;
+    rrow[q] = make_int2(lidx[s0], s1 - s0);
   }
   if (threadIdx.x == 0) run_count[row] = nr;
 }

@@ -119,15 +119,29 @@ def check_index_rows(w, rows_t, gpu_idx, gpu_cnt, gpu_pages, results, allow_page
 
 
 def check_runs(gpu_runs, gpu_run_count, gpu_idx, gpu_cnt, C):
-    """Runs must be exactly the oracle's re-encoding of the GPU's own index list."""
+    """Runs must be exactly the oracle's re-encoding of the GPU's own index list (entries past the
+    run count are not part of the output)."""
     for i in range(len(gpu_cnt)):
         S = np.asarray(gpu_idx[i][: int(gpu_cnt[i])])
         want = orc.runs_of(S, C)
         n = int(gpu_run_count[i])
         got = [tuple(x) for x in np.asarray(gpu_runs[i][:n]).tolist()]
         assert got == want, f"row {i}: runs differ"
-        pad = np.asarray(gpu_runs[i][n:])
-        assert np.all(pad[:, 0] == -1) and np.all(pad[:, 1] == 0)
+
+
+def assert_same_index_outputs(a, b, rows=None):
+    """Two index outputs (dicts of numpy arrays) are identical: every array exactly, except runs,
+    which only count up to each row's run count (entries past it are not written)."""
+    sel = slice(None) if rows is None else rows
+    assert set(a) == set(b), (sorted(a), sorted(b))
+    for key in a:
+        if key == "runs":
+            continue
+        assert np.array_equal(a[key], b[key][sel]), key
+    if "runs" in a:
+        ra, rb, n = a["runs"], b["runs"][sel], a["run_count"]
+        for i in range(len(n)):
+            assert np.array_equal(ra[i][: n[i]], rb[i][: n[i]]), f"runs of row {i}"
 
 
 def check_attention_row(o_gpu, lse_gpu, o_ref, lse_ref, where=""):
