@@ -309,18 +309,50 @@ __device__ __forceinline__ void query_fp8(const u32x4 (&a)[D / 16], int lane, i3
   }
 }
 
+// One direct global->LDS load (16 or 4 bytes per lane; lane i writes LDS bytes [lds + SIZE*i, ..)),
+// issued from asm so that the compiler's wait insertion does not drain it before LDS reads that it
+// cannot prove disjoint; callers wait with an explicit vmcnt. M0 (the load's LDS base) is saved and
+// restored; the s_nop is the wait state between writing M0 and the load reading it.
+// The address is a wave-uniform 64-bit base plus a per-lane 32-bit byte offset.
+template <int SIZE>
+__device__ __forceinline__ void lds_dma(const void* base, uint32_t off, uint32_t lds) {
+  static_assert(SIZE == 16 || SIZE == 4, "load size");
+  uint32_t save;
+  if constexpr (SIZE == 16)
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+                 : "=&s"(save) : "v"(off), "s"(base), "s"(lds) : "memory");
+  else
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2\n\ts_mov_b32 m0, %0"
+                 : "=&s"(save) : "v"(off), "s"(base), "s"(lds) : "memory");
+}
+// Every LDS read this wave issued has returned its data.
+__device__ __forceinline__ void lds_read_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // ============================================================================ Stage 1: coarse page scores
 // Eq. (9), or Eq. (13) with MINMAX. Grid: (ceil(n_rows / R), chunks). Each wave takes tiles of 32
 // block keys of the chunk; R query rows share each loaded tile (prefill). Output: order keys of
 // the page scores, page_keys[row * ld + p] for eligible pages p.
+// Prefill mean keys (the tile's 32 block keys are consecutive rows of the cache): each wave
+// copies its next tile into its own LDS buffer by direct loads while it scores the current one,
+// whole key rows per 16 (or 8) consecutive lanes, so that a load touches 4 (or 8) rows instead of
+// one row per lane; granule c of row t sits at slot c ^ coarse_swz(t) of the row, which keeps the
+// operand reads (16 rows, one granule) free of bank conflicts. Paged and min-max keys are read
+// straight into the operand layout.
+constexpr int kCoarseRowsStaged = 3;
+constexpr int kCoarseStagedWaves = 1;  // waves of a staged-path workgroup
+template <int GR>  // 16-byte granules per key row: 16 (d = 128) or 8 (d = 64)
+__device__ __forceinline__ int coarse_swz(int t) { return GR == 16 ? (t & 15) : ((t >> 1) & 7); }
+
 template <int D, int R, bool PAGED, bool MINMAX>
-__global__ __launch_bounds__(256) void coarse_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void coarse_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
                                                      const float* __restrict__ w, const uint16_t* __restrict__ kmean,
                                                      uint32_t* __restrict__ page_keys, int64_t ld, int tiles_per_chunk) {
   constexpr int DK = MINMAX ? 2 * D : D;  // width of a block key and of the dot product
   constexpr int KS = DK / 16;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31;
-  const int64_t row0 = (int64_t)blockIdx.x * R;
+  // prefill: the last query rows (the most eligible pages) first, so that the long workgroups do
+  // not form the tail of the launch
+  const int64_t row0 = (int64_t)(PAGED ? blockIdx.x : gridDim.x - 1 - blockIdx.x) * R;
   const int nsub = g.P / g.B;
 
   RowInfo ri[R];
@@ -348,6 +380,63 @@ __global__ __launch_bounds__(256) void coarse_kernel(IndexGeom g, int64_t n_rows
     load_head_weights(w, g.H, row, lane, wr[r]);
   }
   const int64_t p_base = ri[0].p_lo;  // identical for every row (depends on k_sink only)
+
+  if constexpr (!PAGED && !MINMAX) if (g.n_sub > 0 && g.n_sub <= ((int64_t)1 << 32) / DK / 2) {
+    constexpr int RB = DK * 2, GR = RB / 16;  // key row bytes, granules
+    constexpr int NDMA = 32 * RB / 1024;      // direct loads per tile (1 KB each)
+    constexpr int RPL = 1024 / RB;            // key rows per load
+    __shared__ __attribute__((aligned(16))) uint8_t csm[kCoarseStagedWaves][2][32 * RB];
+    const int64_t row_lim = g.n_sub - 1;      // (rows past the cache are loaded clamped, scored as 0)
+    // load slot: lane -> key row RPL m + lane / GR of the tile, granule (lane % GR) ^ swz(row)
+    const int tl = lane / GR, cl = lane % GR;
+    const uint8_t* base = reinterpret_cast<const uint8_t*>(kmean);  // byte offsets fit 32 bits (host check)
+    auto issue = [&](int64_t tile, int buf) {
+      const int64_t r0 = p_base * nsub + tile * 32;
+      const uint32_t lds = lds_addr(&csm[wv][buf][0]);
+#pragma unroll
+      for (int m = 0; m < NDMA; ++m) {
+        const int t = RPL * m + tl;
+        const int64_t rr = r0 + t < row_lim ? r0 + t : row_lim;
+        const uint32_t off = (uint32_t)(rr * RB + 16 * (cl ^ coarse_swz<GR>(t)));
+        lds_dma<16>(base, off, lds + 1024 * m);
+      }
+    };
+    // operand read: lane (j, h) at k-step s takes granule (GR / 2) h + s of key row j
+    const uint32_t rd = (uint32_t)(j * RB);
+    const int swz_j = coarse_swz<GR>(j), h = lane >> 5;
+    constexpr int NW = kCoarseStagedWaves;
+    int buf = 0;
+    if (tile_beg + wv < tile_end) issue(tile_beg + wv, 0);
+    for (int64_t tile = tile_beg + wv; tile < tile_end; tile += NW) {
+      const bool more = tile + NW < tile_end;
+      if (more) issue(tile + NW, buf ^ 1);
+      if (more) vm_wait<NDMA>();  // this tile's loads (and earlier stores) are done
+      else vm_wait<0>();
+      const uint8_t* tb = &csm[wv][buf][0];
+      u32x4 b[KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        b[s] = *reinterpret_cast<const u32x4*>(tb + rd + 16 * ((((GR / 2) * h) + s) ^ swz_j));
+      const int64_t sb = tile * 32 + j;
+      const int64_t p = p_base + sb / nsub;
+      const int sub_in_page = (int)(sb % nsub);
+      const bool okp = p * nsub + sub_in_page < g.n_sub;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        f32x16 acc = {};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) acc = mfma32(a[r][s], b[s], acc);
+        float v = head_reduce(acc, wr[r]);
+        for (int o = 1; o < nsub; o <<= 1) v += __shfl_xor(v, o);  // sum the sub-blocks of a page
+        const int64_t row = row0 + r;
+        if (lane < 32 && sub_in_page == 0 && row < n_rows && ri[r].valid && p <= ri[r].p_hi)
+          page_keys[row * ld + p] = okp ? score_key(v) : 0u;
+      }
+      lds_read_wait();  // the operand reads of this buffer are done before it is refilled
+      buf ^= 1;
+    }
+    return;
+  }
 
   for (int64_t tile = tile_beg + wv; tile < tile_end; tile += 4) {
     const int64_t sb = tile * 32 + j;            // sub-block counted from the first eligible page
@@ -615,25 +704,6 @@ __device__ __forceinline__ int fine_swz(int t) {
 
 constexpr int kFineChunk = 64;  // key rows staged in LDS at a time
 constexpr int kFineRowsPerWave = 8;  // query rows a fine-scoring wave takes in turn
-
-// One direct global->LDS load (16 or 4 bytes per lane; lane i writes LDS bytes [lds + SIZE*i, ..)),
-// issued from asm so that the compiler's wait insertion does not drain it before LDS reads that it
-// cannot prove disjoint; callers wait with an explicit vmcnt. M0 (the load's LDS base) is saved and
-// restored; the s_nop is the wait state between writing M0 and the load reading it.
-// The address is a wave-uniform 64-bit base plus a per-lane 32-bit byte offset.
-template <int SIZE>
-__device__ __forceinline__ void lds_dma(const void* base, uint32_t off, uint32_t lds) {
-  static_assert(SIZE == 16 || SIZE == 4, "load size");
-  uint32_t save;
-  if constexpr (SIZE == 16)
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
-                 : "=&s"(save) : "v"(off), "s"(base), "s"(lds) : "memory");
-  else
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2\n\ts_mov_b32 m0, %0"
-                 : "=&s"(save) : "v"(off), "s"(base), "s"(lds) : "memory");
-}
-// Every LDS read this wave issued has returned its data.
-__device__ __forceinline__ void lds_read_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 64 ? 4 : 3, 8))) void fine_xcd_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
@@ -1324,11 +1394,14 @@ template <int D, int R, bool PAGED, bool MINMAX>
 static hipError_t launch_coarse_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
                                   const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
                                   hipStream_t st) {
-  const int tiles_per_chunk = PAGED ? 8 : (int)(max_tiles > 0 ? max_tiles : 1);
+  // the staged path (one wave per workgroup) splits long rows into chunks of 64 tiles
+  const bool staged = !PAGED && !MINMAX && g.n_sub > 0 && g.n_sub <= ((int64_t)1 << 32) / D / 2;
+  const int tiles_per_chunk = PAGED ? 8 : staged ? 64 : (int)(max_tiles > 0 ? max_tiles : 1);
   const int64_t chunks = (max_tiles + tiles_per_chunk - 1) / tiles_per_chunk;
   if (chunks == 0 || n_rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((n_rows + R - 1) / R), (unsigned)chunks);
-  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED, MINMAX>), grid, dim3(256), 0, st, g, n_rows, q, w, kmean, page_keys,
+  const int threads = staged ? 64 * kCoarseStagedWaves : 256;
+  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED, MINMAX>), grid, dim3(threads), 0, st, g, n_rows, q, w, kmean, page_keys,
                      ld, tiles_per_chunk);
   return hipGetLastError();
 }
@@ -1337,8 +1410,9 @@ template <int D, bool MINMAX>
 static hipError_t launch_coarse_d(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
                                   const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
                                   hipStream_t st) {
-  // min-max doubles the operands' width: fewer query rows share a tile (register budget)
-  constexpr int R = MINMAX ? 2 : 4;
+  // query rows sharing a tile: min-max doubles the operands' width, and the staged mean-key path
+  // keeps its tile addressing live (register budget of two waves per SIMD)
+  constexpr int R = MINMAX ? 2 : kCoarseRowsStaged;
   return g.ctx_len != nullptr ? launch_coarse_t<D, 1, true, MINMAX>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
                               : launch_coarse_t<D, R, false, MINMAX>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
 }
