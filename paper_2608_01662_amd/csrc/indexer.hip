@@ -332,27 +332,29 @@ __device__ __forceinline__ void lds_read_wait() { asm volatile("s_waitcnt lgkmcn
 // Eq. (9), or Eq. (13) with MINMAX. Grid: (ceil(n_rows / R), chunks). Each wave takes tiles of 32
 // block keys of the chunk; R query rows share each loaded tile (prefill). Output: order keys of
 // the page scores, page_keys[row * ld + p] for eligible pages p.
-// Prefill mean keys (the tile's 32 block keys are consecutive rows of the cache): each wave
-// copies its next tile into its own LDS buffer by direct loads while it scores the current one,
-// whole key rows per 16 (or 8) consecutive lanes, so that a load touches 4 (or 8) rows instead of
-// one row per lane; granule c of row t sits at slot c ^ coarse_swz(t) of the row, which keeps the
-// operand reads (16 rows, one granule) free of bank conflicts. Paged and min-max keys are read
-// straight into the operand layout.
-constexpr int kCoarseRowsStaged = 3;
-constexpr int kCoarseStagedWaves = 1;  // waves of a staged-path workgroup
+// STAGED (prefill mean keys, rows of at most kCoarseStagedTiles tiles; the tile's 32 block keys are
+// consecutive rows of the cache): one wave per workgroup takes every tile of its R rows, the rows
+// with the most eligible pages first so that the long workgroups do not form the tail of the
+// launch; it copies its next tile into its own LDS buffer by direct loads while it scores the
+// current one, whole key rows per 16 (or 8) consecutive lanes, so that a load touches 4 (or 8)
+// rows instead of one row per lane; granule c of row t sits at slot c ^ coarse_swz(t) of the row,
+// which keeps the operand reads (16 rows, one granule) free of bank conflicts. Otherwise four waves
+// share the tiles of R rows and read the keys straight into the operand layout (long rows: the
+// block keys no longer fit the L2, and four rows per tile read them fewer times).
+constexpr int kCoarseRowsStaged = 3;   // query rows of a staged workgroup (register budget)
+constexpr int kCoarseStagedTiles = 64; // longest row (in 32-key tiles) taken by the staged kernel
 template <int GR>  // 16-byte granules per key row: 16 (d = 128) or 8 (d = 64)
 __device__ __forceinline__ int coarse_swz(int t) { return GR == 16 ? (t & 15) : ((t >> 1) & 7); }
 
-template <int D, int R, bool PAGED, bool MINMAX>
+template <int D, int R, bool PAGED, bool MINMAX, bool STAGED = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void coarse_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
                                                      const float* __restrict__ w, const uint16_t* __restrict__ kmean,
                                                      uint32_t* __restrict__ page_keys, int64_t ld, int tiles_per_chunk) {
   constexpr int DK = MINMAX ? 2 * D : D;  // width of a block key and of the dot product
   constexpr int KS = DK / 16;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31;
-  // prefill: the last query rows (the most eligible pages) first, so that the long workgroups do
-  // not form the tail of the launch
-  const int64_t row0 = (int64_t)(PAGED ? blockIdx.x : gridDim.x - 1 - blockIdx.x) * R;
+  static_assert(!STAGED || (!PAGED && !MINMAX), "staged tiles are consecutive mean keys");
+  const int64_t row0 = (int64_t)(STAGED ? gridDim.x - 1 - blockIdx.x : blockIdx.x) * R;
   const int nsub = g.P / g.B;
 
   RowInfo ri[R];
@@ -381,18 +383,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   }
   const int64_t p_base = ri[0].p_lo;  // identical for every row (depends on k_sink only)
 
-  if constexpr (!PAGED && !MINMAX) if (g.n_sub > 0 && g.n_sub <= ((int64_t)1 << 32) / DK / 2) {
+  if constexpr (STAGED) {  // (the launcher checks 0 < n_sub and n_sub * row bytes < 2^32)
     constexpr int RB = DK * 2, GR = RB / 16;  // key row bytes, granules
     constexpr int NDMA = 32 * RB / 1024;      // direct loads per tile (1 KB each)
     constexpr int RPL = 1024 / RB;            // key rows per load
-    __shared__ __attribute__((aligned(16))) uint8_t csm[kCoarseStagedWaves][2][32 * RB];
+    __shared__ __attribute__((aligned(16))) uint8_t csm[2][32 * RB];
     const int64_t row_lim = g.n_sub - 1;      // (rows past the cache are loaded clamped, scored as 0)
     // load slot: lane -> key row RPL m + lane / GR of the tile, granule (lane % GR) ^ swz(row)
     const int tl = lane / GR, cl = lane % GR;
     const uint8_t* base = reinterpret_cast<const uint8_t*>(kmean);  // byte offsets fit 32 bits (host check)
     auto issue = [&](int64_t tile, int buf) {
       const int64_t r0 = p_base * nsub + tile * 32;
-      const uint32_t lds = lds_addr(&csm[wv][buf][0]);
+      const uint32_t lds = lds_addr(&csm[buf][0]);
 #pragma unroll
       for (int m = 0; m < NDMA; ++m) {
         const int t = RPL * m + tl;
@@ -404,15 +406,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     // operand read: lane (j, h) at k-step s takes granule (GR / 2) h + s of key row j
     const uint32_t rd = (uint32_t)(j * RB);
     const int swz_j = coarse_swz<GR>(j), h = lane >> 5;
-    constexpr int NW = kCoarseStagedWaves;
     int buf = 0;
-    if (tile_beg + wv < tile_end) issue(tile_beg + wv, 0);
-    for (int64_t tile = tile_beg + wv; tile < tile_end; tile += NW) {
-      const bool more = tile + NW < tile_end;
-      if (more) issue(tile + NW, buf ^ 1);
+    issue(tile_beg, 0);
+    for (int64_t tile = tile_beg; tile < tile_end; ++tile) {
+      const bool more = tile + 1 < tile_end;
+      if (more) issue(tile + 1, buf ^ 1);
       if (more) vm_wait<NDMA>();  // this tile's loads (and earlier stores) are done
       else vm_wait<0>();
-      const uint8_t* tb = &csm[wv][buf][0];
+      const uint8_t* tb = &csm[buf][0];
       u32x4 b[KS];
 #pragma unroll
       for (int s = 0; s < KS; ++s)
@@ -1394,14 +1395,19 @@ template <int D, int R, bool PAGED, bool MINMAX>
 static hipError_t launch_coarse_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
                                   const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
                                   hipStream_t st) {
-  // the staged path (one wave per workgroup) splits long rows into chunks of 64 tiles
-  const bool staged = !PAGED && !MINMAX && g.n_sub > 0 && g.n_sub <= ((int64_t)1 << 32) / D / 2;
-  const int tiles_per_chunk = PAGED ? 8 : staged ? 64 : (int)(max_tiles > 0 ? max_tiles : 1);
+  if (max_tiles <= 0 || n_rows == 0) return hipSuccess;
+  if (!PAGED && !MINMAX && max_tiles <= kCoarseStagedTiles && g.n_sub > 0 &&
+      g.n_sub <= ((int64_t)1 << 32) / D / 2) {  // one wave per workgroup, all tiles of its rows
+    constexpr int RS = kCoarseRowsStaged;
+    const dim3 grid((unsigned)((n_rows + RS - 1) / RS), 1u);
+    hipLaunchKernelGGL((coarse_kernel<D, RS, false, false, true>), grid, dim3(64), 0, st, g, n_rows, q, w, kmean,
+                       page_keys, ld, (int)max_tiles);
+    return hipGetLastError();
+  }
+  const int tiles_per_chunk = PAGED ? 8 : (int)max_tiles;
   const int64_t chunks = (max_tiles + tiles_per_chunk - 1) / tiles_per_chunk;
-  if (chunks == 0 || n_rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((n_rows + R - 1) / R), (unsigned)chunks);
-  const int threads = staged ? 64 * kCoarseStagedWaves : 256;
-  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED, MINMAX>), grid, dim3(threads), 0, st, g, n_rows, q, w, kmean, page_keys,
+  hipLaunchKernelGGL((coarse_kernel<D, R, PAGED, MINMAX>), grid, dim3(256), 0, st, g, n_rows, q, w, kmean, page_keys,
                      ld, tiles_per_chunk);
   return hipGetLastError();
 }
@@ -1410,9 +1416,8 @@ template <int D, bool MINMAX>
 static hipError_t launch_coarse_d(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w,
                                   const uint16_t* kmean, uint32_t* page_keys, int64_t ld, int64_t max_tiles,
                                   hipStream_t st) {
-  // query rows sharing a tile: min-max doubles the operands' width, and the staged mean-key path
-  // keeps its tile addressing live (register budget of two waves per SIMD)
-  constexpr int R = MINMAX ? 2 : kCoarseRowsStaged;
+  // min-max doubles the operands' width: fewer query rows share a tile (register budget)
+  constexpr int R = MINMAX ? 2 : 4;
   return g.ctx_len != nullptr ? launch_coarse_t<D, 1, true, MINMAX>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st)
                               : launch_coarse_t<D, R, false, MINMAX>(g, n_rows, q, w, kmean, page_keys, ld, max_tiles, st);
 }
