@@ -1435,7 +1435,10 @@ hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t
                               int32_t* pages, int64_t max_elig, hipStream_t st) {
   if (n_rows == 0) return hipSuccess;
   const size_t lds = (size_t)(max_elig > 0 ? max_elig : 1) * 4;
-  hipLaunchKernelGGL(page_select_kernel<256>, dim3((unsigned)n_rows), dim3(256), lds, st, g, n_rows, page_keys, ld, pages);
+  if (n_rows <= kSelectFewRows)  // few rows (decode): more threads per row
+    hipLaunchKernelGGL(page_select_kernel<1024>, dim3((unsigned)n_rows), dim3(1024), lds, st, g, n_rows, page_keys, ld, pages);
+  else
+    hipLaunchKernelGGL(page_select_kernel<256>, dim3((unsigned)n_rows), dim3(256), lds, st, g, n_rows, page_keys, ld, pages);
   return hipGetLastError();
 }
 
@@ -1657,6 +1660,8 @@ hipError_t prepare_index_kernels() {
     if (e != hipSuccess) return e;
   }
   e = hipFuncSetAttribute((const void*)page_select_kernel<256>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)page_select_kernel<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
   if (e != hipSuccess) return e;
 
   if (dev >= 0 && dev < 64) done[dev] = true;
