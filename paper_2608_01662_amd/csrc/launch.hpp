@@ -35,8 +35,9 @@ hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, co
 // Dynamic LDS bytes of the token selection; rows of up to kSelectRegMax candidates keep their keys
 // in registers (20 KB of static LDS), larger ones stage them in LDS (4 KB of static LDS).
 constexpr int64_t kSelectRegMax = 512 * 64;
-// Calls with at most this many rows (decode batches) select rows of <= 8192 candidates with 1024
-// threads per row instead of 512: with few rows the GPU is mostly idle and per-row latency counts.
+// Calls with at most this many rows (decode batches) select tokens (rows of <= 8192 candidates) and
+// pages with 1024 threads per row instead of 512 and 256: with few rows the GPU is mostly idle and
+// per-row latency counts.
 constexpr int64_t kSelectFewRows = 1024;
 size_t token_select_lds_bytes(int64_t slots_cap, int k_cap, int M);
 inline size_t token_select_static_lds(int64_t slots_cap) { return slots_cap <= kSelectRegMax ? 20 * 1024 : 4 * 1024; }
