@@ -1054,6 +1054,33 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
 constexpr int kSelHistBits = 11;
 constexpr int kSelGatherCap = 8192;
 
+// One streaming pass over a row's n keys in global memory (n a multiple of 32, the row 16-byte
+// aligned): wave w takes the contiguous span [w S, w S + S) (S: the row over the NT / 64 waves, in
+// stretches of 256 keys), lane l reading keys 4l .. 4l + 3 of each stretch with one 16-byte load,
+// four stretches in flight. fn(i, keys i .. i + 3, valid) is called per lane for every stretch of
+// the span in increasing order, so a wave visits its span in position order (stretch by stretch,
+// lane by lane).
+template <int NT, typename F>
+__device__ __forceinline__ void stream_row(const uint32_t* keys, int n, F&& fn) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int span = (n + NW * 256 - 1) / (NW * 256) * 256;
+  const int s0 = wv * span, s1 = s0 + span < n ? s0 + span : n;
+  for (int b = s0; b < s1; b += 1024) {
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = b + 256 * u + 4 * lane;
+      v[u] = i < s1 ? *reinterpret_cast<const u32x4*>(keys + i) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = b + 256 * u + 4 * lane;
+      if (b + 256 * u < s1) fn(i, v[u], i < s1);  // (uniform per wave: the stretch starts in the span)
+    }
+  }
+}
+
 template <int NT>
 __device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h11, uint32_t* sub, int* gcnt,
                                 uint32_t* hist, int* wsum, uint32_t& T, int& take_eq) {
@@ -1062,13 +1089,15 @@ __device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h1
   if (threadIdx.x == 0) *gcnt = 0;
   __syncthreads();
   int nz = 0;
-  for (int i = threadIdx.x; i < n; i += NT) {
-    const uint32_t key = keys[i];
-    if (key != 0u) {
-      atomicAdd(&h11[key >> (32 - kSelHistBits)], 1u);
-      ++nz;
-    }
-  }
+  stream_row<NT>(keys, n, [&](int, const u32x4& v, bool ok) {
+    const uint32_t k4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (ok && k4[c] != 0u) {
+        atomicAdd(&h11[k4[c] >> (32 - kSelHistBits)], 1u);
+        ++nz;
+      }
+  });
   nz = wave_sum(nz);
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = nz;
   __syncthreads();
@@ -1107,19 +1136,98 @@ __device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h1
   const int rem = k - wsum[1];
   // the boundary bin's keys -> LDS (order is irrelevant: only the threshold and the number of
   // ties to take are derived from them; select_compact then takes ties in position order)
-  for (int i = threadIdx.x; i < n; i += NT) {
-    const uint32_t key = keys[i];
-    if (key != 0u && (key >> (32 - kSelHistBits)) == bstar) {
-      const int at = atomicAdd(gcnt, 1);
-      if (at < kSelGatherCap) sub[at] = key;
-    }
-  }
+  stream_row<NT>(keys, n, [&](int, const u32x4& v, bool ok) {
+    const uint32_t k4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (ok && k4[c] != 0u && (k4[c] >> (32 - kSelHistBits)) == bstar) {
+        const int at = atomicAdd(gcnt, 1);
+        if (at < kSelGatherCap) sub[at] = k4[c];
+      }
+  });
   __syncthreads();
   const int nb = *gcnt;
   __syncthreads();
   if (nb <= kSelGatherCap) radix_threshold<NT>(sub, nb, rem, hist, wsum, T, take_eq);
   else radix_threshold<NT>(keys, n, k, hist, wsum, T, take_eq);
   return n_valid;
+}
+
+// select_compact for keys in global memory, in two streaming passes: each wave counts its span's
+// keys above T and its ties, one block scan of the per-wave counts gives each wave its first output
+// rank and the number of ties before its span, and each wave then writes its selected positions in
+// position order (wave-wide prefix sums per stretch, no block barrier). Same selection and ranks
+// as select_compact; returns the number selected.
+template <int NT, typename F>
+__device__ int global_compact(const uint32_t* keys, int n, uint32_t T, int take_eq, int* wsum, F&& emit) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int gt = 0, eq = 0;
+  stream_row<NT>(keys, n, [&](int, const u32x4& v, bool ok) {
+    const uint32_t k4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      gt += ok && k4[c] > T;
+      eq += ok && k4[c] == T;
+    }
+  });
+  gt = wave_sum(gt);
+  eq = wave_sum(eq);
+  if (lane == 0) {
+    wsum[wv] = gt;
+    wsum[NW + wv] = eq;
+  }
+  __syncthreads();
+  int sel_before = 0, eq_before = 0, total = 0, eqb = 0;
+#pragma unroll
+  for (int x = 0; x < NW; ++x) {
+    const int g_ = wsum[x], e_ = wsum[NW + x];
+    int t_ = take_eq - eqb;
+    t_ = t_ < 0 ? 0 : (t_ > e_ ? e_ : t_);
+    if (x < wv) {
+      sel_before += g_ + t_;
+      eq_before += e_;
+    }
+    total += g_ + t_;
+    eqb += e_;
+  }
+  __syncthreads();  // (wsum is reused by the caller)
+  auto excl = [&](int v, int& tot) {  // exclusive prefix over the lanes, and the wave total
+    int inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(inc, o);
+      if (lane >= o) inc += t;
+    }
+    tot = __shfl(inc, 63);
+    return inc - v;
+  };
+  int out = sel_before, eqr = eq_before;
+  stream_row<NT>(keys, n, [&](int i, const u32x4& v, bool ok) {
+    const uint32_t k4[4] = {v.x, v.y, v.z, v.w};
+    int e_l = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) e_l += ok && k4[c] == T;
+    int e_tot;
+    int er = eqr + excl(e_l, e_tot);
+    bool sel[4];
+    int s_l = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bool is_eq = ok && k4[c] == T;
+      sel[c] = ok && (k4[c] > T || (is_eq && er < take_eq));
+      er += is_eq;
+      s_l += sel[c];
+    }
+    int s_tot;
+    int r = out + excl(s_l, s_tot);
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (sel[c]) emit(r++, i + c);
+    out += s_tot;
+    eqr += e_tot;
+  });
+  return total;
 }
 
 // Eq. (12) / Eq. (7) then Eq. (6): S_t = sink ++ (top K_sparse candidates, ascending) ++ window;
@@ -1178,10 +1286,13 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
     const int P = g.P;
     const int64_t p_lo = ri.p_lo;
     const int ks = g.k_sink;
-    const int n_sp = select_compact<NT>(keys, n, T, take, wsum, [&](int rank, int i) {
+    auto emit = [&](int rank, int i) {
       const int64_t page = flat ? p_lo + i / P : (int64_t)lpages[i / P];
       lidx[ks + rank] = (int32_t)(page * P + i % P);
-    });
+    };
+    int n_sp;
+    if constexpr (GK) n_sp = global_compact<NT>(keys, n, T, take, wsum, emit);
+    else n_sp = select_compact<NT>(keys, n, T, take, wsum, emit);
     for (int i = threadIdx.x; i < g.k_sink; i += NT) lidx[i] = i;
     for (int i = threadIdx.x; i < g.k_swa; i += NT) lidx[g.k_sink + n_sp + i] = (int32_t)(ri.t - g.k_swa + 1 + i);
     cnt = g.k_sink + n_sp + g.k_swa;
