@@ -629,42 +629,55 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
   i32x8 qh[D / 64], ql[D / 64];
   if constexpr (FP8) query_fp8<D>(a, lane, qh, ql, wr);
 
-  for (int64_t kk = k0 + wv; kk < k1; kk += 4) {
-    const int64_t page = flat ? ri.p_lo + kk : (int64_t)pages[row * g.M + kk];
-    int64_t kbase = -1;  // key row of the page's first token
-    if (page >= ri.p_lo && page <= ri.p_hi) {
-      if (PAGED) {
-        const int64_t ph = phys_page(g, row, page);
-        kbase = ph >= 0 ? ph * g.kv_page : -1;
-      } else {
-        kbase = page * g.P;  // positions checked below stay <= hi < n_kv
+  constexpr int RAWN = FP8 ? D / 32 : D / 16;  // 16-byte loads per lane per tile
+  auto fetch = [&](int64_t kr, u32x4 (&r)[RAWN], float& scl) {
+    const u32x4* pp = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(k) + kr * (FP8 ? D : 2 * D) +
+                                                    (FP8 ? D / 2 : D) * (lane >> 5));
+#pragma unroll
+    for (int v = 0; v < RAWN; ++v) r[v] = pp[v];
+    scl = FP8 ? kscale[kr] : 1.f;
+  };
+  const int tpp = g.P / 32;  // 32-token tiles per page
+  // the wave's pages (every fourth of the chunk) two at a time: both pages' first key rows are
+  // resolved before any key is loaded, then their (page, tile) items are scored in turn with the
+  // next item's keys in flight, so the second page's lookups overlap the first page's scoring
+  for (int64_t kk0 = k0 + wv; kk0 < k1; kk0 += 8) {
+    int64_t pg[2], kb[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t kk = kk0 + 4 * u;
+      pg[u] = kk < k1 ? (flat ? ri.p_lo + kk : (int64_t)pages[row * g.M + kk]) : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      kb[u] = -1;  // key row of the page's first token
+      if (pg[u] >= ri.p_lo && pg[u] <= ri.p_hi) {
+        if (PAGED) {
+          const int64_t ph = phys_page(g, row, pg[u]);
+          kb[u] = ph >= 0 ? ph * g.kv_page : -1;
+        } else {
+          kb[u] = pg[u] * g.P;  // positions checked below stay <= hi < n_kv
+        }
       }
     }
-    uint32_t* dst = fine_keys + row * ldf + kk * g.P;
-    // key row of lane j in `tile` (row 0, not scored, outside E_t or the cache)
-    auto krow_of = [&](int tile, bool& ok) -> int64_t {
+    const int n_items = (kk0 + 4 < k1 ? 2 : 1) * tpp;
+    // key row of lane j in `item` (row 0, not scored, outside E_t or the cache)
+    auto krow_of = [&](int item, bool& ok) -> int64_t {
+      const int u = item >= tpp, tile = item - u * tpp;
+      const int64_t page = u ? pg[1] : pg[0], kbase = u ? kb[1] : kb[0];
       const int64_t pos = page * g.P + tile * 32 + j;
       ok = kbase >= 0 && pos >= ri.lo && pos <= ri.hi;
       return ok ? kbase + tile * 32 + j : 0;
     };
-    constexpr int RAWN = FP8 ? D / 32 : D / 16;  // 16-byte loads per lane per tile
-    auto fetch = [&](int64_t kr, u32x4 (&r)[RAWN], float& scl) {
-      const u32x4* pp = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint8_t*>(k) + kr * (FP8 ? D : 2 * D) +
-                                                      (FP8 ? D / 2 : D) * (lane >> 5));
-#pragma unroll
-      for (int v = 0; v < RAWN; ++v) r[v] = pp[v];
-      scl = FP8 ? kscale[kr] : 1.f;
-    };
     bool ok;
-    int64_t krow = krow_of(0, ok);
     u32x4 raw[RAWN];
     float sc;
-    fetch(krow, raw, sc);
-    for (int tile = 0; tile < g.P / 32; ++tile) {
+    fetch(krow_of(0, ok), raw, sc);
+    for (int item = 0; item < n_items; ++item) {
       bool nok = false;
       u32x4 nraw[RAWN];
       float nsc = 1.f;
-      if (tile + 1 < g.P / 32) fetch(krow_of(tile + 1, nok), nraw, nsc);  // in flight while this tile is scored
+      if (item + 1 < n_items) fetch(krow_of(item + 1, nok), nraw, nsc);  // in flight while this tile is scored
       f32x16 acc = {};
       if constexpr (FP8) {
 #pragma unroll
@@ -679,7 +692,8 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
       }
       float v = head_reduce(acc, wr);
       if (FP8) v *= sc;
-      if (lane < 32) dst[tile * 32 + j] = ok ? score_key(v) : 0u;
+      const int u = item >= tpp, tile = item - u * tpp;
+      if (lane < 32) fine_keys[row * ldf + (kk0 + 4 * u) * g.P + tile * 32 + j] = ok ? score_key(v) : 0u;
       ok = nok;
       sc = nsc;
 #pragma unroll
