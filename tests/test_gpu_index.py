@@ -139,6 +139,25 @@ def test_index_prefill_parity(w):
     print(w.name, stats)
 
 
+def test_coarse_long_rows():
+    """Calls whose rows hold more than 64 coarse tiles use the four-wave coarse_kernel over four
+    query rows (keys read straight into the operand layout) instead of the staged one-wave kernel:
+    d_I = 64, 2-token sub-blocks in 64-token pages (32 per page) and L = 8192 give the last rows
+    128 tiles of 32 sub-blocks (coarse_kernel<64, 4, false, false, false>). Sampled rows against
+    the oracle, stage-wise."""
+    from dataclasses import replace
+    w = replace(W.SMALL_MLA, name="small_L8192_d64_B2", head_dim=64, sub_block=2, seq_len=8192)
+    assert (w.seq_len // w.page) * (w.page // w.sub_block) // 32 > 64
+    inp = P.prefill_inputs(w)
+    out, _ = _run_prefill(w, inp)
+    boundary = [w.k_sink + w.k_swa, w.k_sink + w.k_swa + w.page, w.keep_pages * w.page + w.k_swa, w.seq_len - 2]
+    rows = _sample_rows(w.seq_len, 157, boundary)
+    res = _oracle_rows(w, inp, rows)
+    stats = P.check_index_rows(w, rows, out["idx"][rows], out["count"][rows], out["pages"][rows], res)
+    P.check_runs(out["runs"][rows], out["run_count"][rows], out["idx"][rows], out["count"][rows], w.run_align)
+    print(w.name, stats)
+
+
 @pytest.mark.parametrize("base", [W.SMALL_FLAT, W.SMALL_MLA], ids=lambda w: w.name)
 def test_flat_short_window_partial_page(base):
     """Flat mode with K_swa < P and a cache that ends inside a page: the page holding a row's last
