@@ -474,15 +474,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 }
 
 // ============================================================================ block-wide top-k
-// Threshold T and tie count of the k largest keys among keys[0..n) (LDS), by four 8-bit radix
-// passes: the selection is {i : key_i > T} plus the first `take_eq` indices with key_i == T.
+// Threshold T and tie count of the k largest keys among keys[0..n) (LDS or global memory), by at
+// most four 8-bit radix passes: the selection is {i : key_i > T} plus the first `take_eq` indices
+// with key_i == T. (1 <= k <= n.)
+// hist[0..256) must be zero on entry (cleared before a barrier) and is zero again on return: the
+// scanning wave clears the bins as it reads them, before the barrier that publishes the boundary
+// bin. Two block barriers per pass. The boundary bin is published in the function's own LDS slots,
+// which a pass rewrites only after its counting barrier, when every wave has read the previous
+// pass's, so no barrier guards the reads and the caller may reuse its LDS right away. When the
+// boundary bin is taken whole (its count equals the rank still missing) and is not the bin of key
+// 0, the search stops there: T is the largest key below the bin and take_eq is 0, which selects
+// exactly the same set (every key equal to the exact threshold lies in that bin and is taken).
+// That needs every candidate key that shares the bin's digits to be among keys[0..n): when keys
+// holds only the candidates that share their top 11 bits, the stop is allowed from the second
+// pass on (first_exit = 1), whose bins fix 16 bits.
 template <int NT>
-__device__ void radix_threshold(const uint32_t* keys, int n, int k, uint32_t* hist, int* bc, uint32_t& T, int& take_eq) {
+__device__ void radix_threshold(const uint32_t* keys, int n, int k, uint32_t* hist, uint32_t& T, int& take_eq,
+                                int first_exit = 0) {
+  __shared__ int slot[3];  // boundary bin, keys in the bins above it, keys in it
   uint32_t prefix = 0, mask = 0;
   int rem = k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;
-    __syncthreads();
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
     for (int i = threadIdx.x; i < n; i += NT) {
       const uint32_t key = keys[i];
       if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
@@ -490,37 +503,44 @@ __device__ void radix_threshold(const uint32_t* keys, int n, int k, uint32_t* hi
     __syncthreads();
     if (threadIdx.x < 64) {
       const int l = threadIdx.x;
-      const uint32_t c0 = hist[4 * l], c1 = hist[4 * l + 1], c2 = hist[4 * l + 2], c3 = hist[4 * l + 3];
-      const uint32_t tot = c0 + c1 + c2 + c3;
+      const uint32_t c[4] = {hist[4 * l], hist[4 * l + 1], hist[4 * l + 2], hist[4 * l + 3]};
+#pragma unroll
+      for (int bq = 0; bq < 4; ++bq) hist[4 * l + bq] = 0;  // cleared for the next pass
+      const uint32_t tot = c[0] + c[1] + c[2] + c[3];
       uint32_t suf = tot;  // sum of totals of lanes >= l
       for (int o = 1; o < 64; o <<= 1) {
         const uint32_t x = __shfl_down(suf, o);
         if (l + o < 64) suf += x;
       }
       uint32_t ge = suf - tot;  // keys in bins above this lane's four
-      const uint32_t c[4] = {c0, c1, c2, c3};
       for (int bq = 3; bq >= 0; --bq) {
         const uint32_t above = ge;
         ge += c[bq];
         if (above < (uint32_t)rem && ge >= (uint32_t)rem) {
-          bc[0] = 4 * l + bq;
-          bc[1] = (int)above;
+          slot[0] = 4 * l + bq;
+          slot[1] = (int)above;
+          slot[2] = (int)c[bq];
         }
       }
     }
     __syncthreads();
-    const uint32_t d = (uint32_t)bc[0];
-    rem -= bc[1];
+    const uint32_t d = (uint32_t)slot[0];
+    rem -= slot[1];
     prefix |= d << shift;
     mask |= 0xFFu << shift;
-    __syncthreads();
+    if (pass >= first_exit && pass < 3 && slot[2] == rem && prefix != 0u) {  // (uniform) the bin is taken whole
+      T = prefix - 1u;
+      take_eq = 0;
+      return;
+    }
   }
   T = prefix;
   take_eq = rem;
 }
 
 // Visits, in index order, every selected index of keys[0..n) (key > T, or key == T among the
-// first take_eq such) and calls emit(rank, i). Returns the number selected.
+// first take_eq such) and calls emit(rank, i). Returns the number selected. The caller writes
+// wsum[0..2 NT/64) again only after a barrier.
 template <int NT, typename F>
 __device__ int select_compact(const uint32_t* keys, int n, uint32_t T, int take_eq, int* wsum, F&& emit) {
   constexpr int NW = NT / 64;
@@ -555,7 +575,8 @@ __device__ int select_compact(const uint32_t* keys, int n, uint32_t T, int take_
     if (sel) emit(base_out + sel_prefix + __popcll(bsel & lanemask_lt()), i);
     base_eq += eq_total;
     base_out += sel_total;
-    __syncthreads();
+    // (no barrier: the next chunk writes wsum[wv] after every wave has passed this chunk's second
+    // barrier, so after all reads of wsum[0..NW), and wsum[NW + wv] after its own first barrier)
   }
   return base_out;
 }
@@ -591,11 +612,12 @@ __global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_
   }
   const int n = (int)n_elig;
   uint32_t* keys = smem;
+  for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0u;
   for (int i = threadIdx.x; i < n; i += NT) keys[i] = page_keys[row * ld + ri.p_lo + i];
   __syncthreads();
   uint32_t T;
   int take;
-  radix_threshold<NT>(keys, n, g.M, hist, wsum, T, take);
+  radix_threshold<NT>(keys, n, g.M, hist, T, take);
   const int64_t p_lo = ri.p_lo;
   select_compact<NT>(keys, n, T, take, wsum, [&](int rank, int i) { out[rank] = (int32_t)(p_lo + i); });
 }
@@ -1100,6 +1122,7 @@ __device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h1
                                 uint32_t* hist, int* wsum, uint32_t& T, int& take_eq) {
   constexpr int NB = 1 << kSelHistBits;
   for (int i = threadIdx.x; i < NB; i += NT) h11[i] = 0;
+  for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;  // (for radix_threshold)
   if (threadIdx.x == 0) *gcnt = 0;
   __syncthreads();
   int nz = 0;
@@ -1119,8 +1142,8 @@ __device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h1
   for (int x = 0; x < NT / 64; ++x) n_valid += wsum[x];
   T = 0;
   take_eq = 0;
+  __syncthreads();  // wsum is reused below, and by the caller's compaction
   if (n_valid <= k) return n_valid;  // (uniform)
-  __syncthreads();  // wsum is reused below
   // bin b* holding the k-th largest key, and the count of keys in the bins above it
   if (threadIdx.x < 64) {
     constexpr int PER = NB / 64;
@@ -1162,8 +1185,8 @@ __device__ int global_threshold(const uint32_t* keys, int n, int k, uint32_t* h1
   __syncthreads();
   const int nb = *gcnt;
   __syncthreads();
-  if (nb <= kSelGatherCap) radix_threshold<NT>(sub, nb, rem, hist, wsum, T, take_eq);
-  else radix_threshold<NT>(keys, n, k, hist, wsum, T, take_eq);
+  if (nb <= kSelGatherCap) radix_threshold<NT>(sub, nb, rem, hist, T, take_eq, 1);
+  else radix_threshold<NT>(keys, n, k, hist, T, take_eq);
   return n_valid;
 }
 
@@ -1286,8 +1309,10 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
       for (int i = threadIdx.x; i < n_sel; i += NT) lpages[i] = pages[row * g.M + i];
     const int n = n_sel * g.P;
     const uint32_t* keys = GK ? fine_keys + row * ldf : smem;
-    if (!GK)
+    if (!GK) {
+      for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0;  // (for radix_threshold)
       for (int i = threadIdx.x; i < n; i += NT) smem[i] = fine_keys[row * ldf + i];
+    }
     __syncthreads();
     uint32_t T = 0;
     int take = 0;
@@ -1295,7 +1320,7 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
       global_threshold<NT>(keys, n, g.k_sparse, h11, gsub, gcnt, hist, wsum, T, take);
     } else {
       const int n_valid = block_count_nonzero(keys, n, wsum);
-      if (n_valid > g.k_sparse) radix_threshold<NT>(keys, n, g.k_sparse, hist, wsum, T, take);
+      if (n_valid > g.k_sparse) radix_threshold<NT>(keys, n, g.k_sparse, hist, T, take);
     }
     const int P = g.P;
     const int64_t p_lo = ri.p_lo;
@@ -1315,8 +1340,8 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
   emit_row<NT>(g, row, lidx, cnt, rstart, wsum, idx, count, runs, run_count);
 }
 
-// Block-wide scans over NT threads of one 32-bit value each.
-// Exclusive prefix (sum over threads < t) and suffix (sum over threads > t); wtot is LDS [NT/64].
+// Exclusive prefix over NT threads of one 32-bit value each (sum over threads < t); wtot is LDS
+// [NT/64]. One block barrier: the caller does not write wtot again before another barrier.
 template <int NT>
 __device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t* wtot) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -1331,13 +1356,40 @@ __device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t* wtot
   uint32_t base = 0;
 #pragma unroll
   for (int x = 0; x < NT / 64; ++x) base += x < wv ? wtot[x] : 0u;
-  __syncthreads();
   return base + inc - v;
 }
-template <int NT>
-__device__ __forceinline__ uint32_t block_excl_suffix(uint32_t v, uint32_t* wtot) {
+
+// One radix step over register-held keys: among keys with (key & mask) == prefix, find the digit
+// value d (BITS bits at SHIFT) such that fewer than rem keys have a larger digit and at least rem
+// have a digit >= d; then narrow prefix/mask to d and take the keys above it off rem. Returns
+// whether the bin of d is taken whole (its count equals the new rem) and is not the bin of key 0:
+// then the keys >= prefix are exactly the selection.
+// hist[0 .. 2^BITS) is all zero on entry and again on return (each thread clears the bins it owns
+// once it has read them). Three block barriers: after the counting, in the scan (a single-barrier
+// suffix: the next write of wtot comes after two more barriers) and after the boundary is found
+// (found is next written after two barriers, so no barrier guards its reads).
+template <int NT, int KPT, int SHIFT, int BITS>
+__device__ __forceinline__ bool radix_step(const uint32_t (&kv)[KPT], uint32_t& prefix, uint32_t& mask, int& rem,
+                                           uint32_t* hist, uint32_t* wtot, uint32_t* found) {
+  constexpr int NB = 1 << BITS;
+  constexpr int BPT = NB >= NT ? NB / NT : 1;  // bins per thread
+#pragma unroll
+  for (int e = 0; e < KPT; ++e)
+    if ((kv[e] & mask) == prefix) atomicAdd(&hist[(kv[e] >> SHIFT) & (NB - 1)], 1u);
+  __syncthreads();
+  const int b0 = threadIdx.x * BPT;
+  uint32_t c[BPT], own = 0;
+#pragma unroll
+  for (int u = 0; u < BPT; ++u) {
+    c[u] = b0 < NB ? hist[b0 + u] : 0u;
+    own += c[u];
+  }
+  if (b0 < NB)
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) hist[b0 + u] = 0u;
+  // keys in the bins of higher threads (wave suffix, then the wave totals of higher waves)
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  uint32_t inc = v;
+  uint32_t inc = own;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const uint32_t t = __shfl_down(inc, o);
@@ -1345,48 +1397,23 @@ __device__ __forceinline__ uint32_t block_excl_suffix(uint32_t v, uint32_t* wtot
   }
   if (lane == 0) wtot[wv] = inc;
   __syncthreads();
-  uint32_t base = 0;
+  uint32_t above = inc - own;
 #pragma unroll
-  for (int x = 0; x < NT / 64; ++x) base += x > wv ? wtot[x] : 0u;
-  __syncthreads();
-  return base + inc - v;
-}
-
-// One radix step over register-held keys: among keys with (key & mask) == prefix, find the digit
-// value d (BITS bits at SHIFT) such that fewer than rem keys have a larger digit and at least rem
-// have a digit >= d; then narrow prefix/mask to d and take the keys above it off rem.
-template <int NT, int KPT, int SHIFT, int BITS>
-__device__ __forceinline__ void radix_step(const uint32_t (&kv)[KPT], uint32_t& prefix, uint32_t& mask, int& rem,
-                                           uint32_t* hist, uint32_t* wtot, uint32_t* found) {
-  constexpr int NB = 1 << BITS;
-  constexpr int BPT = NB >= NT ? NB / NT : 1;  // bins per thread
-  for (int i = threadIdx.x; i < NB; i += NT) hist[i] = 0;
-  __syncthreads();
+  for (int x = 0; x < NT / 64; ++x) above += x > wv ? wtot[x] : 0u;
 #pragma unroll
-  for (int e = 0; e < KPT; ++e)
-    if ((kv[e] & mask) == prefix) atomicAdd(&hist[(kv[e] >> SHIFT) & (NB - 1)], 1u);
-  __syncthreads();
-  const int b0 = threadIdx.x * BPT;
-  uint32_t own = 0;
-  if (b0 < NB)
-#pragma unroll
-    for (int u = 0; u < BPT; ++u) own += hist[b0 + u];
-  uint32_t above = block_excl_suffix<NT>(own, wtot);  // keys in the bins of higher threads
-  if (b0 < NB)
-#pragma unroll
-    for (int u = BPT - 1; u >= 0; --u) {
-      const uint32_t c = hist[b0 + u];
-      if (above < (uint32_t)rem && above + c >= (uint32_t)rem) {
-        found[0] = (uint32_t)(b0 + u);
-        found[1] = above;
-      }
-      above += c;
+  for (int u = BPT - 1; u >= 0; --u) {
+    if (b0 < NB && above < (uint32_t)rem && above + c[u] >= (uint32_t)rem) {
+      found[0] = (uint32_t)(b0 + u);
+      found[1] = above;
+      found[2] = c[u];
     }
+    above += c[u];
+  }
   __syncthreads();
   rem -= (int)found[1];
   prefix |= found[0] << SHIFT;
   mask |= (uint32_t)(NB - 1) << SHIFT;
-  __syncthreads();
+  return found[2] == (uint32_t)rem && prefix != 0u;
 }
 
 // Same result as token_select_kernel for rows of at most NT * KPT candidates: each thread holds
@@ -1424,6 +1451,7 @@ __global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64
     if (!flat)
       for (int i = threadIdx.x; i < n_sel; i += NT) lpages[i] = pages[row * g.M + i];
     const int n = n_sel * g.P;
+    for (int i = threadIdx.x; i < 4096; i += NT) hist[i] = 0u;  // (radix_step keeps it cleared)
     const int i0 = (int)threadIdx.x * KPT;
     uint32_t kv[KPT];
     const uint32_t* src = fine_keys + row * ldf + i0;
@@ -1437,25 +1465,31 @@ __global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64
         for (int u = 0; u < 4; ++u) kv[e + u] = i0 + e + u < n ? src[e + u] : 0u;
       }
     }
-    uint32_t nz = 0;
+    int nz = 0;
 #pragma unroll
     for (int e = 0; e < KPT; ++e) nz += kv[e] != 0u;
-    const uint32_t n_valid = block_excl_prefix<NT>(nz, wtot) + nz;  // valid for the last thread only
-    __shared__ uint32_t found[2];
-    if (threadIdx.x == NT - 1) found[0] = n_valid;
-    __syncthreads();
-    const int nv = (int)found[0];
-    __syncthreads();
+    nz = wave_sum(nz);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = nz;
+    __syncthreads();  // the cleared histogram and the per-wave counts
+    int nv = 0;
+#pragma unroll
+    for (int x = 0; x < NT / 64; ++x) nv += wsum[x];
     uint32_t T = 0;
     int take = 0;
-    if (nv > g.k_sparse) {
+    if (nv > g.k_sparse) {  // (uniform)
+      __shared__ uint32_t found[3];
       uint32_t prefix = 0, mask = 0;
       int rem = g.k_sparse;
-      radix_step<NT, KPT, 20, 12>(kv, prefix, mask, rem, hist, wtot, found);
-      radix_step<NT, KPT, 8, 12>(kv, prefix, mask, rem, hist, wtot, found);
-      radix_step<NT, KPT, 0, 8>(kv, prefix, mask, rem, hist, wtot, found);
-      T = prefix;
-      take = rem;
+      bool whole = radix_step<NT, KPT, 20, 12>(kv, prefix, mask, rem, hist, wtot, found);
+      if (!whole) whole = radix_step<NT, KPT, 8, 12>(kv, prefix, mask, rem, hist, wtot, found);
+      if (whole) {  // the keys >= prefix are the selection
+        T = prefix - 1u;
+        take = 0;
+      } else {
+        radix_step<NT, KPT, 0, 8>(kv, prefix, mask, rem, hist, wtot, found);
+        T = prefix;
+        take = rem;
+      }
     }
     // ordered compaction: selected = key > T, or key == T among the first `take` such (index order)
     uint32_t gt = 0, eq = 0;
