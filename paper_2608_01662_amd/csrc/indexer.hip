@@ -1044,13 +1044,19 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
   // contiguous slice [x E, x E + E) of the list; one block-wide prefix of the per-thread start
   // counts numbers the runs, and each run is stored as one 8-byte (start, length) pair.
   const int C = g.C;
+  const bool c2 = (C & (C - 1)) == 0;  // (uniform) multiples of C by a mask
+  auto starts = [&](int i, int32_t s) {
+    return i == 0 || s != lidx[i - 1] + 1 || (c2 ? (s & (C - 1)) == 0 : (s % C) == 0);
+  };
   const int E = (cnt + NT - 1) / NT;
   const int b = (int)threadIdx.x * E, e = b + E < cnt ? b + E : cnt;
   int mine = 0;
-  for (int i = b; i < e; ++i) {
-    const int32_t s = lidx[i];
-    mine += (i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0) ? 1 : 0;
-  }
+  uint64_t fl = 0;  // start flags of the slice's first 64 entries
+  for (int i = b; i < e; ++i)
+    if (starts(i, lidx[i])) {
+      ++mine;
+      fl |= i - b < 64 ? 1ull << (i - b) : 0ull;
+    }
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   int inc = mine;
 #pragma unroll
@@ -1067,9 +1073,11 @@ __device__ void emit_row(const IndexGeom& g, int64_t row, const int32_t* lidx, i
     r += x < wv ? v : 0;
     nr += v;
   }
-  for (int i = b; i < e; ++i) {
-    const int32_t s = lidx[i];
-    if (i == 0 || s != lidx[i - 1] + 1 || (s % C) == 0) rstart[r++] = i;
+  if (E <= 64) {  // (uniform)
+    for (; fl != 0; fl &= fl - 1) rstart[r++] = b + __ffsll((unsigned long long)fl) - 1;
+  } else {
+    for (int i = b; i < e; ++i)
+      if (starts(i, lidx[i])) rstart[r++] = i;
   }
   __syncthreads();
   int2* rrow = reinterpret_cast<int2*>(runs + row * (int64_t)k_cap * 2);  // 8-byte aligned (checked on the host)
@@ -1323,11 +1331,14 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
       if (n_valid > g.k_sparse) radix_threshold<NT>(keys, n, g.k_sparse, hist, T, take);
     }
     const int P = g.P;
+    const bool p2 = (P & (P - 1)) == 0;  // (uniform) slot -> page by a shift
+    const int lgP = __ffs(P) - 1;
     const int64_t p_lo = ri.p_lo;
     const int ks = g.k_sink;
     auto emit = [&](int rank, int i) {
-      const int64_t page = flat ? p_lo + i / P : (int64_t)lpages[i / P];
-      lidx[ks + rank] = (int32_t)(page * P + i % P);
+      const int pi = p2 ? i >> lgP : i / P;
+      const int64_t page = flat ? p_lo + pi : (int64_t)lpages[pi];
+      lidx[ks + rank] = (int32_t)(page * P + (i - pi * P));
     };
     int n_sp;
     if constexpr (GK) n_sp = global_compact<NT>(keys, n, T, take, wsum, emit);
@@ -1359,78 +1370,152 @@ __device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t* wtot
   return base + inc - v;
 }
 
-// One radix step over register-held keys: among keys with (key & mask) == prefix, find the digit
-// value d (BITS bits at SHIFT) such that fewer than rem keys have a larger digit and at least rem
-// have a digit >= d; then narrow prefix/mask to d and take the keys above it off rem. Returns
-// whether the bin of d is taken whole (its count equals the new rem) and is not the bin of key 0:
-// then the keys >= prefix are exactly the selection.
-// hist[0 .. 2^BITS) is all zero on entry and again on return (each thread clears the bins it owns
-// once it has read them). Three block barriers: after the counting, in the scan (a single-barrier
-// suffix: the next write of wtot comes after two more barriers) and after the boundary is found
-// (found is next written after two barriers, so no barrier guards its reads).
-template <int NT, int KPT, int SHIFT, int BITS>
-__device__ __forceinline__ bool radix_step(const uint32_t (&kv)[KPT], uint32_t& prefix, uint32_t& mask, int& rem,
-                                           uint32_t* hist, uint32_t* wtot, uint32_t* found) {
-  constexpr int NB = 1 << BITS;
-  constexpr int BPT = NB >= NT ? NB / NT : 1;  // bins per thread
-#pragma unroll
-  for (int e = 0; e < KPT; ++e)
-    if ((kv[e] & mask) == prefix) atomicAdd(&hist[(kv[e] >> SHIFT) & (NB - 1)], 1u);
-  __syncthreads();
-  const int b0 = threadIdx.x * BPT;
-  uint32_t c[BPT], own = 0;
-#pragma unroll
-  for (int u = 0; u < BPT; ++u) {
-    c[u] = b0 < NB ? hist[b0 + u] : 0u;
-    own += c[u];
-  }
-  if (b0 < NB)
-#pragma unroll
-    for (int u = 0; u < BPT; ++u) hist[b0 + u] = 0u;
-  // keys in the bins of higher threads (wave suffix, then the wave totals of higher waves)
+// Threshold of the k largest non-zero keys of a row held in registers (KPT per thread): T and take
+// such that the selection is every key > T and the first `take` keys == T (position order), as
+// radix_threshold gives. Each pass counts the keys still in question, those in [lo, hi], into
+// kRangeBins bins that split that interval evenly (bin = (key - lo) * scale / 2^32, non-decreasing
+// in the key), so one row's scores spread over the bins however closely they cluster, and one
+// wave finds the bin holding the rem-th largest key. At most 64 keys in that bin: they are gathered
+// into LDS and that wave ranks them against each other. More: the next pass narrows [lo, hi] to the
+// smallest and largest key of the bin. A bin spans at most (hi - lo + 1) / 511 + 2 values, so the
+// fourth pass sees fewer than kRangeBins values and gives each value its own bin. The scan and the
+// ranking are per-row work done once, by wave 0: with several rows per CU the other waves' wait at
+// the barrier costs less than eight waves repeating them. lo >= 1 (the smallest non-zero key), so
+// key - lo <= hi - lo excludes the zero keys (no candidate) as well as keys outside [lo, hi].
+// hist[0 .. 2 kRangeBins) is zero on entry; aux[0] (gathered count) is 0, aux[6], aux[8] (bin
+// minimum slots) are ~0u and aux[7], aux[9] (bin maximum slots) 0. Needs rem in [1, keys in play].
+constexpr int kRangeBins = 512;
+constexpr int kRangeAux = 10;
+template <int NT, int KPT>
+__device__ __forceinline__ void range_threshold(const uint32_t (&kv)[KPT], uint32_t lo, uint32_t hi, int rem,
+                                                uint32_t* hist, uint32_t* cand, uint32_t* aux, uint32_t& T,
+                                                int& take) {
+  static_assert(kRangeBins == 8 * 64, "a lane scans eight bins");
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  uint32_t inc = own;
+  for (int pass = 0; pass < 4; ++pass) {
+    uint32_t* hb = hist + kRangeBins * (pass & 1);
+    if (pass > 0)  // the other buffer was last read before the previous pass's second barrier
+      for (int i = threadIdx.x; i < kRangeBins; i += NT) hist[kRangeBins * ((pass + 1) & 1) + i] = 0u;
+    const uint32_t range = hi - lo;
+    const bool direct = range < (uint32_t)kRangeBins;  // one value per bin
+    // scale <= 512 * 2^32 / (range + 1), so that bins stay below 512 (range >= 512: it fits 32 bits)
+    const uint32_t scale = direct ? 0u : (uint32_t)floor(2199023255552.0 / ((double)range + 1.0)) - 1u;
+    if (direct) {
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t t = __shfl_down(inc, o);
-    if (lane + o < 64) inc += t;
-  }
-  if (lane == 0) wtot[wv] = inc;
-  __syncthreads();
-  uint32_t above = inc - own;
+      for (int e = 0; e < KPT; ++e)
+        if (kv[e] - lo <= range) atomicAdd(&hb[kv[e] - lo], 1u);
+    } else {
 #pragma unroll
-  for (int x = 0; x < NT / 64; ++x) above += x > wv ? wtot[x] : 0u;
-#pragma unroll
-  for (int u = BPT - 1; u >= 0; --u) {
-    if (b0 < NB && above < (uint32_t)rem && above + c[u] >= (uint32_t)rem) {
-      found[0] = (uint32_t)(b0 + u);
-      found[1] = above;
-      found[2] = c[u];
+      for (int e = 0; e < KPT; ++e)
+        if (kv[e] - lo <= range) atomicAdd(&hb[__umulhi(kv[e] - lo, scale)], 1u);
     }
-    above += c[u];
+    __syncthreads();
+    if (wv == 0) {
+      // lane l holds bins 8 l .. 8 l + 7; keys in the bins of higher lanes by a suffix sum
+      const u32x4 ca = reinterpret_cast<const u32x4*>(hb)[2 * lane];
+      const u32x4 cb = reinterpret_cast<const u32x4*>(hb)[2 * lane + 1];
+      const uint32_t c[8] = {ca.x, ca.y, ca.z, ca.w, cb.x, cb.y, cb.z, cb.w};
+      uint32_t tot = 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) tot += c[u];
+      uint32_t suf = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_down(suf, o);
+        if (lane + o < 64) suf += x;
+      }
+      uint32_t above = suf - tot;
+#pragma unroll
+      for (int u = 7; u >= 0; --u) {
+        if (above < (uint32_t)rem && above + c[u] >= (uint32_t)rem) {
+          aux[1] = 8 * lane + u;
+          aux[2] = above;
+          aux[3] = c[u];
+        }
+        above += c[u];
+      }
+      if (lane == 0) {  // the other parity's bin extrema were last read before this pass's first barrier
+        aux[6 + 2 * ((pass + 1) & 1)] = ~0u;
+        aux[7 + 2 * ((pass + 1) & 1)] = 0u;
+      }
+    }
+    __syncthreads();
+    const uint32_t bb = aux[1], bc = aux[3];
+    rem -= (int)aux[2];
+    if (direct) {  // (uniform) the bin is one key value
+      T = lo + bb;
+      take = rem;
+      return;
+    }
+    auto in_bin = [&](uint32_t key) { return key - lo <= range && __umulhi(key - lo, scale) == bb; };
+    if (bc <= 64u) {  // (uniform)
+#pragma unroll
+      for (int e = 0; e < KPT; ++e)
+        if (in_bin(kv[e])) cand[atomicAdd(&aux[0], 1u)] = kv[e];
+      __syncthreads();
+      if (wv == 0) {
+        // lane l ranks candidate l against all of them: the rem-th largest value has fewer than rem
+        // candidates above it and at least rem at or above it; take = rem - (candidates above it)
+        const int nb = (int)bc;
+        const uint32_t x = cand[lane];  // (lanes >= nb read stale entries and are ignored)
+        int gt = 0, ge = 0;
+        for (int j = 0; j < nb; j += 4) {
+          const u32x4 c4 = *reinterpret_cast<const u32x4*>(cand + j);  // (the same address in every lane)
+          const uint32_t cc[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const bool in = j + u < nb;
+            gt += in && cc[u] > x;
+            ge += in && cc[u] >= x;
+          }
+        }
+        const bool hit = lane < nb && gt < rem && ge >= rem;
+        if (hit && lane == __ffsll(__ballot(hit)) - 1) {
+          aux[4] = x;
+          aux[5] = (uint32_t)(rem - gt);
+        }
+      }
+      __syncthreads();
+      T = aux[4];
+      take = (int)aux[5];
+      return;
+    }
+    // narrow [lo, hi] to the boundary bin's keys
+    uint32_t mn = ~0u, mx = 0u;
+#pragma unroll
+    for (int e = 0; e < KPT; ++e)
+      if (in_bin(kv[e])) {
+        mn = kv[e] < mn ? kv[e] : mn;
+        mx = kv[e] > mx ? kv[e] : mx;
+      }
+    mn = wave_reduce_u32(mn, [](uint32_t p, uint32_t q) { return p < q ? p : q; });
+    mx = wave_reduce_u32(mx, [](uint32_t p, uint32_t q) { return p > q ? p : q; });
+    uint32_t* mm = aux + 6 + 2 * (pass & 1);
+    if (lane == 0) {
+      atomicMin(&mm[0], mn);
+      atomicMax(&mm[1], mx);
+    }
+    __syncthreads();
+    lo = mm[0];
+    hi = mm[1];
   }
-  __syncthreads();
-  rem -= (int)found[1];
-  prefix |= found[0] << SHIFT;
-  mask |= (uint32_t)(NB - 1) << SHIFT;
-  return found[2] == (uint32_t)rem && prefix != 0u;
+  T = lo;  // (not reached: the fourth pass is direct)
+  take = rem;
 }
 
-// Same result as token_select_kernel for rows of at most NT * KPT candidates: each thread holds
-// KPT consecutive keys in registers. The threshold takes three radix steps of 12, 12 and 8 bits
-// (the first spreads the scores of one row over many bins, where an 8-bit exponent digit would
-// put nearly all of them into one or two and serialize the LDS atomics); the ordered compaction
-// is one block-wide scan of (count above T, count equal to T) per thread.
+// Rows of at most 16 keys per thread run eight waves per SIMD (four rows of 512 threads per CU):
+// the registers are capped so that the small LDS footprint is what bounds the rows a CU holds.
 template <int NT, int KPT>
-__global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64_t n_rows,
-                                                              const uint32_t* __restrict__ fine_keys, int64_t ldf,
-                                                              const int32_t* __restrict__ pages,
-                                                              int32_t* __restrict__ idx, int32_t* __restrict__ count,
-                                                              int32_t* __restrict__ runs, int32_t* __restrict__ run_count) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(KPT <= 16 ? 8 : 1))) void token_select_reg_kernel(
+    IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ fine_keys, int64_t ldf, const int32_t* __restrict__ pages,
+    int32_t* __restrict__ idx, int32_t* __restrict__ count, int32_t* __restrict__ runs, int32_t* __restrict__ run_count) {
   extern __shared__ int32_t dyn[];  // lidx [k_cap], rstart [k_cap], lpages [M]
-  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t hist[2 * kRangeBins];
+  __shared__ __align__(16) uint32_t cand[64];
+  __shared__ uint32_t aux[kRangeAux];
   __shared__ uint32_t wtot[NT / 64 + 2];
   __shared__ int wsum[NT / 64 + 2];
+  __shared__ uint32_t wlo[NT / 64], whi[NT / 64];
   const int k_cap = g.k_sink + g.k_swa + g.k_sparse;
   int32_t* lidx = dyn;
   int32_t* rstart = dyn + k_cap;
@@ -1451,7 +1536,8 @@ __global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64
     if (!flat)
       for (int i = threadIdx.x; i < n_sel; i += NT) lpages[i] = pages[row * g.M + i];
     const int n = n_sel * g.P;
-    for (int i = threadIdx.x; i < 4096; i += NT) hist[i] = 0u;  // (radix_step keeps it cleared)
+    for (int i = threadIdx.x; i < 2 * kRangeBins; i += NT) hist[i] = 0u;
+    if (threadIdx.x < kRangeAux) aux[threadIdx.x] = (threadIdx.x == 6 || threadIdx.x == 8) ? ~0u : 0u;
     const int i0 = (int)threadIdx.x * KPT;
     uint32_t kv[KPT];
     const uint32_t* src = fine_keys + row * ldf + i0;
@@ -1465,55 +1551,62 @@ __global__ __launch_bounds__(NT) void token_select_reg_kernel(IndexGeom g, int64
         for (int u = 0; u < 4; ++u) kv[e + u] = i0 + e + u < n ? src[e + u] : 0u;
       }
     }
-    int nz = 0;
+    // non-zero keys (the candidates), their smallest and their largest
+    uint32_t nz = 0, mn = ~0u, mx = 0u;
 #pragma unroll
-    for (int e = 0; e < KPT; ++e) nz += kv[e] != 0u;
-    nz = wave_sum(nz);
-    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = nz;
-    __syncthreads();  // the cleared histogram and the per-wave counts
+    for (int e = 0; e < KPT; ++e)
+      if (kv[e] != 0u) {
+        ++nz;
+        mn = kv[e] < mn ? kv[e] : mn;
+        mx = kv[e] > mx ? kv[e] : mx;
+      }
+    nz = wave_reduce_u32(nz, [](uint32_t p, uint32_t q) { return p + q; });
+    mn = wave_reduce_u32(mn, [](uint32_t p, uint32_t q) { return p < q ? p : q; });
+    mx = wave_reduce_u32(mx, [](uint32_t p, uint32_t q) { return p > q ? p : q; });
+    if ((threadIdx.x & 63) == 0) {
+      wsum[threadIdx.x >> 6] = (int)nz;
+      wlo[threadIdx.x >> 6] = mn;
+      whi[threadIdx.x >> 6] = mx;
+    }
+    __syncthreads();  // the cleared histograms, aux and the per-wave counts
     int nv = 0;
+    uint32_t lo = ~0u, hi = 0u;
 #pragma unroll
-    for (int x = 0; x < NT / 64; ++x) nv += wsum[x];
+    for (int x = 0; x < NT / 64; ++x) {
+      nv += wsum[x];
+      lo = wlo[x] < lo ? wlo[x] : lo;
+      hi = whi[x] > hi ? whi[x] : hi;
+    }
     uint32_t T = 0;
     int take = 0;
-    if (nv > g.k_sparse) {  // (uniform)
-      __shared__ uint32_t found[3];
-      uint32_t prefix = 0, mask = 0;
-      int rem = g.k_sparse;
-      bool whole = radix_step<NT, KPT, 20, 12>(kv, prefix, mask, rem, hist, wtot, found);
-      if (!whole) whole = radix_step<NT, KPT, 8, 12>(kv, prefix, mask, rem, hist, wtot, found);
-      if (whole) {  // the keys >= prefix are the selection
-        T = prefix - 1u;
-        take = 0;
-      } else {
-        radix_step<NT, KPT, 0, 8>(kv, prefix, mask, rem, hist, wtot, found);
-        T = prefix;
-        take = rem;
-      }
-    }
-    // ordered compaction: selected = key > T, or key == T among the first `take` such (index order)
+    if (nv > g.k_sparse) range_threshold<NT, KPT>(kv, lo, hi, g.k_sparse, hist, cand, aux, T, take);  // (uniform)
+    // ordered compaction: selected = key > T, or key == T among the first `take` such (index order);
+    // with T = 0 (every candidate selected) take is 0, so counting the zero keys as ties is harmless
     uint32_t gt = 0, eq = 0;
 #pragma unroll
     for (int e = 0; e < KPT; ++e) {
       gt += kv[e] > T;
-      eq += kv[e] == T && kv[e] != 0u;
+      eq += kv[e] == T;
     }
     const uint32_t pre = block_excl_prefix<NT>(gt | (eq << 16), wtot);
     const int eq_before = (int)(pre >> 16);
     int out = (int)(pre & 0xFFFFu) + (eq_before < take ? eq_before : take);
     int eqr = eq_before;
     const int P = g.P, ks = g.k_sink;
+    auto pos_of = [&](int i) {
+      const int pi = i / P;
+      const int64_t page = flat ? ri.p_lo + pi : (int64_t)lpages[pi];
+      return (int32_t)(page * P + (i - pi * P));
+    };
+    if (gt + eq > 0) {  // (P is a multiple of 32: a thread's KPT <= 32 keys lie in one page)
+      const int32_t base = KPT <= 32 || P % KPT == 0 ? pos_of(i0) : 0;
 #pragma unroll
-    for (int e = 0; e < KPT; ++e) {
-      const uint32_t key = kv[e];
-      const bool is_eq = key == T && key != 0u;
-      const bool sel = key > T || (is_eq && eqr < take);
-      eqr += is_eq;
-      if (sel) {
-        const int i = i0 + e;
-        const int64_t page = flat ? ri.p_lo + i / P : (int64_t)lpages[i / P];
-        lidx[ks + out] = (int32_t)(page * P + i % P);
-        ++out;
+      for (int e = 0; e < KPT; ++e) {
+        const uint32_t key = kv[e];
+        const bool is_eq = key == T;
+        const bool sel = key > T || (is_eq && eqr < take);
+        eqr += is_eq;
+        if (sel) lidx[ks + out++] = KPT <= 32 || P % KPT == 0 ? base + e : pos_of(i0 + e);
       }
     }
     const int n_sp = nv > g.k_sparse ? g.k_sparse : nv;

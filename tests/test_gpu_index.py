@@ -345,6 +345,39 @@ def test_designed_inputs_select_latest():
             assert np.array_equal(S[w.k_sink:S.size - w.k_swa], want), (mode, t)
 
 
+@pytest.mark.parametrize("mode", ["two_values_outliers", "dense_cluster_outliers"])
+def test_selection_clustered_scores(mode):
+    """Designed scores for the selection's range histograms (Eq. 7 then Eq. 6): every head's query
+    is +e_0 and w = 1, so a token's score is H times component 0 of its key. Every 61st token is
+    an outlier (key 32768), which stretches the key range so far that the other scores share one or
+    a few of the first pass's 512 bins:
+      * two_values_outliers: the rest alternate between 1.0 and 1.0078125; the boundary bin holds
+        hundreds of keys, the next pass narrows to those two values and then to ties of one value
+        (the direct pass, take = rank still missing);
+      * dense_cluster_outliers: the rest take the 128 bf16 values of [1, 2) in turn; the first
+        pass's boundary bin holds several values with 64 ties each, the next pass gives each value
+        its own bin and ranks the boundary value's ties.
+    Flat indexing at L = 8192 (K_sparse = 256, every row's candidates in registers); sampled rows
+    against the oracle, ties to the earlier position."""
+    from dataclasses import replace
+    w = replace(W.L2K_MQA, name=f"clustered_{mode}", keep_pages=0, seq_len=8192)
+    n, H, d = w.seq_len, w.n_heads, w.head_dim
+    q = np.zeros((n, H, d), np.float32)
+    q[:, :, 0] = 1.0
+    kb = np.zeros((n, d), np.uint16)
+    s = np.arange(n)
+    kb[:, 0] = 0x3F80 + (s % 2) if mode == "two_values_outliers" else 0x3F80 + (s % 128)
+    kb[s % 61 == 5, 0] = 0x4700
+    inp = dict(q=synth.to_bf16_bits(q), w=np.ones((n, H), np.float32), k=kb, k_scale=None)
+    out, _ = _run_prefill(w, inp, pages=False)
+    rows = sorted(set(range(w.k_sink + w.k_swa + w.k_sparse, n, 151)) | {n - 1})
+    res = _oracle_rows(w, inp, rows)
+    stats = P.check_index_rows(w, rows, out["idx"][rows], out["count"][rows], None, res)
+    P.check_runs(out["runs"][rows], out["run_count"][rows], out["idx"][rows], out["count"][rows], w.run_align)
+    assert stats["exact"] == stats["rows"], stats   # exact ties: both sides take the earliest positions
+    print(mode, stats)
+
+
 def test_fine_scoring_orders_every_fp8_code():
     """The fine stage widens fp8 keys to bf16 on the GPU. Designed case: each eligible token carries
     one distinct e4m3fn code in component 0 (all 254 non-NaN codes, in seeded random positions),
