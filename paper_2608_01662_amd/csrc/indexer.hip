@@ -593,6 +593,191 @@ __device__ int block_count_nonzero(const uint32_t* keys, int n, int* wsum) {
   return tot;
 }
 
+// Exclusive prefix over NT threads of one value each (sum over threads < t); wtot is LDS [NT/64].
+// One block barrier: the caller does not write wtot again before another barrier.
+template <int NT, typename V>
+__device__ __forceinline__ V block_excl_prefix(V v, V* wtot) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  V inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const V t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
+  }
+  if (lane == 63) wtot[wv] = inc;
+  __syncthreads();
+  V base = 0;
+#pragma unroll
+  for (int x = 0; x < NT / 64; ++x) base += x < wv ? wtot[x] : V(0);
+  return base + inc - v;
+}
+
+// Number, smallest and largest of the non-zero keys of the block (each(fn) visits this thread's
+// keys). One block barrier, which also publishes whatever the caller wrote to LDS before the call;
+// wsum, wlo, whi ([NT/64] each) are next written by the caller only after another barrier.
+template <int NT, typename Each>
+__device__ __forceinline__ void block_nonzero_range(Each&& each, int* wsum, uint32_t* wlo, uint32_t* whi, int& nv,
+                                                    uint32_t& lo, uint32_t& hi) {
+  uint32_t nz = 0, mn = ~0u, mx = 0u;
+  each([&](uint32_t key) {
+    if (key != 0u) {
+      ++nz;
+      mn = key < mn ? key : mn;
+      mx = key > mx ? key : mx;
+    }
+  });
+  nz = wave_reduce_u32(nz, [](uint32_t p, uint32_t q) { return p + q; });
+  mn = wave_reduce_u32(mn, [](uint32_t p, uint32_t q) { return p < q ? p : q; });
+  mx = wave_reduce_u32(mx, [](uint32_t p, uint32_t q) { return p > q ? p : q; });
+  if ((threadIdx.x & 63) == 0) {
+    wsum[threadIdx.x >> 6] = (int)nz;
+    wlo[threadIdx.x >> 6] = mn;
+    whi[threadIdx.x >> 6] = mx;
+  }
+  __syncthreads();
+  nv = 0;
+  lo = ~0u;
+  hi = 0u;
+#pragma unroll
+  for (int x = 0; x < NT / 64; ++x) {
+    nv += wsum[x];
+    lo = wlo[x] < lo ? wlo[x] : lo;
+    hi = whi[x] > hi ? whi[x] : hi;
+  }
+}
+
+// Threshold of the k largest non-zero keys of a row held in registers (KPT per thread): T and take
+// such that the selection is every key > T and the first `take` keys == T (position order), as
+// radix_threshold gives. Each pass counts the keys still in question, those in [lo, hi], into
+// kRangeBins bins that split that interval evenly (bin = (key - lo) * scale / 2^32, non-decreasing
+// in the key), so one row's scores spread over the bins however closely they cluster, and one
+// wave finds the bin holding the rem-th largest key. At most 64 keys in that bin: they are gathered
+// into LDS and that wave ranks them against each other. More: the next pass narrows [lo, hi] to the
+// smallest and largest key of the bin. A bin spans at most (hi - lo + 1) / 511 + 2 values, so the
+// fourth pass sees fewer than kRangeBins values and gives each value its own bin. The scan and the
+// ranking are per-row work done once, by wave 0: with several rows per CU the other waves' wait at
+// the barrier costs less than eight waves repeating them. lo >= 1 (the smallest non-zero key), so
+// key - lo <= hi - lo excludes the zero keys (no candidate) as well as keys outside [lo, hi].
+// hist[0 .. 2 kRangeBins) is zero on entry; aux[0] (gathered count) is 0, aux[6], aux[8] (bin
+// minimum slots) are ~0u and aux[7], aux[9] (bin maximum slots) 0. Needs rem in [1, keys in play].
+constexpr int kRangeBins = 512;
+constexpr int kRangeAux = 10;
+// each(fn) calls fn(key) for every key this thread holds.
+template <int NT, typename Each>
+__device__ __forceinline__ void range_threshold(Each&& each, uint32_t lo, uint32_t hi, int rem, uint32_t* hist,
+                                                uint32_t* cand, uint32_t* aux, uint32_t& T, int& take) {
+  static_assert(kRangeBins == 8 * 64, "a lane scans eight bins");
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int pass = 0; pass < 4; ++pass) {
+    uint32_t* hb = hist + kRangeBins * (pass & 1);
+    if (pass > 0)  // the other buffer was last read before the previous pass's second barrier
+      for (int i = threadIdx.x; i < kRangeBins; i += NT) hist[kRangeBins * ((pass + 1) & 1) + i] = 0u;
+    const uint32_t range = hi - lo;
+    const bool direct = range < (uint32_t)kRangeBins;  // one value per bin
+    // scale <= 512 * 2^32 / (range + 1), so that bins stay below 512 (range >= 512: it fits 32 bits)
+    const uint32_t scale = direct ? 0u : (uint32_t)floor(2199023255552.0 / ((double)range + 1.0)) - 1u;
+    if (direct)
+      each([&](uint32_t key) {
+        if (key - lo <= range) atomicAdd(&hb[key - lo], 1u);
+      });
+    else
+      each([&](uint32_t key) {
+        if (key - lo <= range) atomicAdd(&hb[__umulhi(key - lo, scale)], 1u);
+      });
+    __syncthreads();
+    if (wv == 0) {
+      // lane l holds bins 8 l .. 8 l + 7; keys in the bins of higher lanes by a suffix sum
+      const u32x4 ca = reinterpret_cast<const u32x4*>(hb)[2 * lane];
+      const u32x4 cb = reinterpret_cast<const u32x4*>(hb)[2 * lane + 1];
+      const uint32_t c[8] = {ca.x, ca.y, ca.z, ca.w, cb.x, cb.y, cb.z, cb.w};
+      uint32_t tot = 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) tot += c[u];
+      uint32_t suf = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_down(suf, o);
+        if (lane + o < 64) suf += x;
+      }
+      uint32_t above = suf - tot;
+#pragma unroll
+      for (int u = 7; u >= 0; --u) {
+        if (above < (uint32_t)rem && above + c[u] >= (uint32_t)rem) {
+          aux[1] = 8 * lane + u;
+          aux[2] = above;
+          aux[3] = c[u];
+        }
+        above += c[u];
+      }
+      if (lane == 0) {  // the other parity's bin extrema were last read before this pass's first barrier
+        aux[6 + 2 * ((pass + 1) & 1)] = ~0u;
+        aux[7 + 2 * ((pass + 1) & 1)] = 0u;
+      }
+    }
+    __syncthreads();
+    const uint32_t bb = aux[1], bc = aux[3];
+    rem -= (int)aux[2];
+    if (direct) {  // (uniform) the bin is one key value
+      T = lo + bb;
+      take = rem;
+      return;
+    }
+    auto in_bin = [&](uint32_t key) { return key - lo <= range && __umulhi(key - lo, scale) == bb; };
+    if (bc <= 64u) {  // (uniform)
+      each([&](uint32_t key) {
+        if (in_bin(key)) cand[atomicAdd(&aux[0], 1u)] = key;
+      });
+      __syncthreads();
+      if (wv == 0) {
+        // lane l ranks candidate l against all of them: the rem-th largest value has fewer than rem
+        // candidates above it and at least rem at or above it; take = rem - (candidates above it)
+        const int nb = (int)bc;
+        const uint32_t x = cand[lane];  // (lanes >= nb read stale entries and are ignored)
+        int gt = 0, ge = 0;
+        for (int j = 0; j < nb; j += 4) {
+          const u32x4 c4 = *reinterpret_cast<const u32x4*>(cand + j);  // (the same address in every lane)
+          const uint32_t cc[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const bool in = j + u < nb;
+            gt += in && cc[u] > x;
+            ge += in && cc[u] >= x;
+          }
+        }
+        const bool hit = lane < nb && gt < rem && ge >= rem;
+        if (hit && lane == __ffsll(__ballot(hit)) - 1) {
+          aux[4] = x;
+          aux[5] = (uint32_t)(rem - gt);
+        }
+      }
+      __syncthreads();
+      T = aux[4];
+      take = (int)aux[5];
+      return;
+    }
+    // narrow [lo, hi] to the boundary bin's keys
+    uint32_t mn = ~0u, mx = 0u;
+    each([&](uint32_t key) {
+      if (in_bin(key)) {
+        mn = key < mn ? key : mn;
+        mx = key > mx ? key : mx;
+      }
+    });
+    mn = wave_reduce_u32(mn, [](uint32_t p, uint32_t q) { return p < q ? p : q; });
+    mx = wave_reduce_u32(mx, [](uint32_t p, uint32_t q) { return p > q ? p : q; });
+    uint32_t* mm = aux + 6 + 2 * (pass & 1);
+    if (lane == 0) {
+      atomicMin(&mm[0], mn);
+      atomicMax(&mm[1], mx);
+    }
+    __syncthreads();
+    lo = mm[0];
+    hi = mm[1];
+  }
+  T = lo;  // (not reached: the fourth pass is direct)
+  take = rem;
+}
+
 // ============================================================================ Stage 1: page top-M
 // Eq. (10): P_t = the M eligible pages of largest coarse score (ties to the smaller page),
 // written in ascending page order and padded with -1. All eligible pages when there are <= M.
@@ -600,8 +785,12 @@ template <int NT>
 __global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ page_keys,
                                                          int64_t ld, int32_t* __restrict__ pages) {
   extern __shared__ uint32_t smem[];
-  __shared__ uint32_t hist[256];
-  __shared__ int wsum[2 * NT / 64 + 2];
+  __shared__ uint32_t hist[2 * kRangeBins];
+  __shared__ __align__(16) uint32_t cand[64];
+  __shared__ uint32_t aux[kRangeAux];
+  __shared__ uint64_t wtot[NT / 64];
+  __shared__ int wsum[NT / 64];
+  __shared__ uint32_t wlo[NT / 64], whi[NT / 64];
   const int64_t row = blockIdx.x;
   const RowInfo ri = row_info(g, row);
   int32_t* out = pages + row * g.M;
@@ -612,14 +801,40 @@ __global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_
   }
   const int n = (int)n_elig;
   uint32_t* keys = smem;
-  for (int i = threadIdx.x; i < 256; i += NT) hist[i] = 0u;
+  for (int i = threadIdx.x; i < 2 * kRangeBins; i += NT) hist[i] = 0u;
+  if (threadIdx.x < kRangeAux) aux[threadIdx.x] = (threadIdx.x == 6 || threadIdx.x == 8) ? ~0u : 0u;
   for (int i = threadIdx.x; i < n; i += NT) keys[i] = page_keys[row * ld + ri.p_lo + i];
   __syncthreads();
-  uint32_t T;
-  int take;
-  radix_threshold<NT>(keys, n, g.M, hist, T, take);
-  const int64_t p_lo = ri.p_lo;
-  select_compact<NT>(keys, n, T, take, wsum, [&](int rank, int i) { out[rank] = (int32_t)(p_lo + i); });
+  // thread x holds the contiguous slice [x E, x E + E) of the row's page keys
+  const int E = (n + NT - 1) / NT;
+  const int b = (int)threadIdx.x * E, e = b + E < n ? b + E : n;
+  auto each = [&](auto&& fn) {
+    for (int i = b; i < e; ++i) fn(keys[i]);
+  };
+  int nv;
+  uint32_t lo, hi;
+  block_nonzero_range<NT>(each, wsum, wlo, whi, nv, lo, hi);
+  // the M-th largest key: among the non-zero ones, or 0 (pages without a score, taken first to last)
+  uint32_t T = 0;
+  int take = g.M - nv;
+  if (nv > g.M) range_threshold<NT>(each, lo, hi, g.M, hist, cand, aux, T, take);  // (uniform)
+  else take = take > 0 ? take : 0;
+  // ordered compaction of the slices: (count above T, count equal to T) per thread, one block scan
+  uint32_t gt = 0, eq = 0;
+  each([&](uint32_t key) {
+    gt += key > T;
+    eq += key == T;
+  });
+  const uint64_t pre = block_excl_prefix<NT>((uint64_t)gt | ((uint64_t)eq << 32), wtot);
+  const int eq_before = (int)(pre >> 32);
+  int rank = (int)(uint32_t)pre + (eq_before < take ? eq_before : take);
+  int eqr = eq_before;
+  for (int i = b; i < e; ++i) {
+    const uint32_t key = keys[i];
+    const bool is_eq = key == T;
+    if (key > T || (is_eq && eqr < take)) out[rank++] = (int32_t)(ri.p_lo + i);
+    eqr += is_eq;
+  }
 }
 
 // ============================================================================ Stage 2: fine token scores
@@ -1351,158 +1566,6 @@ __global__ __launch_bounds__(NT) void token_select_kernel(IndexGeom g, int64_t n
   emit_row<NT>(g, row, lidx, cnt, rstart, wsum, idx, count, runs, run_count);
 }
 
-// Exclusive prefix over NT threads of one 32-bit value each (sum over threads < t); wtot is LDS
-// [NT/64]. One block barrier: the caller does not write wtot again before another barrier.
-template <int NT>
-__device__ __forceinline__ uint32_t block_excl_prefix(uint32_t v, uint32_t* wtot) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  uint32_t inc = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t t = __shfl_up(inc, o);
-    if (lane >= o) inc += t;
-  }
-  if (lane == 63) wtot[wv] = inc;
-  __syncthreads();
-  uint32_t base = 0;
-#pragma unroll
-  for (int x = 0; x < NT / 64; ++x) base += x < wv ? wtot[x] : 0u;
-  return base + inc - v;
-}
-
-// Threshold of the k largest non-zero keys of a row held in registers (KPT per thread): T and take
-// such that the selection is every key > T and the first `take` keys == T (position order), as
-// radix_threshold gives. Each pass counts the keys still in question, those in [lo, hi], into
-// kRangeBins bins that split that interval evenly (bin = (key - lo) * scale / 2^32, non-decreasing
-// in the key), so one row's scores spread over the bins however closely they cluster, and one
-// wave finds the bin holding the rem-th largest key. At most 64 keys in that bin: they are gathered
-// into LDS and that wave ranks them against each other. More: the next pass narrows [lo, hi] to the
-// smallest and largest key of the bin. A bin spans at most (hi - lo + 1) / 511 + 2 values, so the
-// fourth pass sees fewer than kRangeBins values and gives each value its own bin. The scan and the
-// ranking are per-row work done once, by wave 0: with several rows per CU the other waves' wait at
-// the barrier costs less than eight waves repeating them. lo >= 1 (the smallest non-zero key), so
-// key - lo <= hi - lo excludes the zero keys (no candidate) as well as keys outside [lo, hi].
-// hist[0 .. 2 kRangeBins) is zero on entry; aux[0] (gathered count) is 0, aux[6], aux[8] (bin
-// minimum slots) are ~0u and aux[7], aux[9] (bin maximum slots) 0. Needs rem in [1, keys in play].
-constexpr int kRangeBins = 512;
-constexpr int kRangeAux = 10;
-template <int NT, int KPT>
-__device__ __forceinline__ void range_threshold(const uint32_t (&kv)[KPT], uint32_t lo, uint32_t hi, int rem,
-                                                uint32_t* hist, uint32_t* cand, uint32_t* aux, uint32_t& T,
-                                                int& take) {
-  static_assert(kRangeBins == 8 * 64, "a lane scans eight bins");
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  for (int pass = 0; pass < 4; ++pass) {
-    uint32_t* hb = hist + kRangeBins * (pass & 1);
-    if (pass > 0)  // the other buffer was last read before the previous pass's second barrier
-      for (int i = threadIdx.x; i < kRangeBins; i += NT) hist[kRangeBins * ((pass + 1) & 1) + i] = 0u;
-    const uint32_t range = hi - lo;
-    const bool direct = range < (uint32_t)kRangeBins;  // one value per bin
-    // scale <= 512 * 2^32 / (range + 1), so that bins stay below 512 (range >= 512: it fits 32 bits)
-    const uint32_t scale = direct ? 0u : (uint32_t)floor(2199023255552.0 / ((double)range + 1.0)) - 1u;
-    if (direct) {
-#pragma unroll
-      for (int e = 0; e < KPT; ++e)
-        if (kv[e] - lo <= range) atomicAdd(&hb[kv[e] - lo], 1u);
-    } else {
-#pragma unroll
-      for (int e = 0; e < KPT; ++e)
-        if (kv[e] - lo <= range) atomicAdd(&hb[__umulhi(kv[e] - lo, scale)], 1u);
-    }
-    __syncthreads();
-    if (wv == 0) {
-      // lane l holds bins 8 l .. 8 l + 7; keys in the bins of higher lanes by a suffix sum
-      const u32x4 ca = reinterpret_cast<const u32x4*>(hb)[2 * lane];
-      const u32x4 cb = reinterpret_cast<const u32x4*>(hb)[2 * lane + 1];
-      const uint32_t c[8] = {ca.x, ca.y, ca.z, ca.w, cb.x, cb.y, cb.z, cb.w};
-      uint32_t tot = 0;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) tot += c[u];
-      uint32_t suf = tot;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t x = __shfl_down(suf, o);
-        if (lane + o < 64) suf += x;
-      }
-      uint32_t above = suf - tot;
-#pragma unroll
-      for (int u = 7; u >= 0; --u) {
-        if (above < (uint32_t)rem && above + c[u] >= (uint32_t)rem) {
-          aux[1] = 8 * lane + u;
-          aux[2] = above;
-          aux[3] = c[u];
-        }
-        above += c[u];
-      }
-      if (lane == 0) {  // the other parity's bin extrema were last read before this pass's first barrier
-        aux[6 + 2 * ((pass + 1) & 1)] = ~0u;
-        aux[7 + 2 * ((pass + 1) & 1)] = 0u;
-      }
-    }
-    __syncthreads();
-    const uint32_t bb = aux[1], bc = aux[3];
-    rem -= (int)aux[2];
-    if (direct) {  // (uniform) the bin is one key value
-      T = lo + bb;
-      take = rem;
-      return;
-    }
-    auto in_bin = [&](uint32_t key) { return key - lo <= range && __umulhi(key - lo, scale) == bb; };
-    if (bc <= 64u) {  // (uniform)
-#pragma unroll
-      for (int e = 0; e < KPT; ++e)
-        if (in_bin(kv[e])) cand[atomicAdd(&aux[0], 1u)] = kv[e];
-      __syncthreads();
-      if (wv == 0) {
-        // lane l ranks candidate l against all of them: the rem-th largest value has fewer than rem
-        // candidates above it and at least rem at or above it; take = rem - (candidates above it)
-        const int nb = (int)bc;
-        const uint32_t x = cand[lane];  // (lanes >= nb read stale entries and are ignored)
-        int gt = 0, ge = 0;
-        for (int j = 0; j < nb; j += 4) {
-          const u32x4 c4 = *reinterpret_cast<const u32x4*>(cand + j);  // (the same address in every lane)
-          const uint32_t cc[4] = {c4.x, c4.y, c4.z, c4.w};
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const bool in = j + u < nb;
-            gt += in && cc[u] > x;
-            ge += in && cc[u] >= x;
-          }
-        }
-        const bool hit = lane < nb && gt < rem && ge >= rem;
-        if (hit && lane == __ffsll(__ballot(hit)) - 1) {
-          aux[4] = x;
-          aux[5] = (uint32_t)(rem - gt);
-        }
-      }
-      __syncthreads();
-      T = aux[4];
-      take = (int)aux[5];
-      return;
-    }
-    // narrow [lo, hi] to the boundary bin's keys
-    uint32_t mn = ~0u, mx = 0u;
-#pragma unroll
-    for (int e = 0; e < KPT; ++e)
-      if (in_bin(kv[e])) {
-        mn = kv[e] < mn ? kv[e] : mn;
-        mx = kv[e] > mx ? kv[e] : mx;
-      }
-    mn = wave_reduce_u32(mn, [](uint32_t p, uint32_t q) { return p < q ? p : q; });
-    mx = wave_reduce_u32(mx, [](uint32_t p, uint32_t q) { return p > q ? p : q; });
-    uint32_t* mm = aux + 6 + 2 * (pass & 1);
-    if (lane == 0) {
-      atomicMin(&mm[0], mn);
-      atomicMax(&mm[1], mx);
-    }
-    __syncthreads();
-    lo = mm[0];
-    hi = mm[1];
-  }
-  T = lo;  // (not reached: the fourth pass is direct)
-  take = rem;
-}
-
 // Rows of at most 16 keys per thread run eight waves per SIMD (four rows of 512 threads per CU):
 // the registers are capped so that the small LDS footprint is what bounds the rows a CU holds.
 template <int NT, int KPT>
@@ -1551,35 +1614,18 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(KPT <= 16 ? 
         for (int u = 0; u < 4; ++u) kv[e + u] = i0 + e + u < n ? src[e + u] : 0u;
       }
     }
-    // non-zero keys (the candidates), their smallest and their largest
-    uint32_t nz = 0, mn = ~0u, mx = 0u;
+    auto each = [&](auto&& fn) {
 #pragma unroll
-    for (int e = 0; e < KPT; ++e)
-      if (kv[e] != 0u) {
-        ++nz;
-        mn = kv[e] < mn ? kv[e] : mn;
-        mx = kv[e] > mx ? kv[e] : mx;
-      }
-    nz = wave_reduce_u32(nz, [](uint32_t p, uint32_t q) { return p + q; });
-    mn = wave_reduce_u32(mn, [](uint32_t p, uint32_t q) { return p < q ? p : q; });
-    mx = wave_reduce_u32(mx, [](uint32_t p, uint32_t q) { return p > q ? p : q; });
-    if ((threadIdx.x & 63) == 0) {
-      wsum[threadIdx.x >> 6] = (int)nz;
-      wlo[threadIdx.x >> 6] = mn;
-      whi[threadIdx.x >> 6] = mx;
-    }
-    __syncthreads();  // the cleared histograms, aux and the per-wave counts
-    int nv = 0;
-    uint32_t lo = ~0u, hi = 0u;
-#pragma unroll
-    for (int x = 0; x < NT / 64; ++x) {
-      nv += wsum[x];
-      lo = wlo[x] < lo ? wlo[x] : lo;
-      hi = whi[x] > hi ? whi[x] : hi;
-    }
+      for (int e = 0; e < KPT; ++e) fn(kv[e]);
+    };
+    // non-zero keys (the candidates), their smallest and their largest; the barrier also publishes
+    // the cleared histograms and aux
+    int nv;
+    uint32_t lo, hi;
+    block_nonzero_range<NT>(each, wsum, wlo, whi, nv, lo, hi);
     uint32_t T = 0;
     int take = 0;
-    if (nv > g.k_sparse) range_threshold<NT, KPT>(kv, lo, hi, g.k_sparse, hist, cand, aux, T, take);  // (uniform)
+    if (nv > g.k_sparse) range_threshold<NT>(each, lo, hi, g.k_sparse, hist, cand, aux, T, take);  // (uniform)
     // ordered compaction: selected = key > T, or key == T among the first `take` such (index order);
     // with T = 0 (every candidate selected) take is 0, so counting the zero keys as ties is harmless
     uint32_t gt = 0, eq = 0;
@@ -1906,14 +1952,15 @@ hipError_t prepare_index_kernels() {
   const void* sel[] = {(const void*)token_select_kernel<512, false>, (const void*)token_select_kernel<1024, true>,
                        (const void*)token_select_reg_kernel<512, 16>, (const void*)token_select_reg_kernel<512, 32>,
                        (const void*)token_select_reg_kernel<512, 64>, (const void*)token_select_reg_kernel<1024, 8>};
-  for (const void* f : sel) {  // (the register-key kernels have 20 KB of static LDS, the others 4 KB)
+  for (const void* f : sel) {  // (static LDS: under 4 KB in the first two, under 20 KB in the others)
     e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (f == sel[0] || f == sel[1]) ? lim : lim - 16 * 1024);
     if (e != hipSuccess) return e;
   }
-  e = hipFuncSetAttribute((const void*)page_select_kernel<256>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
+  // the page selection's static LDS (range histograms) is under 8 KB
+  e = hipFuncSetAttribute((const void*)page_select_kernel<256>, hipFuncAttributeMaxDynamicSharedMemorySize, lim - 4096);
   if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)page_select_kernel<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
+  e = hipFuncSetAttribute((const void*)page_select_kernel<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, lim - 4096);
   if (e != hipSuccess) return e;
 
   if (dev >= 0 && dev < 64) done[dev] = true;

@@ -15,7 +15,7 @@ namespace {
 
 thread_local char g_err[512] = "";
 constexpr size_t kMaxLds = 160 * 1024;        // gfx950 LDS per workgroup
-constexpr size_t kSelectStaticLds = 4 * 1024;  // static LDS of the select kernels (upper bound)
+constexpr size_t kSelectStaticLds = 8 * 1024;  // static LDS of the page selection (upper bound)
 
 lsa_status fail(lsa_status st, const char* fmt, ...) {
   va_list ap;
