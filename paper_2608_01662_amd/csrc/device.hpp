@@ -176,20 +176,6 @@ __device__ __forceinline__ float sum4_xor16_32(float x) {
   const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
-// Reduction over the whole wave without LDS traffic: DPP exchanges within quads (lanes l^1, l^2),
-// half rows and rows (mirrors), then gfx950's row swaps (lanes l^16, l^32). op must be commutative
-// and associative; every lane ends with the result.
-template <typename Op>
-__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, Op op) {
-  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false));   // quad_perm [1, 0, 3, 2]
-  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false));   // quad_perm [2, 3, 0, 1]
-  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, false));  // row_half_mirror
-  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, false));  // row_mirror
-  const auto a = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  v = op(a[0], a[1]);
-  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return op(b[0], b[1]);
-}
 __device__ __forceinline__ uint64_t lanemask_lt() {
   int l = threadIdx.x & 63;
   return l == 0 ? 0ull : (~0ull >> (64 - l));

@@ -612,6 +612,20 @@ __device__ __forceinline__ V block_excl_prefix(V v, V* wtot) {
   return base + inc - v;
 }
 
+// Reduction over the whole wave without LDS traffic: DPP exchanges within quads (lanes l^1, l^2),
+// half rows and rows (mirrors), then gfx950's row swaps (lanes l^16, l^32). op must be commutative
+// and associative; every lane ends with the result.
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, Op op) {
+  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false));   // quad_perm [1, 0, 3, 2]
+  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false));   // quad_perm [2, 3, 0, 1]
+  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  v = op(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, false));  // row_mirror
+  const auto a = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = op(a[0], a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return op(b[0], b[1]);
+}
 // Number, smallest and largest of the non-zero keys of the block (each(fn) visits this thread's
 // keys). One block barrier, which also publishes whatever the caller wrote to LDS before the call;
 // wsum, wlo, whi ([NT/64] each) are next written by the caller only after another barrier.
