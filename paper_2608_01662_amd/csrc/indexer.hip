@@ -215,13 +215,16 @@ __device__ __forceinline__ void load_key_operand(const void* __restrict__ k, int
 __device__ __forceinline__ float relu(float x) { return __int_as_float(max(__float_as_int(x), 0)); }
 
 // sum_j w_j ReLU(acc_j) over the 32 heads of this lane's key column (Eq. 1 / Eq. 9), as four
-// interleaved partial sums (a fixed order, so every tile and row rounds the same way).
+// interleaved partial sums (a fixed order, so every tile and row rounds the same way). The two
+// lane halves hold 16 heads each; v_permlane32_swap hands each lane its partner's half sum
+// (a VALU exchange, no LDS round trip), and a + b == b + a, so both lanes agree bit for bit.
 __device__ __forceinline__ float head_reduce(const f32x16& acc, const float (&wr)[16]) {
   float p[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int r = 0; r < 16; ++r) p[r & 3] = fmaf(wr[r], relu(acc[r]), p[r & 3]);
   const float v = (p[0] + p[1]) + (p[2] + p[3]);
-  return v + __shfl_xor(v, 32);
+  const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(x[0]) + __uint_as_float(x[1]);
 }
 
 // A operand of min-max pooling (Eq. 13): per dimension max(q k_max, q k_min) = q+ k_max + q- k_min
@@ -1100,10 +1103,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FP8 || D == 
             acc1 = mfma32(a[s], raw1[s], acc1);
           }
         }
-        // key t of the chunk (position r0 + t) is scored iff lo <= t <= hi (32-bit, wave-uniform bounds)
-        const int64_t r0 = page_of(bit) * P + c0;
-        const int lo = (int)(ri.lo - r0 < 0 ? -1 : ri.lo - r0 > 64 ? 64 : ri.lo - r0);
-        const int hi = (int)(ri.hi - r0 < 0 ? -1 : ri.hi - r0 > 64 ? 64 : ri.hi - r0);
+        // key t of the chunk (position r0 + t) is scored iff lo <= t <= hi (wave-uniform bounds in
+        // 32 bits: positions are below n_kv < 2^31)
+        const int r0 = (int)page_of(bit) * P + c0;
+        const int dlo = (int)ri.lo - r0, dhi = (int)ri.hi - r0;
+        const int lo = dlo < 0 ? -1 : (dlo > 64 ? 64 : dlo);
+        const int hi = dhi < 0 ? -1 : (dhi > 64 ? 64 : dhi);
         const float v0 = head_reduce(acc0, wr) * sc0;
         const float v1 = head_reduce(acc1, wr) * sc1;
         pk0 = (t0 >= lo && t0 <= hi) ? score_key(v0) : 0u;
