@@ -30,38 +30,41 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 }
 
 // ============================================================================ MLA 64 x 576 / 512
-// One workgroup = 8 waves = one query row (or one split of its index list), two waves per SIMD
-// so that one wave's softmax and LDS traffic overlap the other's matrix work. Wave
-// (hq, kw) = (w >> 1, w & 1) owns heads 16hq..16hq+15 and
-//   * computes the partial S^T (32 tokens x 16 heads, two 16x16x32 M-tiles) over dims
-//     [288 kw, 288 kw + 288) of the 576; the two partials of a head quarter are summed through a
-//     2 KB-per-wave LDS exchange (a + b == b + a, so both waves see identical scores),
-//   * accumulates O^T for value columns [256 kw, 256 kw + 256): 16 blocks of 16 x 16.
-// Per wave: 36 Q-operand registers and 64 accumulator registers.
+// One workgroup = 8 waves = one query row (or one split of its index list), two waves per SIMD.
+// The waves split the work by role, one pair per head quarter hq = w & 3 (heads 16hq..16hq+15):
+//   * scorer w (w < 4) computes S^T (32 tokens x its 16 heads, two 16x16x32 M-tiles) over all 576
+//     dims, does the online softmax and leaves P (bf16, already in the B-operand layout of the
+//     value product) and the factor its running maximum moved by in an LDS slot;
+//   * value wave w + 4, one tile behind, rescales its O^T by that factor and accumulates
+//     O^T += V^T P^T over all 512 value columns (32 blocks of 16 x 16).
+// No score is split across waves, so the only synchronisation is one barrier per tile: at barrier
+// it, tile it has landed, the scorers have written P of tile it - 1 and the value waves are done
+// with tile it - 2. Three tile buffers rotate (tile it scored, tile it - 1 in the value products,
+// tile it + 1 loading); the value waves issue the loads and the P slots alternate by tile parity.
+// A scorer holds 72 Q-operand registers, a value wave 128 accumulator registers; the two roles
+// run separate loops with the same barrier sequence, so that their registers share the file.
 //
 // The row's index list is validated once into LDS (-1 for entries to skip). Tiles of 32 gathered
-// latent rows are moved by direct global->LDS loads into NBUF rotating buffers (NBUF - 1 tiles in
-// flight while one is consumed); waves 0..3 issue them. Tile layout: 1 KB blocks of 8 tokens x 8
+// latent rows are moved by direct global->LDS loads. Tile layout: 1 KB blocks of 8 tokens x 8
 // chunks (chunk c = dims 8c..8c+7): token t = 8o + j, chunk c sits in block 9o + c / 8 at 16-byte
 // slot 8j + ((c % 8) ^ mla_swz(o, j)), mla_swz(o, j) = (j & 6) | (o & 1). One direct load fills
-// one block, eight consecutive lanes taking one whole 128-byte line of one row (8 rows per load;
-// loads of 2 lanes per row touched 32 rows and cost about 7% more time at L = 128K), and the XOR
-// keeps the K-operand reads (16 tokens, one chunk) and the transposed V reads (4 tokens x 4 chunks
-// per half-wave) free of LDS bank conflicts. The K reads still take the LDS's slower path (about
-// 120 instead of 200 bytes per clock): a ds_read_b128 runs at full rate only when each 16-lane
-// quarter reads one aligned 256-byte segment, which a token-major tile cannot offer for 16 tokens
-// of one chunk; layouts that do (chunk-major) need loads that touch 16 or 32 rows each, and those
-// measured slower overall.
+// one block, eight consecutive lanes taking one whole 128-byte line of one row (8 rows per load),
+// and the XOR keeps the K-operand reads (16 tokens, one chunk) and the transposed V reads (4
+// tokens x 4 chunks per half-wave) free of LDS bank conflicts. The K reads still take the LDS's
+// slower path (about 120 instead of 200 bytes per clock): a ds_read_b128 runs at full rate only
+// when each 16-lane quarter reads one aligned 256-byte segment, which a token-major tile cannot
+// offer for 16 tokens of one chunk; layouts that do (chunk-major) need loads that touch 16 or 32
+// rows each, and those measured slower overall.
 //
-// Schedules that were measured and not kept: running the two wave groups half a tile apart
-// (ping-pong) is slower here, because the 36 KB of LDS writes a tile refill makes hold up the
-// LDS reads of whichever group computes scores meanwhile; staging the tiles through VGPRs instead
-// of direct loads has the same effect.
+// Before the role split, wave (hq, kw) computed half of the dims of S for its 16 heads and the
+// pair summed their partials through LDS behind a second barrier per tile (74 ms per layer at
+// L = 128K against 62 ms now, same LDS bytes otherwise): the cost was the extra synchronisation
+// of the eight waves, not the bytes exchanged.
 constexpr int kMlaT = 32;
 constexpr int kMlaTile = 36 * 1024;  // 72 chunks x 32 tokens x 16 bytes
-constexpr int kMlaXch = 8 * 2048;    // partial-score exchange, 2 KB per wave
-constexpr int kMlaLoaders = 4;       // waves that issue the direct loads
-constexpr int kMlaLoads = 9;         // direct loads per loader wave per tile (36 x 1 KB)
+constexpr int kMlaBufs = 3;          // tile buffers: scored, in the value products, loading
+constexpr int kMlaLoads = 9;         // direct loads per value wave per tile (36 x 1 KB)
+constexpr int kMlaPSlot = 4 * 1280;  // per tile parity: 4 scorers x (1 KB of P + 256 B of factors)
 __device__ __forceinline__ int mla_swz(int o, int j) { return (j & 6) | (o & 1); }
 constexpr int kMlaHalf = 18 * 1024;  // the second 16 tokens of a tile start 18 blocks later
 constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
@@ -114,27 +117,28 @@ __device__ __forceinline__ int64_t block_prefix512(int64_t v, int64_t* wtot, int
 // WIN: the window branch of the split attention as a query-tiled kernel (Sec. 4.1.1): a workgroup
 // takes two consecutive query rows t0, t0 + 1 and heads 32 blockIdx.y .. + 31, and walks the
 // contiguous cache rows of the union of their windows, [t0 - k_swa + 1, t0 + 1], once: every tile
-// is loaded once into LDS for both rows. Wave w works on row t0 + (w >> 2) with the per-wave code
-// of the list kernel (16 heads, half of the dims, half of the value columns); each row masks the
-// tokens outside its own window. Writes the fp32 partial of split a.part.
+// is loaded once into LDS for both rows. Pair w4 (scorer w4, value wave w4 + 4) works on row
+// t0 + (w4 >> 1) and heads 32 blockIdx.y + 16 (w4 & 1) ..; each row masks the tokens outside its
+// own window. Writes the fp32 partial of split a.part.
 // (Two rows of 64 heads would hold 2 x (73.7 KB of Q operand + 131 KB of fp32 accumulators), 80%
 // of a CU's 512 KB register file, before any operand; tiling 2 rows x 32 heads keeps the 64 query
 // vectors per tile of the list kernel.)
-template <bool SPLIT, int NBUF, bool WIN = false>
+template <bool SPLIT, bool WIN = false>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void mla_attn_kernel(AttnGeom a) {
-  static_assert(NBUF >= 2 && NBUF <= 3, "two or three tile buffers");
   static_assert(!WIN || SPLIT, "the window kernel writes partials");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[NBUF * kMlaTile + kMlaXch];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kMlaBufs * kMlaTile + 2 * kMlaPSlot];
   __shared__ int32_t ids[WIN ? 1 : kMlaIdCap];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int i16 = lane & 15, g = lane >> 4;
-  const int hq = WIN ? 2 * (int)blockIdx.y + ((wv >> 1) & 1) : wv >> 1, kw = wv & 1;
+  const int w4 = wv & 3;  // scorer / value-wave pair
+  const bool scorer = wv < 4;
+  const int hq = WIN ? 2 * (int)blockIdx.y + (w4 & 1) : w4;
   const int head = 16 * hq + i16;
-  const bool loader = wv < kMlaLoaders;
-  // WIN: item = row pair; the second row of a pair past n_rows (odd count) computes nothing it writes
+  // WIN: item = row pair, pair w4 on row 2 item + (w4 >> 1); the second row of a pair past n_rows
+  // (odd count) computes nothing it writes
   const int64_t item = xcd_band(blockIdx.x, WIN ? (a.n_rows + 1) / 2 : a.n_rows);
-  const int64_t wrow = WIN ? 2 * item + (wv >> 2) : item;
+  const int64_t wrow = WIN ? 2 * item + (w4 >> 1) : item;
   const bool row_ok = wrow < a.n_rows;
   const int64_t row = row_ok ? wrow : a.n_rows - 1;
   const int split = SPLIT ? (a.part >= 0 ? a.part : (int)blockIdx.y) : 0;
@@ -193,67 +197,16 @@ void mla_attn_kernel(AttnGeom a) {
   const int n = s1 > s0 ? s1 - s0 : 0;
   const int32_t* slots = a.rows ? a.rows + row * a.k_cap + s0 : nullptr;  // list form (unused with runs)
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
-  uint8_t* xch = lds + NBUF * kMlaTile;
-
-  // Q^T as the B operand of S^T = K Q^T: column = head, k-step s covers dims 288kw + 32s + 8g .. +7.
-  u32x4 qb[9];
-  {
-    const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (row * 64 + head) * 576 + 288 * kw + 8 * g);
-#pragma unroll
-    for (int s = 0; s < 9; ++s) qb[s] = qp[4 * s];
-  }
-  f32x4 o[16];
-#pragma unroll
-  for (int c = 0; c < 16; ++c) o[c] = f32x4{};
-  float m = -INFINITY, l = 0.f;
-
-  // K operand of k-step s, M-tile mt: token 16mt + i16 = 8(2mt + i16/8) + (i16 % 8), chunk
-  // 36kw + 4s + g = 8 (s'/2) + 4 (s' % 2) + g with s' = s + 9kw. Two base offsets, for even and odd
-  // s; the rest is an immediate (s/2 blocks, mt * 18 blocks).
-  const int ksw = mla_swz(i16 >> 3, i16 & 7);
-  const int k_row = 9 * (i16 >> 3) * 1024 + 8 * (i16 & 7) * 16;
-  const int k_p0 = k_row + ((0 + g) ^ ksw) * 16, k_p1 = k_row + ((4 + g) ^ ksw) * 16;
-  const int k_even = kw ? k_p1 + 4 * 1024 : k_p0;       // s even: s' % 2 = kw, block s'/2 = s/2 + 4kw
-  const int k_odd = kw ? k_p0 + 5 * 1024 : k_p1;        // s odd: s' % 2 = 1 - kw, block (s-1)/2 + 5kw
-  // V^T operand of value block c: source lane (vq, gq) supplies token 4g + vq (and +16), dims
-  // 256kw + 16c + 4gq .. +3, i.e. token 8(g/2) + 4(g % 2) + vq, chunk 32kw + 2c + gq/2 = block
-  // 4kw + c/4, chunk 2(c % 4) + gq/2 of it, byte 8(gq % 2): one base offset per c % 4.
-  const int vq = i16 >> 2, gq = i16 & 3;
-  const int vj = 4 * (g & 1) + vq, vsw = mla_swz(g >> 1, vj);
-  int v_off[4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-    v_off[u] = (9 * (g >> 1) + 4 * kw) * 1024 + (8 * vj + ((2 * u + (gq >> 1)) ^ vsw)) * 16 + (gq & 1) * 8;
-  // Direct load k of loader wave w fills block 9w + k (tokens 8w.., chunks 8k..): lane 8j + u takes
-  // token 8w + j, chunk 8k + (u ^ mla_swz(w, j)), 16 bytes of one 128-byte line per lane.
-  const int lj = lane & 31;  // token of this lane's validity bit in the softmax mask
-  const int dj = lane >> 3;
-  const int dma_tok = 8 * wv + dj;
-  const int64_t dma_col = ((lane & 7) ^ mla_swz(wv, dj)) * 16;
-  auto issue = [&](int tile, int buf) {
-    int r;
-    if (WIN) {  // contiguous rows; positions past the union re-read its last row (masked)
-      const int64_t p = win0 + (int64_t)tile * kMlaT + dma_tok;
-      r = (int)(p < u_last ? p : u_last);
-    } else {
-      r = ids[tile * kMlaT + dma_tok];
-    }
-    const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
-    const uint8_t* const srcs[kMlaLoads] = {src,       src + 128, src + 256, src + 384,  src + 512,
-                                            src + 640, src + 768, src + 896, src + 1024};
-    lds_dma16x9(srcs, lds_addr(lds + buf * kMlaTile + wv * (kMlaLoads * 1024)));
-  };
+  uint8_t* const pslots = lds + kMlaBufs * kMlaTile;
+  uint8_t* const slot0 = pslots + w4 * 1280;  // this pair's P slot of tile parity 0
+  __shared__ float fin[2 * 64];               // per pair and head: reference max and sum
 
   constexpr int kPass = WIN ? (1 << 30) : kMlaIdCap;  // the window needs no staged list
-  for (int c0 = 0; c0 < n; c0 += kPass) {
-    const int nc = n - c0 < kPass ? n - c0 : kPass;
-    const int ntiles = (nc + kMlaT - 1) / kMlaT;
-    // list entries -> LDS, validated (-1 = skip; the last tile is padded with -1)
-    if (!WIN && a.runs && threadIdx.x == 0) rq_n = 0;  // the previous pass's readers passed a barrier since
-    if (!WIN) __syncthreads();  // the previous chunk's readers of `ids` are done
-    if (WIN) {
-      // nothing to stage: tile rows are win0 + 32 it + 0..31
-    } else if (a.runs) {
+  // list entries [c0, c0 + nc) -> LDS, validated (-1 = skip; the last tile is padded with -1)
+  auto stage = [&](int c0, int nc, int ntiles) {
+    if (a.runs && threadIdx.x == 0) rq_n = 0;  // the previous pass's readers passed a barrier since
+    __syncthreads();  // the previous chunk's readers of `ids` are done
+    if (a.runs) {
       // list entries [s0 + c0, s0 + c0 + nc) from the runs (runs partition the list, so every entry
       // is written once): each thread writes the entries of its own short runs that fall in this
       // chunk and queues the longer ones, which the whole block then writes, 512 entries at a time
@@ -307,105 +260,175 @@ void mla_attn_kernel(AttnGeom a) {
       }
     }
     __syncthreads();
-    // the Q operand arrived before the list entries; let the compiler place its wait for Q here,
-    // ahead of the first direct loads, rather than drain those loads before the first tile
-#pragma unroll
-    for (int s = 0; s < 9; ++s) asm volatile("" ::"v"(qb[s]));
-    if (loader)
-      for (int x = 0; x < NBUF - 1 && x < ntiles; ++x) issue(x, x);
+  };
+  // cache row of token `tok` of tile `tile` (WIN: contiguous rows; positions past the union re-read
+  // its last row, masked), -1 for a skipped entry
+  auto tile_row = [&](int tile, int tok) -> int {
+    if constexpr (WIN) {
+      const int64_t p = win0 + (int64_t)tile * kMlaT + tok;
+      return (int)(p < u_last ? p : u_last);
+    } else {
+      return ids[tile * kMlaT + tok];
+    }
+  };
 
-    // byte offsets of the buffer being read and of the one refilled next, rotated as wave-uniform
-    // scalars (a modulo by the buffer count would be strength-reduced into per-read address math)
-    uint32_t cur_off = 0, next_off = (NBUF - 1) * kMlaTile;
-    for (int it = 0; it < ntiles; ++it) {
-      // tile `it` has landed (a loader may keep the loads of later tiles in flight); after this
-      // barrier every wave is also done with tile it - 1, whose buffer is refilled next
-      if (loader) {
-        if (NBUF == 3 && it + 1 < ntiles) vm_wait_barrier<kMlaLoads>();
-        else vm_wait_barrier<0>();
-        if (it + NBUF - 1 < ntiles) issue(it + NBUF - 1, next_off / kMlaTile);
-      } else {
-        barrier_only();
-      }
-      const uint8_t* tb = lds + __builtin_amdgcn_readfirstlane(cur_off);
-      cur_off = cur_off + kMlaTile == NBUF * kMlaTile ? 0 : cur_off + kMlaTile;
-      next_off = next_off + kMlaTile == NBUF * kMlaTile ? 0 : next_off + kMlaTile;
-
-      // ---- partial S^T = K Q^T over this wave's 288 dims
-      // all 18 K operands are requested before the first product, so the LDS latency is paid
-      // once per tile rather than once per product
-      u32x4 ka[18];
+  if (scorer) {
+    // Q^T as the B operand of S^T = K Q^T: column = head, k-step s covers dims 32s + 8g .. +7
+    u32x4 qb[18];
+    {
+      const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (row * 64 + head) * 576 + 8 * g);
 #pragma unroll
-      for (int s = 0; s < 9; ++s)
+      for (int s = 0; s < 18; ++s) qb[s] = qp[4 * s];
+    }
+    // K operand of k-step s, M-tile mt: token 16mt + i16 = 8(2mt + i16/8) + (i16 % 8), chunk
+    // 4s + g = 8 (s/2) + 4 (s % 2) + g: one base offset for even and one for odd s, the rest an
+    // immediate (s/2 blocks, mt * 18 blocks)
+    const int ksw = mla_swz(i16 >> 3, i16 & 7);
+    const int k_row = 9 * (i16 >> 3) * 1024 + 8 * (i16 & 7) * 16;
+    const int k_even = k_row + ((0 + g) ^ ksw) * 16, k_odd = k_row + ((4 + g) ^ ksw) * 16;
+    const int lj = lane & 31;  // token of this lane's validity bit in the softmax mask
+    float m = -INFINITY, l = 0.f;
+    for (int c0 = 0; c0 < n; c0 += kPass) {
+      const int nc = n - c0 < kPass ? n - c0 : kPass;
+      const int ntiles = (nc + kMlaT - 1) / kMlaT;
+      if constexpr (!WIN) stage(c0, nc, ntiles);
+      __syncthreads();
+      uint32_t cur_off = 0;
+      for (int it = 0; it <= ntiles; ++it) {
+        // tile it has landed; this scorer's P writes of tile it - 1 are complete
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        const uint8_t* tb = lds + __builtin_amdgcn_readfirstlane(cur_off);
+        cur_off = cur_off + kMlaTile == kMlaBufs * kMlaTile ? 0 : cur_off + kMlaTile;
+        if (it == ntiles) continue;  // (the value waves' last tile)
+        // S^T over all 576 dims: K operands in two batches of 18, each requested before its products
+        f32x4 sacc[2] = {f32x4{}, f32x4{}};
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
-          ka[2 * s + mt] = *reinterpret_cast<const u32x4*>(tb + ((s & 1) ? k_odd : k_even) + (s >> 1) * 1024 + mt * kMlaHalf);
-      __builtin_amdgcn_sched_barrier(0);  // keep the scheduler from sinking the reads again
-      f32x4 sacc[2] = {f32x4{}, f32x4{}};
+        for (int bt = 0; bt < 2; ++bt) {
+          u32x4 ka[18];
 #pragma unroll
-      for (int s = 0; s < 9; ++s)
+          for (int s9 = 0; s9 < 9; ++s9)
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) sacc[mt] = mfma16(ka[2 * s + mt], qb[s], sacc[mt]);
-      // ---- sum the two partials of this head quarter
-      {
-        f32x4* mine = reinterpret_cast<f32x4*>(xch + wv * 2048) + lane;
-        mine[0] = sacc[0];
-        mine[64] = sacc[1];
-        lds_done_barrier();
-        const f32x4* other = reinterpret_cast<const f32x4*>(xch + (wv ^ 1) * 2048) + lane;
-        sacc[0] += other[0];
-        sacc[1] += other[64];
-      }
-      // ---- online softmax (base 2); lane holds tokens 16mt + 4g + r of head `head`
-      uint32_t vmask;
-      if (WIN) {
-        const int64_t p = win0 + (int64_t)it * kMlaT + lj;
-        vmask = (uint32_t)__ballot(p >= w_lo && p <= w_hi);
-      } else {
-        vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
-      }
-      if (vmask != 0xFFFFFFFFu) {  // partial or skipped tokens: mask them
+            for (int mt = 0; mt < 2; ++mt) {
+              const int s = 9 * bt + s9;
+              ka[2 * s9 + mt] = *reinterpret_cast<const u32x4*>(tb + ((s & 1) ? k_odd : k_even) + (s >> 1) * 1024 + mt * kMlaHalf);
+            }
+          __builtin_amdgcn_sched_barrier(0);  // keep the scheduler from sinking the reads again
+#pragma unroll
+          for (int s9 = 0; s9 < 9; ++s9)
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) sacc[mt] = mfma16(ka[2 * s9 + mt], qb[9 * bt + s9], sacc[mt]);
+        }
+        // online softmax (base 2); lane holds tokens 16mt + 4g + r of head `head`
+        uint32_t vmask;
+        if constexpr (WIN) {
+          const int64_t p = win0 + (int64_t)it * kMlaT + lj;
+          vmask = (uint32_t)__ballot(p >= w_lo && p <= w_hi);
+        } else {
+          vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
+        }
+        if (vmask != 0xFFFFFFFFu) {  // partial or skipped tokens: mask them
+#pragma unroll
+          for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int tk = 16 * mt + 4 * g + r;
+              sacc[mt][r] = ((vmask >> tk) & 1u) ? sacc[mt][r] : -INFINITY;
+            }
+        }
+        float smax = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
+                           fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+        smax = max4_xor16_32(smax);
+        const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
+        // the reference maximum moves only when a head's maximum grows by more than 2^8; the value
+        // wave rescales its accumulators by the factor left in the slot (1 otherwise)
+        float alpha = 1.f;
+        if (mx > m + kLazy) {
+          alpha = fast_exp2(m - mx);
+          l *= alpha;
+          m = mx;
+        }
+        const float mb = m == -INFINITY ? 0.f : m;  // m = -inf only while every score is -inf
+        float p[8];
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int tk = 16 * mt + 4 * g + r;
-            sacc[mt][r] = ((vmask >> tk) & 1u) ? sacc[mt][r] : -INFINITY;
+            p[4 * mt + r] = fast_exp2(fmaf(sacc[mt][r], a.scale_log2, -mb));  // -inf -> 0
+            l += p[4 * mt + r];
           }
+        // B operand P^T: k index 8g + v <-> token (v < 4 ? 4g + v : 16 + 4g + v - 4)
+        const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                          pack_bf16x2(p[6], p[7])};
+        uint8_t* slot = slot0 + (it & 1) * kMlaPSlot;
+        *reinterpret_cast<u32x4*>(slot + 16 * lane) = pb;
+        *reinterpret_cast<float*>(slot + 1024 + 4 * lane) = alpha;
       }
-      float smax = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
-                         fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
-      smax = max4_xor16_32(smax);
-      const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
-      const bool need = mx > m + kLazy;
-      if (__ballot(need)) {
-        // Rare after the first tile (the reference max only moves by > 2^8).
-        const float alpha = need ? fast_exp2(m - mx) : 1.f;
+    }
+    const float lt = sum4_xor16_32(l);
+    if (g == 0) {
+      fin[2 * (16 * w4 + i16)] = m;
+      fin[2 * (16 * w4 + i16) + 1] = lt;
+    }
+    __syncthreads();
+    return;
+  }
+
+  // ---- value wave: O^T += V^T P^T over all 512 value columns, one tile behind the scorer.
+  // V^T operand of value block c: source lane (vq, gq) supplies token 4g + vq (and +16), dims
+  // 16c + 4gq .. +3, i.e. token 8(g/2) + 4(g % 2) + vq, chunk 2c + gq/2 = block c/4, chunk
+  // 2(c % 4) + gq/2 of it, byte 8(gq % 2): one base offset per c % 4.
+  const int vq = i16 >> 2, gq = i16 & 3;
+  const int vj = 4 * (g & 1) + vq, vsw = mla_swz(g >> 1, vj);
+  int v_off[4];
 #pragma unroll
-        for (int c = 0; c < 16; ++c) o[c] *= alpha;
-        l *= alpha;
-        m = need ? mx : m;
+  for (int u = 0; u < 4; ++u) v_off[u] = 9 * (g >> 1) * 1024 + (8 * vj + ((2 * u + (gq >> 1)) ^ vsw)) * 16 + (gq & 1) * 8;
+  f32x4 o[32];
+#pragma unroll
+  for (int c = 0; c < 32; ++c) o[c] = f32x4{};
+  // Direct load k of value wave w4 fills block 9 w4 + k (tokens 8 w4.., chunks 8k..): lane 8j + u
+  // takes token 8 w4 + j, chunk 8k + (u ^ mla_swz(w4, j)), 16 bytes of one 128-byte line per lane.
+  const int dj = lane >> 3;
+  const int dma_tok = 8 * w4 + dj;
+  const int64_t dma_col = ((lane & 7) ^ mla_swz(w4, dj)) * 16;
+  auto issue = [&](int tile, uint32_t buf_off) {
+    const int r = tile_row(tile, dma_tok);
+    const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
+    const uint8_t* const srcs[kMlaLoads] = {src,       src + 128, src + 256, src + 384,  src + 512,
+                                            src + 640, src + 768, src + 896, src + 1024};
+    lds_dma16x9(srcs, lds_addr(lds + buf_off + w4 * (kMlaLoads * 1024)));
+  };
+  for (int c0 = 0; c0 < n; c0 += kPass) {
+    const int nc = n - c0 < kPass ? n - c0 : kPass;
+    const int ntiles = (nc + kMlaT - 1) / kMlaT;
+    if constexpr (!WIN) stage(c0, nc, ntiles);
+    __syncthreads();
+    if (ntiles > 0) issue(0, 0);
+    // buffer byte offsets rotated as wave-uniform scalars: tile it - 1 (read now), it, it + 1
+    uint32_t prev_off = 2 * kMlaTile, cur_off = 0, next_off = kMlaTile;
+    for (int it = 0; it <= ntiles; ++it) {
+      // tile it has landed; the scorers' P of tile it - 1 is in its slot; tile it - 2 is free
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if (it + 1 < ntiles) issue(it + 1, next_off);
+      const uint8_t* tp = lds + __builtin_amdgcn_readfirstlane(prev_off);
+      const uint32_t t0 = prev_off;
+      prev_off = cur_off;
+      cur_off = next_off;
+      next_off = t0;
+      if (it == 0) continue;  // (nothing scored yet)
+      const uint8_t* slot = slot0 + ((it - 1) & 1) * kMlaPSlot;
+      const u32x4 pb = *reinterpret_cast<const u32x4*>(slot + 16 * lane);
+      const float alpha = *reinterpret_cast<const float*>(slot + 1024 + 4 * lane);
+      if (__ballot(alpha != 1.f)) {  // rare after the first tile
+#pragma unroll
+        for (int c = 0; c < 32; ++c) o[c] *= alpha;
       }
-      const float mb = m == -INFINITY ? 0.f : m;  // m = -inf only while every score is -inf
-      float p[8];
+      // V operands in batches of eight, each requested before its products
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          p[4 * mt + r] = fast_exp2(fmaf(sacc[mt][r], a.scale_log2, -mb));  // -inf -> 0
-          l += p[4 * mt + r];
-        }
-      // B operand P^T: k index 8g + v <-> token (v < 4 ? 4g + v : 16 + 4g + v - 4)
-      const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                        pack_bf16x2(p[6], p[7])};
-      // ---- O^T += V^T P^T over this wave's 256 value columns; V^T via transposed LDS reads
-      // (V operands requested in two batches of eight, again to pay the LDS latency rarely)
-#pragma unroll
-      for (int c8 = 0; c8 < 16; c8 += 8) {
+      for (int c8 = 0; c8 < 32; c8 += 8) {
         u32x4 va[8];
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
-          const uint8_t* vb = tb + v_off[(c8 + c) & 3] + ((c8 + c) >> 2) * 1024;
+          const uint8_t* vb = tp + v_off[(c8 + c) & 3] + ((c8 + c) >> 2) * 1024;
           va[c] = tr16_pair(vb, vb + kMlaHalf);
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -414,26 +437,26 @@ void mla_attn_kernel(AttnGeom a) {
       }
     }
   }
-
-  const float lt = sum4_xor16_32(l);
-  // accumulator layout: lane holds value columns 256kw + 16c + 4g + r of head `head`
-  const int dv0 = 256 * kw + 4 * g;
+  __syncthreads();  // the scorers' reference maxima and sums
+  const float mfin = fin[2 * (16 * w4 + i16)], lt = fin[2 * (16 * w4 + i16) + 1];
+  // accumulator layout: lane holds value columns 16c + 4g + r of head `head`
+  const int dv0 = 4 * g;
   if (!SPLIT) {
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     uint16_t* orow = a.out + (row * 64 + head) * 512 + dv0;
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
+    for (int c = 0; c < 32; ++c) {
       const u32x2 v = {pack_bf16x2(o[c][0] * inv, o[c][1] * inv), pack_bf16x2(o[c][2] * inv, o[c][3] * inv)};
       *reinterpret_cast<u32x2*>(orow + 16 * c) = v;
     }
-    if (a.lse && g == 0 && kw == 0) a.lse[row * 64 + head] = lt > 0.f ? (m + __log2f(lt)) * kLn2 : -INFINITY;
+    if (a.lse && g == 0) a.lse[row * 64 + head] = lt > 0.f ? (mfin + __log2f(lt)) * kLn2 : -INFINITY;
   } else if (row_ok) {
     const int64_t pi = (row * a.n_split + split) * 64 + head;
     float* po = a.part_o + pi * 512 + dv0;
 #pragma unroll
-    for (int c = 0; c < 16; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = o[c];
-    if (g == 0 && kw == 0) {
-      a.part_ml[pi * 2] = m;
+    for (int c = 0; c < 32; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = o[c];
+    if (g == 0) {
+      a.part_ml[pi * 2] = mfin;
       a.part_ml[pi * 2 + 1] = lt;
     }
   }
@@ -603,13 +626,9 @@ __global__ __launch_bounds__(256) void translate_rows_kernel(const int32_t* __re
 }
 
 // ============================================================================ host launchers
-// Two tile buffers: one tile in flight while one is consumed. With whole-line loads this measured
-// 2% faster than three buffers (two tiles in flight) at the L = 128K shape; with the earlier
-// 32-byte-per-row loads three buffers had been 0.7% faster.
-constexpr int kMlaBufs = 2;
 template <bool SPLIT>
 static void launch_mla_kernel(dim3 grid, const AttnGeom& a, hipStream_t st) {
-  hipLaunchKernelGGL((mla_attn_kernel<SPLIT, kMlaBufs>), grid, dim3(512), 0, st, a);
+  hipLaunchKernelGGL((mla_attn_kernel<SPLIT>), grid, dim3(512), 0, st, a);
 }
 
 hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st) {
@@ -632,7 +651,7 @@ hipError_t launch_mla_attn_part(const AttnGeom& a, hipStream_t st) {
 
 hipError_t launch_mla_attn_window(const AttnGeom& a, hipStream_t st) {
   if (a.n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL((mla_attn_kernel<true, kMlaBufs, true>), dim3((unsigned)((a.n_rows + 1) / 2), 2u), dim3(512), 0,
+  hipLaunchKernelGGL((mla_attn_kernel<true, true>), dim3((unsigned)((a.n_rows + 1) / 2), 2u), dim3(512), 0,
                      st, a);
   return hipGetLastError();
 }
