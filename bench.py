@@ -57,9 +57,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(workload: str):
     """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary,
-    or None when that summary is missing or was taken on different kernel sources."""
+    or None when that summary is missing, was taken on another workload or on different kernel
+    sources."""
     try:
         kv = {}
         with open(TRAFFIC_FILE) as fh:
@@ -67,7 +68,7 @@ def measured_traffic():
                 if ":" in line and not line.startswith("#"):
                     k, v = line.split(":", 1)
                     kv[k.strip()] = v.strip()
-        if kv.get("kernel_sources_sha256") != kernel_source_hash():
+        if kv.get("workload") != workload or kv.get("kernel_sources_sha256") != kernel_source_hash():
             return None
         return int(kv["traffic_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
@@ -551,7 +552,7 @@ def main():
                                 else "mla_attn_kernel"),
                      "bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS,
-                     "traffic": None if (split_attn or runs_attn) else measured_traffic(),
+                     "traffic": None if (split_attn or runs_attn) else measured_traffic(w.name),
                      "algorithmic_bytes_per_launch": attn_bytes, "launch_ms": attn_avg},
         "breakdown": {
             "block_cache_ms": float(bm_ms), "index_ms": float(idx_ms), "attn_ms_per_layer": attn_ms,
