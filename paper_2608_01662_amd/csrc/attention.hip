@@ -31,12 +31,14 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 
 // ============================================================================ MLA 64 x 576 / 512
 // One workgroup = 8 waves = one query row (or one split of its index list), two waves per SIMD.
-// The waves split the work by role, one pair per head quarter hq = w & 3 (heads 16hq..16hq+15):
-//   * scorer w (w < 4) computes S^T (32 tokens x its 16 heads, two 16x16x32 M-tiles) over all 576
-//     dims, does the online softmax and leaves P (bf16, already in the B-operand layout of the
-//     value product) and the factor its running maximum moved by in an LDS slot;
-//   * value wave w + 4, one tile behind, rescales its O^T by that factor and accumulates
-//     O^T += V^T P^T over all 512 value columns (32 blocks of 16 x 16).
+// The waves split the work by role:
+//   * scorer w (w < 4) computes S^T (32 tokens x heads 16w..16w+15, two 16x16x32 M-tiles) over
+//     all 576 dims, does the online softmax and leaves P (bf16, head-major) and the factor its
+//     running maximum moved by in an LDS slot;
+//   * value wave w + 4, one tile behind, takes the 32 heads of scorers 2(w >> 1), 2(w >> 1) + 1
+//     and value columns 256 (w & 1) .. + 255: it rescales its O^T by the factors and accumulates
+//     O^T += V^T P^T on 32x32x16 products (dims on the rows, heads on the columns), so that every
+//     V byte is read by two value waves per tile.
 // No score is split across waves, so the only synchronisation is one barrier per tile: at barrier
 // it, tile it has landed, the scorers have written P of tile it - 1 and the value waves are done
 // with tile it - 2. Three tile buffers rotate (tile it scored, tile it - 1 in the value products,
@@ -47,10 +49,12 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 // The row's index list is validated once into LDS (-1 for entries to skip). Tiles of 32 gathered
 // latent rows are moved by direct global->LDS loads. Tile layout: 1 KB blocks of 8 tokens x 8
 // chunks (chunk c = dims 8c..8c+7): token t = 8o + j, chunk c sits in block 9o + c / 8 at 16-byte
-// slot 8j + ((c % 8) ^ mla_swz(o, j)), mla_swz(o, j) = (j & 6) | (o & 1). One direct load fills
-// one block, eight consecutive lanes taking one whole 128-byte line of one row (8 rows per load),
-// and the XOR keeps the K-operand reads (16 tokens, one chunk) and the transposed V reads (4
-// tokens x 4 chunks per half-wave) free of LDS bank conflicts. The K reads still take the LDS's
+// slot 8j + ((c % 8) ^ mla_swz(o, j)), mla_swz(o, j) = 4 j1 + 2 j2 + (o & 1) with j1, j2 bits 1 and
+// 2 of j. One direct load fills one block, eight consecutive lanes taking one whole 128-byte line
+// of one row (8 rows per load), and the XOR keeps the K-operand reads (16 tokens, one chunk per
+// 16 lanes) and the value waves' transposed V reads (per 32 lanes, 4 token rows x 64 bytes: rows
+// 4r and 4r + 2, which share a half of the banks, land in opposite halves of the slots) free of
+// LDS bank conflicts (checked on the host against 64 banks of 4 bytes, 32 lanes per cycle). The K reads still take the LDS's
 // slower path (about 120 instead of 200 bytes per clock): a ds_read_b128 runs at full rate only
 // when each 16-lane quarter reads one aligned 256-byte segment, which a token-major tile cannot
 // offer for 16 tokens of one chunk; layouts that do (chunk-major) need loads that touch 16 or 32
@@ -58,14 +62,16 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 //
 // Before the role split, wave (hq, kw) computed half of the dims of S for its 16 heads and the
 // pair summed their partials through LDS behind a second barrier per tile (74 ms per layer at
-// L = 128K against 62 ms now, same LDS bytes otherwise): the cost was the extra synchronisation
-// of the eight waves, not the bytes exchanged.
+// L = 128K against 62 ms for the split with 16-head value waves, same LDS bytes otherwise): the
+// cost was the extra synchronisation of the eight waves, not the bytes exchanged. 32-head value
+// waves then halved the transposed V reads (60 ms).
 constexpr int kMlaT = 32;
 constexpr int kMlaTile = 36 * 1024;  // 72 chunks x 32 tokens x 16 bytes
 constexpr int kMlaBufs = 3;          // tile buffers: scored, in the value products, loading
 constexpr int kMlaLoads = 9;         // direct loads per value wave per tile (36 x 1 KB)
-constexpr int kMlaPSlot = 4 * 1280;  // per tile parity: 4 scorers x (1 KB of P + 256 B of factors)
-__device__ __forceinline__ int mla_swz(int o, int j) { return (j & 6) | (o & 1); }
+constexpr int kMlaPHead = 80;        // bytes per head in a P slot: 32 bf16 tokens + 16 B of padding
+constexpr int kMlaPSlot = 64 * kMlaPHead + 64 * 4;  // per tile parity: P of 64 heads + their rescale factors
+__device__ __forceinline__ int mla_swz(int o, int j) { return ((j & 2) << 1) | ((j & 4) >> 1) | (o & 1); }
 constexpr int kMlaHalf = 18 * 1024;  // the second 16 tokens of a tile start 18 blocks later
 constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
 
@@ -117,9 +123,10 @@ __device__ __forceinline__ int64_t block_prefix512(int64_t v, int64_t* wtot, int
 // WIN: the window branch of the split attention as a query-tiled kernel (Sec. 4.1.1): a workgroup
 // takes two consecutive query rows t0, t0 + 1 and heads 32 blockIdx.y .. + 31, and walks the
 // contiguous cache rows of the union of their windows, [t0 - k_swa + 1, t0 + 1], once: every tile
-// is loaded once into LDS for both rows. Pair w4 (scorer w4, value wave w4 + 4) works on row
-// t0 + (w4 >> 1) and heads 32 blockIdx.y + 16 (w4 & 1) ..; each row masks the tokens outside its
-// own window. Writes the fp32 partial of split a.part.
+// is loaded once into LDS for both rows. Scorer w4 works on row t0 + (w4 >> 1) and heads
+// 32 blockIdx.y + 16 (w4 & 1) .., value wave w4 + 4 on row t0 + (w4 >> 1), heads 32 blockIdx.y ..
+// + 31 and value columns 256 (w4 & 1) ..; each row masks the tokens outside its own window.
+// Writes the fp32 partial of split a.part.
 // (Two rows of 64 heads would hold 2 x (73.7 KB of Q operand + 131 KB of fp32 accumulators), 80%
 // of a CU's 512 KB register file, before any operand; tiling 2 rows x 32 heads keeps the 64 query
 // vectors per tile of the list kernel.)
@@ -198,8 +205,10 @@ void mla_attn_kernel(AttnGeom a) {
   const int32_t* slots = a.rows ? a.rows + row * a.k_cap + s0 : nullptr;  // list form (unused with runs)
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
   uint8_t* const pslots = lds + kMlaBufs * kMlaTile;
-  uint8_t* const slot0 = pslots + w4 * 1280;  // this pair's P slot of tile parity 0
-  __shared__ float fin[2 * 64];               // per pair and head: reference max and sum
+  // P slots: head-major [2 scorer pairs][32 heads][32 tokens] bf16, then the 64 rescale factors;
+  // scorer w4 writes local heads 16 (w4 & 1) .. of pair w4 >> 1, value wave w4 reads pair w4 >> 1
+  const int pair = w4 >> 1;
+  __shared__ float fin[2 * 64];               // per (pair, local head): reference max and sum
 
   constexpr int kPass = WIN ? (1 << 30) : kMlaIdCap;  // the window needs no staged list
   // list entries [c0, c0 + nc) -> LDS, validated (-1 = skip; the last tile is padded with -1)
@@ -356,35 +365,51 @@ void mla_attn_kernel(AttnGeom a) {
             p[4 * mt + r] = fast_exp2(fmaf(sacc[mt][r], a.scale_log2, -mb));  // -inf -> 0
             l += p[4 * mt + r];
           }
-        // B operand P^T: k index 8g + v <-> token (v < 4 ? 4g + v : 16 + 4g + v - 4)
+        // P of tokens 4g .. 4g + 3 and 16 + 4g .. 16 + 4g + 3, bf16, into the head's row of the slot
         const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                           pack_bf16x2(p[6], p[7])};
-        uint8_t* slot = slot0 + (it & 1) * kMlaPSlot;
-        *reinterpret_cast<u32x4*>(slot + 16 * lane) = pb;
-        *reinterpret_cast<float*>(slot + 1024 + 4 * lane) = alpha;
+        uint8_t* slot = pslots + (it & 1) * kMlaPSlot;
+        const int lh = 32 * pair + 16 * (w4 & 1) + i16;  // (pair, local head)
+        *reinterpret_cast<u32x2*>(slot + lh * kMlaPHead + 8 * g) = u32x2{pb.x, pb.y};        // tokens 4g ..
+        *reinterpret_cast<u32x2*>(slot + lh * kMlaPHead + 32 + 8 * g) = u32x2{pb.z, pb.w};   // tokens 16 + 4g ..
+        if (g == 0) *reinterpret_cast<float*>(slot + 64 * kMlaPHead + 4 * lh) = alpha;
       }
     }
     const float lt = sum4_xor16_32(l);
     if (g == 0) {
-      fin[2 * (16 * w4 + i16)] = m;
-      fin[2 * (16 * w4 + i16) + 1] = lt;
+      const int lh = 32 * pair + 16 * (w4 & 1) + i16;
+      fin[2 * lh] = m;
+      fin[2 * lh + 1] = lt;
     }
     __syncthreads();
     return;
   }
 
-  // ---- value wave: O^T += V^T P^T over all 512 value columns, one tile behind the scorer.
-  // V^T operand of value block c: source lane (vq, gq) supplies token 4g + vq (and +16), dims
-  // 16c + 4gq .. +3, i.e. token 8(g/2) + 4(g % 2) + vq, chunk 2c + gq/2 = block c/4, chunk
-  // 2(c % 4) + gq/2 of it, byte 8(gq % 2): one base offset per c % 4.
-  const int vq = i16 >> 2, gq = i16 & 3;
-  const int vj = 4 * (g & 1) + vq, vsw = mla_swz(g >> 1, vj);
-  int v_off[4];
+  // ---- value wave (pair, dh) = (w4 >> 1, w4 & 1): O^T += V^T P^T for the 32 heads of the scorer
+  // pair and value columns 256 dh .. + 255, one tile behind the scorers, on 32x32x16 products
+  // (dims on the rows, heads on the columns, 16 tokens per k-step): every V byte is read by two
+  // value waves per tile. A operand of value block c (dims 256 dh + 32 c ..), k-step ks: lane l
+  // holds dim l % 32, tokens 16 ks + 8 (l / 32) + 0..7, from two transposed reads; in 16-lane
+  // group G = l / 16, source lane s of read r supplies token 16 ks + 8 (G / 2) + 4 r + s / 4,
+  // dims 256 dh + 32 c + 16 (G % 2) + 4 (s % 4) .. + 3: chunk 32 dh + 4 c + 2 (G % 2) + (s % 4) / 2,
+  // i.e. block 9 (2 ks + G / 2) + 4 dh + c / 2, chunk 4 (c % 2) + 2 (G % 2) + (s % 4) / 2 of it. The
+  // swizzle depends on the token row and o % 2 only, so there is one base offset per (r, c % 2) and
+  // the rest is an immediate (ks * 18 KB, (c / 2) KB).
+  const int dh = w4 & 1;
+  const int G = lane >> 4, sl = lane & 15;
+  int v_off[2][2];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) v_off[u] = 9 * (g >> 1) * 1024 + (8 * vj + ((2 * u + (gq >> 1)) ^ vsw)) * 16 + (gq & 1) * 8;
-  f32x4 o[32];
+  for (int r = 0; r < 2; ++r)
 #pragma unroll
-  for (int c = 0; c < 32; ++c) o[c] = f32x4{};
+    for (int par = 0; par < 2; ++par) {
+      const int tk = 8 * (G >> 1) + 4 * r + (sl >> 2), o = tk >> 3, j = tk & 7;
+      const int ch = 4 * par + 2 * (G & 1) + ((sl >> 1) & 1);  // chunk within the block 9 o + 4 dh + c / 2
+      v_off[r][par] = (9 * o + 4 * dh) * 1024 + (8 * j + (ch ^ mla_swz(o, j))) * 16 + (sl & 1) * 8;
+    }
+  const int lh = 32 * pair + (lane & 31);  // (pair, local head) of this lane's accumulator column
+  f32x16 o[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) o[c] = f32x16{};
   // Direct load k of value wave w4 fills block 9 w4 + k (tokens 8 w4.., chunks 8k..): lane 8j + u
   // takes token 8 w4 + j, chunk 8k + (u ^ mla_swz(w4, j)), 16 bytes of one 128-byte line per lane.
   const int dj = lane >> 3;
@@ -415,47 +440,63 @@ void mla_attn_kernel(AttnGeom a) {
       cur_off = next_off;
       next_off = t0;
       if (it == 0) continue;  // (nothing scored yet)
-      const uint8_t* slot = slot0 + ((it - 1) & 1) * kMlaPSlot;
-      const u32x4 pb = *reinterpret_cast<const u32x4*>(slot + 16 * lane);
-      const float alpha = *reinterpret_cast<const float*>(slot + 1024 + 4 * lane);
+      const uint8_t* slot = pslots + ((it - 1) & 1) * kMlaPSlot;
+      // B operand P^T of k-step ks: head lh, tokens 16 ks + 8 (l / 32) .. + 7
+      const u32x4 pb0 = *reinterpret_cast<const u32x4*>(slot + lh * kMlaPHead + 16 * (lane >> 5));
+      const u32x4 pb1 = *reinterpret_cast<const u32x4*>(slot + lh * kMlaPHead + 32 + 16 * (lane >> 5));
+      const float alpha = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 4 * lh);
       if (__ballot(alpha != 1.f)) {  // rare after the first tile
 #pragma unroll
-        for (int c = 0; c < 32; ++c) o[c] *= alpha;
+        for (int c = 0; c < 8; ++c) o[c] *= alpha;
       }
-      // V operands in batches of eight, each requested before its products
+      // V operands of four value blocks (both k-steps) at a time, each batch requested before its products
 #pragma unroll
-      for (int c8 = 0; c8 < 32; c8 += 8) {
+      for (int c4 = 0; c4 < 8; c4 += 4) {
         u32x4 va[8];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const uint8_t* vb = tp + v_off[(c8 + c) & 3] + ((c8 + c) >> 2) * 1024;
-          va[c] = tr16_pair(vb, vb + kMlaHalf);
-        }
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const int cc = c4 + c;
+            const uint8_t* b0 = tp + v_off[0][cc & 1] + ks * kMlaHalf + (cc >> 1) * 1024;
+            const uint8_t* b1 = tp + v_off[1][cc & 1] + ks * kMlaHalf + (cc >> 1) * 1024;
+            va[2 * c + ks] = tr16_pair(b0, b1);
+          }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[c8 + c] = mfma16(va[c], pb, o[c8 + c]);
+        for (int c = 0; c < 4; ++c) o[c4 + c] = mfma32(va[2 * c], pb0, o[c4 + c]);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) o[c4 + c] = mfma32(va[2 * c + 1], pb1, o[c4 + c]);
       }
     }
   }
   __syncthreads();  // the scorers' reference maxima and sums
-  const float mfin = fin[2 * (16 * w4 + i16)], lt = fin[2 * (16 * w4 + i16) + 1];
-  // accumulator layout: lane holds value columns 16c + 4g + r of head `head`
-  const int dv0 = 4 * g;
+  const float mfin = fin[2 * lh], lt = fin[2 * lh + 1];
+  // accumulator layout: lane l, register r of block c holds dim 256 dh + 32 c + 8 (r / 4) +
+  // 4 (l / 32) + r % 4 of head (WIN ? 32 blockIdx.y : 32 pair) + l % 32
+  const int vhead = (WIN ? 32 * (int)blockIdx.y : 32 * pair) + (lane & 31);
+  const int dv0 = 256 * dh + 4 * (lane >> 5);
   if (!SPLIT) {
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    uint16_t* orow = a.out + (row * 64 + head) * 512 + dv0;
+    uint16_t* orow = a.out + (row * 64 + vhead) * 512 + dv0;
 #pragma unroll
-    for (int c = 0; c < 32; ++c) {
-      const u32x2 v = {pack_bf16x2(o[c][0] * inv, o[c][1] * inv), pack_bf16x2(o[c][2] * inv, o[c][3] * inv)};
-      *reinterpret_cast<u32x2*>(orow + 16 * c) = v;
-    }
-    if (a.lse && g == 0) a.lse[row * 64 + head] = lt > 0.f ? (mfin + __log2f(lt)) * kLn2 : -INFINITY;
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const u32x2 v = {pack_bf16x2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
+                         pack_bf16x2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
+        *reinterpret_cast<u32x2*>(orow + 32 * c + 8 * q) = v;
+      }
+    if (a.lse && dh == 0 && lane < 32) a.lse[row * 64 + vhead] = lt > 0.f ? (mfin + __log2f(lt)) * kLn2 : -INFINITY;
   } else if (row_ok) {
-    const int64_t pi = (row * a.n_split + split) * 64 + head;
+    const int64_t pi = (row * a.n_split + split) * 64 + vhead;
     float* po = a.part_o + pi * 512 + dv0;
 #pragma unroll
-    for (int c = 0; c < 32; ++c) *reinterpret_cast<f32x4*>(po + 16 * c) = o[c];
-    if (g == 0) {
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<f32x4*>(po + 32 * c + 8 * q) = f32x4{o[c][4 * q], o[c][4 * q + 1], o[c][4 * q + 2], o[c][4 * q + 3]};
+    if (dh == 0 && lane < 32) {
       a.part_ml[pi * 2] = mfin;
       a.part_ml[pi * 2 + 1] = lt;
     }
