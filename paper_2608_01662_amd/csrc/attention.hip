@@ -3,11 +3,11 @@
 // columns) and MQA-128 (16 heads, separate K and V of 128).
 //
 // Both kernels compute S^T = K Q^T (keys on the MFMA rows, heads on the columns) so that in the
-// accumulator layout each lane holds 16 (or 8) tokens of ONE head: the per-head softmax max and
-// sum are in-lane reductions plus one or two lane exchanges, and the exponentiated scores are
-// already in the B-operand layout of the next product O^T += V^T P^T. V^T reaches the A-operand
-// layout through ds_read_b64_tr_b16 (a 16 x 4 transpose read on gfx950), so V is stored once,
-// token-major, in the same LDS tile as K.
+// accumulator layout each lane holds several tokens of one head per block: the per-head softmax
+// max and sum are in-lane reductions plus two lane exchanges, and the exponentiated scores are in
+// the B-operand layout of the product O^T += V^T P^T (MQA: in registers; MLA: written head-major
+// to LDS for the value waves). V^T reaches the A-operand layout through ds_read_b64_tr_b16 (a
+// 16 x 4 transpose read on gfx950), so V is stored once, token-major, in the same LDS tile as K.
 //
 // Online softmax in base 2 with a lazily updated reference maximum: the accumulators are only
 // rescaled when a head's running maximum grows by more than 2^8, which keeps every
@@ -32,19 +32,23 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 // ============================================================================ MLA 64 x 576 / 512
 // One workgroup = 8 waves = one query row (or one split of its index list), two waves per SIMD.
 // The waves split the work by role:
-//   * scorer w (w < 4) computes S^T (32 tokens x heads 16w..16w+15, two 16x16x32 M-tiles) over
-//     all 576 dims, does the online softmax and leaves P (bf16, head-major) and the factor its
-//     running maximum moved by in an LDS slot;
-//   * value wave w + 4, one tile behind, takes the 32 heads of scorers 2(w >> 1), 2(w >> 1) + 1
-//     and value columns 256 (w & 1) .. + 255: it rescales its O^T by the factors and accumulates
-//     O^T += V^T P^T on 32x32x16 products (dims on the rows, heads on the columns), so that every
-//     V byte is read by two value waves per tile.
-// No score is split across waves, so the only synchronisation is one barrier per tile: at barrier
-// it, tile it has landed, the scorers have written P of tile it - 1 and the value waves are done
-// with tile it - 2. Three tile buffers rotate (tile it scored, tile it - 1 in the value products,
-// tile it + 1 loading); the value waves issue the loads and the P slots alternate by tile parity.
-// A scorer holds 72 Q-operand registers, a value wave 128 accumulator registers; the two roles
-// run separate loops with the same barrier sequence, so that their registers share the file.
+//   * scorer w (w < 4) computes S^T for tokens 16 (w & 1) .. + 15 of every tile and the 32 heads
+//     32 (w >> 1) .. + 31 (two 16x16x32 head blocks sharing each K operand, so that every K byte
+//     is read by two scorers per tile) over all 576 dims, does the online softmax of its token
+//     half and leaves P (bf16, head-major) and the reference maximum it used in an LDS slot;
+//   * value wave w + 4, one tile behind, accumulates O^T += V^T P^T for all 64 heads and value
+//     columns 128 w .. + 127 on 32x32x16 products (dims on the rows, heads on the columns): each V
+//     operand feeds two head blocks, and every V byte is read once per tile.
+// The two token halves of a head keep their own reference maxima. A scorer adopts the other
+// half's reference of the previous tile when that is larger, so the two differ only in the tile
+// after one of them moved; the value wave then brings the lower half's P (rounded to bf16 a second
+// time) and its accumulators to the larger one. No score is split across waves, so the only
+// synchronisation is one barrier per tile: at barrier it, tile it has landed, the scorers have
+// written P of tile it - 1 and the value waves are done with tile it - 2. Three tile buffers
+// rotate (tile it scored, tile it - 1 in the value products, tile it + 1 loading); the value waves
+// issue the loads and the P slots alternate by tile parity. A scorer holds 144 Q-operand
+// registers, a value wave 128 accumulator registers; the two roles run separate loops with the
+// same barrier sequence, so that their registers share the file.
 //
 // The row's index list is validated once into LDS (-1 for entries to skip). Tiles of 32 gathered
 // latent rows are moved by direct global->LDS loads. Tile layout: 1 KB blocks of 8 tokens x 8
@@ -64,16 +68,25 @@ __device__ __forceinline__ u32x4 tr16_pair(const uint8_t* pa, const uint8_t* pb)
 // pair summed their partials through LDS behind a second barrier per tile (74 ms per layer at
 // L = 128K against 62 ms for the split with 16-head value waves, same LDS bytes otherwise): the
 // cost was the extra synchronisation of the eight waves, not the bytes exchanged. 32-head value
-// waves then halved the transposed V reads (60 ms).
+// waves then halved the transposed V reads (60 ms), scorers split by tokens instead of heads
+// halved the K reads (56 ms), and 64-head value waves halved the V reads again (55 ms).
 constexpr int kMlaT = 32;
 constexpr int kMlaTile = 36 * 1024;  // 72 chunks x 32 tokens x 16 bytes
 constexpr int kMlaBufs = 3;          // tile buffers: scored, in the value products, loading
 constexpr int kMlaLoads = 9;         // direct loads per value wave per tile (36 x 1 KB)
 constexpr int kMlaPHead = 80;        // bytes per head in a P slot: 32 bf16 tokens + 16 B of padding
-constexpr int kMlaPSlot = 64 * kMlaPHead + 64 * 4;  // per tile parity: P of 64 heads + their rescale factors
+constexpr int kMlaPSlot = 64 * kMlaPHead + 2 * 64 * 4;  // per tile parity: P of 64 heads + the reference maxima of both token halves
 __device__ __forceinline__ int mla_swz(int o, int j) { return ((j & 2) << 1) | ((j & 4) >> 1) | (o & 1); }
 constexpr int kMlaHalf = 18 * 1024;  // the second 16 tokens of a tile start 18 blocks later
 constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
+// eight bf16 scaled by f (rounded to nearest even again)
+__device__ __forceinline__ u32x4 scale_bf16x8(u32x4 v, float f) {
+  u32x4 r;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    r[k] = pack_bf16x2(__uint_as_float(v[k] << 16) * f, __uint_as_float(v[k] & 0xFFFF0000u) * f);
+  return r;
+}
 
 // Run form of an index list: runs [start, start + len) of cache rows, in list order. Thread t of
 // the 512 takes the contiguous block of runs [t U, t U + U), U = ceil(n_runs / 512).
@@ -123,9 +136,10 @@ __device__ __forceinline__ int64_t block_prefix512(int64_t v, int64_t* wtot, int
 // WIN: the window branch of the split attention as a query-tiled kernel (Sec. 4.1.1): a workgroup
 // takes two consecutive query rows t0, t0 + 1 and heads 32 blockIdx.y .. + 31, and walks the
 // contiguous cache rows of the union of their windows, [t0 - k_swa + 1, t0 + 1], once: every tile
-// is loaded once into LDS for both rows. Scorer w4 works on row t0 + (w4 >> 1) and heads
-// 32 blockIdx.y + 16 (w4 & 1) .., value wave w4 + 4 on row t0 + (w4 >> 1), heads 32 blockIdx.y ..
-// + 31 and value columns 256 (w4 & 1) ..; each row masks the tokens outside its own window.
+// is loaded once into LDS for both rows. Scorer w4 works on row t0 + (w4 >> 1), heads
+// 32 blockIdx.y .. + 31 and tokens 16 (w4 & 1) .. of every tile, value wave w4 + 4 on both rows,
+// heads 32 blockIdx.y .. + 31 and value columns 128 w4 ..; each row masks the tokens outside its
+// own window.
 // Writes the fp32 partial of split a.part.
 // (Two rows of 64 heads would hold 2 x (73.7 KB of Q operand + 131 KB of fp32 accumulators), 80%
 // of a CU's 512 KB register file, before any operand; tiling 2 rows x 32 heads keeps the 64 query
@@ -140,8 +154,6 @@ void mla_attn_kernel(AttnGeom a) {
   const int i16 = lane & 15, g = lane >> 4;
   const int w4 = wv & 3;  // scorer / value-wave pair
   const bool scorer = wv < 4;
-  const int hq = WIN ? 2 * (int)blockIdx.y + (w4 & 1) : w4;
-  const int head = 16 * hq + i16;
   // WIN: item = row pair, pair w4 on row 2 item + (w4 >> 1); the second row of a pair past n_rows
   // (odd count) computes nothing it writes
   const int64_t item = xcd_band(blockIdx.x, WIN ? (a.n_rows + 1) / 2 : a.n_rows);
@@ -205,10 +217,11 @@ void mla_attn_kernel(AttnGeom a) {
   const int32_t* slots = a.rows ? a.rows + row * a.k_cap + s0 : nullptr;  // list form (unused with runs)
   const uint8_t* kvb = reinterpret_cast<const uint8_t*>(a.kv);
   uint8_t* const pslots = lds + kMlaBufs * kMlaTile;
-  // P slots: head-major [2 scorer pairs][32 heads][32 tokens] bf16, then the 64 rescale factors;
-  // scorer w4 writes local heads 16 (w4 & 1) .. of pair w4 >> 1, value wave w4 reads pair w4 >> 1
+  // P slots: head-major [2 scorer pairs][32 heads][32 tokens] bf16, then the reference maxima
+  // [2 token halves][64 (pair, local head)]; scorer w4 writes tokens 16 (w4 & 1) .. of the 32
+  // heads of pair w4 >> 1, every value wave reads all 64
   const int pair = w4 >> 1;
-  __shared__ float fin[2 * 64];               // per (pair, local head): reference max and sum
+  __shared__ float fin[2 * 2 * 64];           // per (token half, pair, local head): reference max and sum
 
   constexpr int kPass = WIN ? (1 << 30) : kMlaIdCap;  // the window needs no staged list
   // list entries [c0, c0 + nc) -> LDS, validated (-1 = skip; the last tile is padded with -1)
@@ -282,21 +295,25 @@ void mla_attn_kernel(AttnGeom a) {
   };
 
   if (scorer) {
-    // Q^T as the B operand of S^T = K Q^T: column = head, k-step s covers dims 32s + 8g .. +7
-    u32x4 qb[18];
-    {
-      const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (row * 64 + head) * 576 + 8 * g);
+    // scorer w4 takes tokens 16 th .. + 15 of every tile for the 32 heads of its pair
+    const int th = w4 & 1;
+    const int hbase = WIN ? 32 * (int)blockIdx.y : 32 * pair;
+    // Q^T as the B operand of S^T = K Q^T: column = head 16 nb + i16, k-step s covers dims 32s + 8g .. +7
+    u32x4 qb[2][18];
 #pragma unroll
-      for (int s = 0; s < 18; ++s) qb[s] = qp[4 * s];
+    for (int nb = 0; nb < 2; ++nb) {
+      const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + (row * 64 + hbase + 16 * nb + i16) * 576 + 8 * g);
+#pragma unroll
+      for (int s = 0; s < 18; ++s) qb[nb][s] = qp[4 * s];
     }
-    // K operand of k-step s, M-tile mt: token 16mt + i16 = 8(2mt + i16/8) + (i16 % 8), chunk
+    // K operand of k-step s: token 16 th + i16 = 8(2th + i16/8) + (i16 % 8), chunk
     // 4s + g = 8 (s/2) + 4 (s % 2) + g: one base offset for even and one for odd s, the rest an
-    // immediate (s/2 blocks, mt * 18 blocks)
+    // immediate (s/2 blocks)
     const int ksw = mla_swz(i16 >> 3, i16 & 7);
-    const int k_row = 9 * (i16 >> 3) * 1024 + 8 * (i16 & 7) * 16;
+    const int k_row = th * kMlaHalf + 9 * (i16 >> 3) * 1024 + 8 * (i16 & 7) * 16;
     const int k_even = k_row + ((0 + g) ^ ksw) * 16, k_odd = k_row + ((4 + g) ^ ksw) * 16;
     const int lj = lane & 31;  // token of this lane's validity bit in the softmax mask
-    float m = -INFINITY, l = 0.f;
+    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
     for (int c0 = 0; c0 < n; c0 += kPass) {
       const int nc = n - c0 < kPass ? n - c0 : kPass;
       const int ntiles = (nc + kMlaT - 1) / kMlaT;
@@ -309,25 +326,38 @@ void mla_attn_kernel(AttnGeom a) {
         const uint8_t* tb = lds + __builtin_amdgcn_readfirstlane(cur_off);
         cur_off = cur_off + kMlaTile == kMlaBufs * kMlaTile ? 0 : cur_off + kMlaTile;
         if (it == ntiles) continue;  // (the value waves' last tile)
-        // S^T over all 576 dims: K operands in two batches of 18, each requested before its products
-        f32x4 sacc[2] = {f32x4{}, f32x4{}};
+        // the other token half's reference maxima of tile it - 1 (adopted when larger)
+        float mp[2] = {-INFINITY, -INFINITY};
+        if (it > 0) {
+          const uint8_t* pr = pslots + ((it - 1) & 1) * kMlaPSlot + 64 * kMlaPHead + (1 - th) * 256;
 #pragma unroll
-        for (int bt = 0; bt < 2; ++bt) {
-          u32x4 ka[18];
-#pragma unroll
-          for (int s9 = 0; s9 < 9; ++s9)
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt) {
-              const int s = 9 * bt + s9;
-              ka[2 * s9 + mt] = *reinterpret_cast<const u32x4*>(tb + ((s & 1) ? k_odd : k_even) + (s >> 1) * 1024 + mt * kMlaHalf);
-            }
-          __builtin_amdgcn_sched_barrier(0);  // keep the scheduler from sinking the reads again
-#pragma unroll
-          for (int s9 = 0; s9 < 9; ++s9)
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt) sacc[mt] = mfma16(ka[2 * s9 + mt], qb[9 * bt + s9], sacc[mt]);
+          for (int nb = 0; nb < 2; ++nb) mp[nb] = *reinterpret_cast<const float*>(pr + 4 * (32 * pair + 16 * nb + i16));
         }
-        // online softmax (base 2); lane holds tokens 16mt + 4g + r of head `head`
+        // S^T over all 576 dims: K operands in batches of KB, the next batch requested before the
+        // products of the current one; every K operand feeds both head blocks
+        constexpr int KB = 3;
+        f32x4 sacc[2] = {f32x4{}, f32x4{}};
+        u32x4 ka[2][KB];
+#pragma unroll
+        for (int s6 = 0; s6 < KB; ++s6)
+          ka[0][s6] = *reinterpret_cast<const u32x4*>(tb + ((s6 & 1) ? k_odd : k_even) + (s6 >> 1) * 1024);
+#pragma unroll
+        for (int bt = 0; bt < 18 / KB; ++bt) {
+          if (bt + 1 < 18 / KB) {
+#pragma unroll
+            for (int s6 = 0; s6 < KB; ++s6) {
+              const int s = KB * (bt + 1) + s6;
+              ka[(bt + 1) & 1][s6] = *reinterpret_cast<const u32x4*>(tb + ((s & 1) ? k_odd : k_even) + (s >> 1) * 1024);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int s6 = 0; s6 < KB; ++s6)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) sacc[nb] = mfma16(ka[bt & 1][s6], qb[nb][KB * bt + s6], sacc[nb]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        // online softmax (base 2); lane holds tokens 16 th + 4g + r of heads 16 nb + i16
         uint32_t vmask;
         if constexpr (WIN) {
           const int64_t p = win0 + (int64_t)it * kMlaT + lj;
@@ -335,67 +365,64 @@ void mla_attn_kernel(AttnGeom a) {
         } else {
           vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
         }
-        if (vmask != 0xFFFFFFFFu) {  // partial or skipped tokens: mask them
+        const uint32_t hmask = (vmask >> (16 * th)) & 0xFFFFu;
+        if (hmask != 0xFFFFu) {  // partial or skipped tokens: mask them
 #pragma unroll
-          for (int mt = 0; mt < 2; ++mt)
+          for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int tk = 16 * mt + 4 * g + r;
-              sacc[mt][r] = ((vmask >> tk) & 1u) ? sacc[mt][r] : -INFINITY;
-            }
+            for (int r = 0; r < 4; ++r) sacc[nb][r] = ((hmask >> (4 * g + r)) & 1u) ? sacc[nb][r] : -INFINITY;
         }
-        float smax = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
-                           fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
-        smax = max4_xor16_32(smax);
-        const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
-        // the reference maximum moves only when a head's maximum grows by more than 2^8; the value
-        // wave rescales its accumulators by the factor left in the slot (1 otherwise)
-        float alpha = 1.f;
-        if (mx > m + kLazy) {
-          alpha = fast_exp2(m - mx);
-          l *= alpha;
-          m = mx;
-        }
-        const float mb = m == -INFINITY ? 0.f : m;  // m = -inf only while every score is -inf
-        float p[8];
+        uint8_t* slot = pslots + (it & 1) * kMlaPSlot;
 #pragma unroll
-        for (int mt = 0; mt < 2; ++mt)
+        for (int nb = 0; nb < 2; ++nb) {
+          float smax = fmaxf(fmaxf(sacc[nb][0], sacc[nb][1]), fmaxf(sacc[nb][2], sacc[nb][3]));
+          smax = max4_xor16_32(smax);
+          const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
+          // the reference maximum moves when a head's maximum grows by more than 2^8, or to the
+          // other half's reference when that is larger; the value wave reconciles the two halves
+          float tgt = mx > m[nb] + kLazy ? mx : m[nb];
+          tgt = fmaxf(tgt, mp[nb]);
+          if (tgt > m[nb]) {
+            l[nb] *= fast_exp2(m[nb] - tgt);
+            m[nb] = tgt;
+          }
+          const float mb = m[nb] == -INFINITY ? 0.f : m[nb];  // m = -inf only while every score is -inf
+          float p[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            p[4 * mt + r] = fast_exp2(fmaf(sacc[mt][r], a.scale_log2, -mb));  // -inf -> 0
-            l += p[4 * mt + r];
+            p[r] = fast_exp2(fmaf(sacc[nb][r], a.scale_log2, -mb));  // -inf -> 0
+            l[nb] += p[r];
           }
-        // P of tokens 4g .. 4g + 3 and 16 + 4g .. 16 + 4g + 3, bf16, into the head's row of the slot
-        const u32x4 pb = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                          pack_bf16x2(p[6], p[7])};
-        uint8_t* slot = pslots + (it & 1) * kMlaPSlot;
-        const int lh = 32 * pair + 16 * (w4 & 1) + i16;  // (pair, local head)
-        *reinterpret_cast<u32x2*>(slot + lh * kMlaPHead + 8 * g) = u32x2{pb.x, pb.y};        // tokens 4g ..
-        *reinterpret_cast<u32x2*>(slot + lh * kMlaPHead + 32 + 8 * g) = u32x2{pb.z, pb.w};   // tokens 16 + 4g ..
-        if (g == 0) *reinterpret_cast<float*>(slot + 64 * kMlaPHead + 4 * lh) = alpha;
+          // P of tokens 16 th + 4g .. + 3, bf16, into the head's row of the slot
+          const int lh = 32 * pair + 16 * nb + i16;  // (pair, local head)
+          *reinterpret_cast<u32x2*>(slot + lh * kMlaPHead + 32 * th + 8 * g) = u32x2{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
+          if (g == 0) *reinterpret_cast<float*>(slot + 64 * kMlaPHead + th * 256 + 4 * lh) = m[nb];
+        }
       }
     }
-    const float lt = sum4_xor16_32(l);
-    if (g == 0) {
-      const int lh = 32 * pair + 16 * (w4 & 1) + i16;
-      fin[2 * lh] = m;
-      fin[2 * lh + 1] = lt;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const float lt = sum4_xor16_32(l[nb]);
+      if (g == 0) {
+        const int lh = 32 * pair + 16 * nb + i16;
+        fin[2 * (64 * th + lh)] = m[nb];
+        fin[2 * (64 * th + lh) + 1] = lt;
+      }
     }
     __syncthreads();
     return;
   }
 
-  // ---- value wave (pair, dh) = (w4 >> 1, w4 & 1): O^T += V^T P^T for the 32 heads of the scorer
-  // pair and value columns 256 dh .. + 255, one tile behind the scorers, on 32x32x16 products
-  // (dims on the rows, heads on the columns, 16 tokens per k-step): every V byte is read by two
-  // value waves per tile. A operand of value block c (dims 256 dh + 32 c ..), k-step ks: lane l
-  // holds dim l % 32, tokens 16 ks + 8 (l / 32) + 0..7, from two transposed reads; in 16-lane
-  // group G = l / 16, source lane s of read r supplies token 16 ks + 8 (G / 2) + 4 r + s / 4,
-  // dims 256 dh + 32 c + 16 (G % 2) + 4 (s % 4) .. + 3: chunk 32 dh + 4 c + 2 (G % 2) + (s % 4) / 2,
-  // i.e. block 9 (2 ks + G / 2) + 4 dh + c / 2, chunk 4 (c % 2) + 2 (G % 2) + (s % 4) / 2 of it. The
+  // ---- value wave w4: O^T += V^T P^T for all 64 (pair, local head) columns and value columns
+  // 128 w4 .. + 127, one tile behind the scorers, on 32x32x16 products (dims on the rows, heads on
+  // the columns, 16 tokens per k-step): every V operand feeds both head blocks, and every V byte is
+  // read by one value wave per tile. A operand of value block c (dims 128 w4 + 32 c ..), k-step ks:
+  // lane l holds dim l % 32, tokens 16 ks + 8 (l / 32) + 0..7, from two transposed reads; in
+  // 16-lane group G = l / 16, source lane s of read r supplies token 16 ks + 8 (G / 2) + 4 r + s / 4,
+  // dims 128 w4 + 32 c + 16 (G % 2) + 4 (s % 4) .. + 3: chunk 16 w4 + 4 c + 2 (G % 2) + (s % 4) / 2,
+  // i.e. block 9 (2 ks + G / 2) + 2 w4 + c / 2, chunk 4 (c % 2) + 2 (G % 2) + (s % 4) / 2 of it. The
   // swizzle depends on the token row and o % 2 only, so there is one base offset per (r, c % 2) and
   // the rest is an immediate (ks * 18 KB, (c / 2) KB).
-  const int dh = w4 & 1;
   const int G = lane >> 4, sl = lane & 15;
   int v_off[2][2];
 #pragma unroll
@@ -403,13 +430,14 @@ void mla_attn_kernel(AttnGeom a) {
 #pragma unroll
     for (int par = 0; par < 2; ++par) {
       const int tk = 8 * (G >> 1) + 4 * r + (sl >> 2), o = tk >> 3, j = tk & 7;
-      const int ch = 4 * par + 2 * (G & 1) + ((sl >> 1) & 1);  // chunk within the block 9 o + 4 dh + c / 2
-      v_off[r][par] = (9 * o + 4 * dh) * 1024 + (8 * j + (ch ^ mla_swz(o, j))) * 16 + (sl & 1) * 8;
+      const int ch = 4 * par + 2 * (G & 1) + ((sl >> 1) & 1);  // chunk within the block 9 o + 2 w4 + c / 2
+      v_off[r][par] = (9 * o + 2 * w4) * 1024 + (8 * j + (ch ^ mla_swz(o, j))) * 16 + (sl & 1) * 8;
     }
-  const int lh = 32 * pair + (lane & 31);  // (pair, local head) of this lane's accumulator column
-  f32x16 o[8];
+  const int oj = lane & 31;  // local head of this lane's accumulator column in each head block
+  f32x16 o[8];               // block 4 hb + c: heads 32 hb .., dims 128 w4 + 32 c ..
 #pragma unroll
   for (int c = 0; c < 8; ++c) o[c] = f32x16{};
+  float m_o[2] = {-INFINITY, -INFINITY};  // reference maxima of the accumulators
   // Direct load k of value wave w4 fills block 9 w4 + k (tokens 8 w4.., chunks 8k..): lane 8j + u
   // takes token 8 w4 + j, chunk 8k + (u ^ mla_swz(w4, j)), 16 bytes of one 128-byte line per lane.
   const int dj = lane >> 3;
@@ -441,77 +469,113 @@ void mla_attn_kernel(AttnGeom a) {
       next_off = t0;
       if (it == 0) continue;  // (nothing scored yet)
       const uint8_t* slot = pslots + ((it - 1) & 1) * kMlaPSlot;
-      // B operand P^T of k-step ks: head lh, tokens 16 ks + 8 (l / 32) .. + 7
-      const u32x4 pb0 = *reinterpret_cast<const u32x4*>(slot + lh * kMlaPHead + 16 * (lane >> 5));
-      const u32x4 pb1 = *reinterpret_cast<const u32x4*>(slot + lh * kMlaPHead + 32 + 16 * (lane >> 5));
-      const float alpha = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 4 * lh);
-      if (__ballot(alpha != 1.f)) {  // rare after the first tile
+      // B operand P^T of head block hb, k-step ks: head 32 hb + oj, tokens 16 ks + 8 (l / 32) .. + 7
+      u32x4 pb[2][2];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[c] *= alpha;
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+          pb[hb][ks] = *reinterpret_cast<const u32x4*>(slot + (32 * hb + oj) * kMlaPHead + 32 * ks + 16 * (lane >> 5));
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        const float mA = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 4 * (32 * hb + oj));
+        const float mB = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 256 + 4 * (32 * hb + oj));
+        const float mn = fmaxf(mA, mB);  // >= m_o: the references never decrease
+        if (__ballot(mA != mB || mn > m_o[hb])) {  // rare once the halves agree
+          const float alpha = mn > m_o[hb] ? fast_exp2(m_o[hb] - mn) : 1.f;  // m_o = -inf -> 0
+          m_o[hb] = mn;
+          if (__ballot(alpha != 1.f)) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) o[4 * hb + c] *= alpha;
+          }
+          // P of the half whose reference is below m_o, brought to m_o
+          const float fa = mA == mn ? 1.f : fast_exp2(mA - mn), fb = mB == mn ? 1.f : fast_exp2(mB - mn);
+          if (__ballot(fa != 1.f)) pb[hb][0] = scale_bf16x8(pb[hb][0], fa);
+          if (__ballot(fb != 1.f)) pb[hb][1] = scale_bf16x8(pb[hb][1], fb);
+        }
       }
-      // V operands of four value blocks (both k-steps) at a time, each batch requested before its products
+      // V operands of the four value blocks (both k-steps), requested before the products
+      u32x4 va[4][2];
 #pragma unroll
-      for (int c4 = 0; c4 < 8; c4 += 4) {
-        u32x4 va[8];
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const uint8_t* b0 = tp + v_off[0][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
+          const uint8_t* b1 = tp + v_off[1][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
+          va[c][ks] = tr16_pair(b0, b1);
+        }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int c = 0; c < 4; ++c)
 #pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            const int cc = c4 + c;
-            const uint8_t* b0 = tp + v_off[0][cc & 1] + ks * kMlaHalf + (cc >> 1) * 1024;
-            const uint8_t* b1 = tp + v_off[1][cc & 1] + ks * kMlaHalf + (cc >> 1) * 1024;
-            va[2 * c + ks] = tr16_pair(b0, b1);
-          }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) o[c4 + c] = mfma32(va[2 * c], pb0, o[c4 + c]);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) o[c4 + c] = mfma32(va[2 * c + 1], pb1, o[c4 + c]);
-      }
+          for (int hb = 0; hb < 2; ++hb) o[4 * hb + c] = mfma32(va[c][ks], pb[hb][ks], o[4 * hb + c]);
     }
   }
   __syncthreads();  // the scorers' reference maxima and sums
-  const float mfin = fin[2 * lh], lt = fin[2 * lh + 1];
-  // accumulator layout: lane l, register r of block c holds dim 256 dh + 32 c + 8 (r / 4) +
-  // 4 (l / 32) + r % 4 of head (WIN ? 32 blockIdx.y : 32 pair) + l % 32
-  const int vhead = (WIN ? 32 * (int)blockIdx.y : 32 * pair) + (lane & 31);
-  const int dv0 = 256 * dh + 4 * (lane >> 5);
+  // accumulator layout: lane l, register r of block 4 hb + c holds dim 128 w4 + 32 c + 8 (r / 4) +
+  // 4 (l / 32) + r % 4 of local head 32 hb + l % 32: in the list kernel head 32 hb + l % 32 of the
+  // row, in the window kernel head 32 blockIdx.y + l % 32 of row 2 item + hb
+  float mfin[2], lt[2];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb) {
+    // the two token halves' sums brought to the accumulators' reference (the larger final maximum)
+    const int lh = 32 * hb + oj;
+    const float ma = fin[2 * lh], la = fin[2 * lh + 1], mb = fin[2 * (64 + lh)], lb = fin[2 * (64 + lh) + 1];
+    mfin[hb] = fmaxf(ma, mb);
+    lt[hb] = (ma == mfin[hb] ? la : la * fast_exp2(ma - mfin[hb])) + (mb == mfin[hb] ? lb : lb * fast_exp2(mb - mfin[hb]));
+  }
   if (!SPLIT) {
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    // the normalised O of this wave (32 heads x 256 value columns, bf16) is staged head-major in
-    // the tile buffers, idle since the barrier above (528 bytes per head: 512 + 16 of padding),
-    // and written as whole 512-byte head rows, two rows per store instruction, instead of 8-byte
-    // pieces of 32 rows (0.4 ms of the ≈1.9 ms the output stores cost per launch at L = 128K)
-    uint8_t* ost = lds + w4 * (32 * 528);
-    const int oj = lane & 31;
+    // the normalised O of this wave (64 heads x 128 value columns, bf16) is staged head-major in
+    // the tile buffers, idle since the barrier above (272 bytes per head: 256 + 16 of padding),
+    // and written as 256-byte pieces of the head rows, four per store instruction
+    uint8_t* ost = lds + w4 * (64 * 272);
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
+    for (int hb = 0; hb < 2; ++hb) {
+      const float inv = lt[hb] > 0.f ? 1.f / lt[hb] : 0.f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const u32x2 v = {pack_bf16x2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
-                         pack_bf16x2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
-        *reinterpret_cast<u32x2*>(ost + oj * 528 + (32 * c + 8 * q + 4 * (lane >> 5)) * 2) = v;
-      }
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x16& ob = o[4 * hb + c];
+          const u32x2 v = {pack_bf16x2(ob[4 * q] * inv, ob[4 * q + 1] * inv),
+                           pack_bf16x2(ob[4 * q + 2] * inv, ob[4 * q + 3] * inv)};
+          *reinterpret_cast<u32x2*>(ost + (32 * hb + oj) * 272 + (32 * c + 8 * q + 4 * (lane >> 5)) * 2) = v;
+        }
+    }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // (this wave's staging writes are done)
-    const int vbase = WIN ? 32 * (int)blockIdx.y : 32 * pair;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-      const int hh = 2 * k + (lane >> 5);
-      const u32x4 v = *reinterpret_cast<const u32x4*>(ost + hh * 528 + 16 * oj);
-      *reinterpret_cast<u32x4*>(a.out + (row * 64 + vbase + hh) * 512 + 256 * dh + 8 * oj) = v;
+      const int hh = 4 * k + (lane >> 4);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(ost + hh * 272 + 16 * (lane & 15));
+      *reinterpret_cast<u32x4*>(a.out + (row * 64 + hh) * 512 + 128 * w4 + 8 * (lane & 15)) = v;
     }
-    if (a.lse && dh == 0 && lane < 32) a.lse[row * 64 + vhead] = lt > 0.f ? (mfin + __log2f(lt)) * kLn2 : -INFINITY;
-  } else if (row_ok) {
-    const int64_t pi = (row * a.n_split + split) * 64 + vhead;
-    float* po = a.part_o + pi * 512 + dv0;
+    if (a.lse && w4 == 0 && lane < 32) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
+      for (int hb = 0; hb < 2; ++hb)
+        a.lse[row * 64 + 32 * hb + oj] = lt[hb] > 0.f ? (mfin[hb] + __log2f(lt[hb])) * kLn2 : -INFINITY;
+    }
+  } else {
+    const int dv0 = 128 * w4 + 4 * (lane >> 5);
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<f32x4*>(po + 32 * c + 8 * q) = f32x4{o[c][4 * q], o[c][4 * q + 1], o[c][4 * q + 2], o[c][4 * q + 3]};
-    if (dh == 0 && lane < 32) {
-      a.part_ml[pi * 2] = mfin;
-      a.part_ml[pi * 2 + 1] = lt;
+    for (int hb = 0; hb < 2; ++hb) {
+      const int64_t orow = WIN ? 2 * item + hb : row;
+      if (orow >= a.n_rows) continue;  // WIN: the second row of an odd count
+      const int ohead = (WIN ? 32 * (int)blockIdx.y : 32 * hb) + oj;
+      const int64_t pi = (orow * a.n_split + split) * 64 + ohead;
+      float* po = a.part_o + pi * 512 + dv0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x16& ob = o[4 * hb + c];
+          *reinterpret_cast<f32x4*>(po + 32 * c + 8 * q) = f32x4{ob[4 * q], ob[4 * q + 1], ob[4 * q + 2], ob[4 * q + 3]};
+        }
+      if (w4 == 0 && lane < 32) {
+        a.part_ml[pi * 2] = mfin[hb];
+        a.part_ml[pi * 2 + 1] = lt[hb];
+      }
     }
   }
 }
