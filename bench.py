@@ -44,9 +44,12 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    """SHA-256 of the attention kernel's sources with comments and blank lines removed, so that
-    an edit of the comments alone keeps the committed traffic figure valid."""
+    """SHA-256 of the attention kernel's sources with comments and blank lines removed (so that
+    an edit of the comments alone keeps the committed traffic figure valid), and of the extra
+    compiler flags of attention.hip."""
+    from paper_2608_01662_amd.build import EXTRA_FLAGS
     h = hashlib.sha256()
+    h.update((" ".join(EXTRA_FLAGS.get("attention.hip", [])) + "\n").encode())
     for f in KERNEL_SOURCES:
         with open(f) as fh:
             text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)

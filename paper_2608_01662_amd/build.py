@@ -27,7 +27,10 @@ HIPCC_FLAGS = [
 
 # Per-source extra flags. The indexer's MFMA accumulators are reduced by vector code right after
 # each product chain: keeping them in VGPRs (not AGPRs) saves a register copy per element.
-EXTRA_FLAGS = {"indexer.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# The attention kernels never produce a NaN from finite inputs (masked scores are -inf and every
+# difference of two -inf is guarded): without NaN semantics the softmax maxima compile to plain
+# v_max_f32, without the canonicalising v_max_f32 x, x, x in front of each operand.
+EXTRA_FLAGS = {"indexer.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"], "attention.hip": ["-fno-honor-nans"]}
 
 
 def _hipcc() -> str:

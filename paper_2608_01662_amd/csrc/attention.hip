@@ -326,7 +326,11 @@ void mla_attn_kernel(AttnGeom a) {
         const uint8_t* tb = lds + __builtin_amdgcn_readfirstlane(cur_off);
         cur_off = cur_off + kMlaTile == kMlaBufs * kMlaTile ? 0 : cur_off + kMlaTile;
         if (it == ntiles) continue;  // (the value waves' last tile)
-        // the other token half's reference maxima of tile it - 1 (adopted when larger)
+        // issued first, so that their LDS round trips overlap the products: this lane's list entry
+        // of the tile (softmax mask) and the other token half's reference maxima of tile it - 1
+        // (adopted when larger)
+        int idv = 0;
+        if constexpr (!WIN) idv = ids[it * kMlaT + lj];
         float mp[2] = {-INFINITY, -INFINITY};
         if (it > 0) {
           const uint8_t* pr = pslots + ((it - 1) & 1) * kMlaPSlot + 64 * kMlaPHead + (1 - th) * 256;
@@ -363,7 +367,7 @@ void mla_attn_kernel(AttnGeom a) {
           const int64_t p = win0 + (int64_t)it * kMlaT + lj;
           vmask = (uint32_t)__ballot(p >= w_lo && p <= w_hi);
         } else {
-          vmask = (uint32_t)__ballot(ids[it * kMlaT + lj] >= 0);
+          vmask = (uint32_t)__ballot(idv >= 0);
         }
         const uint32_t hmask = (vmask >> (16 * th)) & 0xFFFFu;
         if (hmask != 0xFFFFu) {  // partial or skipped tokens: mask them
@@ -443,8 +447,7 @@ void mla_attn_kernel(AttnGeom a) {
   const int dj = lane >> 3;
   const int dma_tok = 8 * w4 + dj;
   const int64_t dma_col = ((lane & 7) ^ mla_swz(w4, dj)) * 16;
-  auto issue = [&](int tile, uint32_t buf_off) {
-    const int r = tile_row(tile, dma_tok);
+  auto issue = [&](int r, uint32_t buf_off) {
     const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
     const uint8_t* const srcs[kMlaLoads] = {src,       src + 128, src + 256, src + 384,  src + 512,
                                             src + 640, src + 768, src + 896, src + 1024};
@@ -455,13 +458,15 @@ void mla_attn_kernel(AttnGeom a) {
     const int ntiles = (nc + kMlaT - 1) / kMlaT;
     if constexpr (!WIN) stage(c0, nc, ntiles);
     __syncthreads();
-    if (ntiles > 0) issue(0, 0);
+    if (ntiles > 0) issue(tile_row(0, dma_tok), 0);
+    int nrow = ntiles > 1 ? tile_row(1, dma_tok) : -1;  // row of this lane's next load, read a tile ahead
     // buffer byte offsets rotated as wave-uniform scalars: tile it - 1 (read now), it, it + 1
     uint32_t prev_off = 2 * kMlaTile, cur_off = 0, next_off = kMlaTile;
     for (int it = 0; it <= ntiles; ++it) {
       // tile it has landed; the scorers' P of tile it - 1 is in its slot; tile it - 2 is free
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      if (it + 1 < ntiles) issue(it + 1, next_off);
+      if (it + 1 < ntiles) issue(nrow, next_off);
+      if (it + 2 < ntiles) nrow = tile_row(it + 2, dma_tok);
       const uint8_t* tp = lds + __builtin_amdgcn_readfirstlane(prev_off);
       const uint32_t t0 = prev_off;
       prev_off = cur_off;
@@ -469,6 +474,13 @@ void mla_attn_kernel(AttnGeom a) {
       next_off = t0;
       if (it == 0) continue;  // (nothing scored yet)
       const uint8_t* slot = pslots + ((it - 1) & 1) * kMlaPSlot;
+      // all LDS reads of the tile first (reference maxima, P, V), then the rescale checks
+      float mA[2], mB[2];
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        mA[hb] = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 4 * (32 * hb + oj));
+        mB[hb] = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 256 + 4 * (32 * hb + oj));
+      }
       // B operand P^T of head block hb, k-step ks: head 32 hb + oj, tokens 16 ks + 8 (l / 32) .. + 7
       u32x4 pb[2][2];
 #pragma unroll
@@ -476,25 +488,7 @@ void mla_attn_kernel(AttnGeom a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
           pb[hb][ks] = *reinterpret_cast<const u32x4*>(slot + (32 * hb + oj) * kMlaPHead + 32 * ks + 16 * (lane >> 5));
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        const float mA = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 4 * (32 * hb + oj));
-        const float mB = *reinterpret_cast<const float*>(slot + 64 * kMlaPHead + 256 + 4 * (32 * hb + oj));
-        const float mn = fmaxf(mA, mB);  // >= m_o: the references never decrease
-        if (__ballot(mA != mB || mn > m_o[hb])) {  // rare once the halves agree
-          const float alpha = mn > m_o[hb] ? fast_exp2(m_o[hb] - mn) : 1.f;  // m_o = -inf -> 0
-          m_o[hb] = mn;
-          if (__ballot(alpha != 1.f)) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) o[4 * hb + c] *= alpha;
-          }
-          // P of the half whose reference is below m_o, brought to m_o
-          const float fa = mA == mn ? 1.f : fast_exp2(mA - mn), fb = mB == mn ? 1.f : fast_exp2(mB - mn);
-          if (__ballot(fa != 1.f)) pb[hb][0] = scale_bf16x8(pb[hb][0], fa);
-          if (__ballot(fb != 1.f)) pb[hb][1] = scale_bf16x8(pb[hb][1], fb);
-        }
-      }
-      // V operands of the four value blocks (both k-steps), requested before the products
+      // V operands of the four value blocks (both k-steps)
       u32x4 va[4][2];
 #pragma unroll
       for (int c = 0; c < 4; ++c)
@@ -504,6 +498,23 @@ void mla_attn_kernel(AttnGeom a) {
           const uint8_t* b1 = tp + v_off[1][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
           va[c][ks] = tr16_pair(b0, b1);
         }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        const float mn = fmaxf(mA[hb], mB[hb]);  // >= m_o: the references never decrease
+        if (__ballot(mA[hb] != mB[hb] || mn > m_o[hb])) {  // rare once the halves agree
+          const float alpha = mn > m_o[hb] ? fast_exp2(m_o[hb] - mn) : 1.f;  // m_o = -inf -> 0
+          m_o[hb] = mn;
+          if (__ballot(alpha != 1.f)) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) o[4 * hb + c] *= alpha;
+          }
+          // P of the half whose reference is below m_o, brought to m_o
+          const float fa = mA[hb] == mn ? 1.f : fast_exp2(mA[hb] - mn), fb = mB[hb] == mn ? 1.f : fast_exp2(mB[hb] - mn);
+          if (__ballot(fa != 1.f)) pb[hb][0] = scale_bf16x8(pb[hb][0], fa);
+          if (__ballot(fb != 1.f)) pb[hb][1] = scale_bf16x8(pb[hb][1], fb);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
