@@ -462,19 +462,35 @@ void mla_attn_kernel(AttnGeom a) {
     int nrow = ntiles > 1 ? tile_row(1, dma_tok) : -1;  // row of this lane's next load, read a tile ahead
     // buffer byte offsets rotated as wave-uniform scalars: tile it - 1 (read now), it, it + 1
     uint32_t prev_off = 2 * kMlaTile, cur_off = 0, next_off = kMlaTile;
+    u32x4 va[4][2];  // V operands of tile it - 1, read in the previous iteration
     for (int it = 0; it <= ntiles; ++it) {
       // tile it has landed; the scorers' P of tile it - 1 is in its slot; tile it - 2 is free
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
       if (it + 1 < ntiles) issue(nrow, next_off);
       if (it + 2 < ntiles) nrow = tile_row(it + 2, dma_tok);
-      const uint8_t* tp = lds + __builtin_amdgcn_readfirstlane(prev_off);
       const uint32_t t0 = prev_off;
       prev_off = cur_off;
       cur_off = next_off;
       next_off = t0;
-      if (it == 0) continue;  // (nothing scored yet)
+      // V operands of tile it (landed), for the products of the next iteration: four value
+      // blocks, both k-steps
+      auto read_v = [&]() {
+        const uint8_t* tp = lds + __builtin_amdgcn_readfirstlane(prev_off);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            const uint8_t* b0 = tp + v_off[0][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
+            const uint8_t* b1 = tp + v_off[1][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
+            va[c][ks] = tr16_pair(b0, b1);
+          }
+      };
+      if (it == 0) {  // (nothing scored yet)
+        read_v();
+        continue;
+      }
       const uint8_t* slot = pslots + ((it - 1) & 1) * kMlaPSlot;
-      // all LDS reads of the tile first (reference maxima, P, V), then the rescale checks
+      // the tile's LDS reads first (reference maxima, P; V was read a tile ahead), then the checks
       float mA[2], mB[2];
 #pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
@@ -488,16 +504,6 @@ void mla_attn_kernel(AttnGeom a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks)
           pb[hb][ks] = *reinterpret_cast<const u32x4*>(slot + (32 * hb + oj) * kMlaPHead + 32 * ks + 16 * (lane >> 5));
-      // V operands of the four value blocks (both k-steps)
-      u32x4 va[4][2];
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const uint8_t* b0 = tp + v_off[0][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
-          const uint8_t* b1 = tp + v_off[1][c & 1] + ks * kMlaHalf + (c >> 1) * 1024;
-          va[c][ks] = tr16_pair(b0, b1);
-        }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
@@ -522,6 +528,10 @@ void mla_attn_kernel(AttnGeom a) {
         for (int c = 0; c < 4; ++c)
 #pragma unroll
           for (int hb = 0; hb < 2; ++hb) o[4 * hb + c] = mfma32(va[c][ks], pb[hb][ks], o[4 * hb + c]);
+      if (it < ntiles) {
+        __builtin_amdgcn_sched_barrier(0);
+        read_v();
+      }
     }
   }
   __syncthreads();  // the scorers' reference maxima and sums
