@@ -125,6 +125,76 @@ def test_closed_forms_and_edge_lists(attn):
         P.check_attention_row(o[i], l[i], oref, lref, f"row {i}")
 
 
+# Rows whose scores jump far above everything before them at chosen list positions: (list length,
+# [(list position, log2 margin of the jump over the largest background score of every head)]).
+# Position 32 t + x lies in tile t, token half x // 16 of the MLA kernel's tiles. A margin above 8
+# moves the lazy reference maximum of the half that holds the jump; the other half then differs
+# for a tile (or to the end of the list, when the jump is in the last tile).
+_SPIKE_ROWS = [
+    (300, [(2 * 32 + 20, 9.5)]),                      # mid-list, second half
+    (300, [(4 * 32 + 3, 9.5)]),                       # mid-list, first half
+    (310, [(9 * 32 + 18, 9.5)]),                      # last (partial) tile, second half
+    (300, [(32 + 5, 9.5), (6 * 32 + 24, 19.0)]),      # two jumps, one per half
+    (300, [(3 * 32 + 5, 9.5), (3 * 32 + 25, 9.5)]),   # both halves of one tile
+    (300, [(0, 9.5)]),                                # the first entry
+    (20, [(18, 9.5)]),                                # one partial tile
+    (300, [(7 * 32 + 10, 9.5), (7 * 32 + 11, 12.0)]),  # two in one half of one tile
+]
+
+
+def _spike_inputs(w, k_cap=320):
+    """Queries q_h = q0 + 0.1 noise per row (every head scores a vector along q0 alike), background
+    cache rows N(0, 0.25), and per jump a cache row c * q0 / |q0| with c chosen so that every head's
+    score of it exceeds that head's largest background score of the row by the listed margin (log2
+    units). Returns bf16 bits of Q [rows, H, 576] and of the cache, and the index lists."""
+    H, dqk, dv = w.attn_dims
+    g = np.random.default_rng(11)
+    n_kv, n_rows = w.seq_len, len(_SPIKE_ROWS)
+    n_bg = n_kv - 2 * n_rows  # the last 2 rows per test row hold its jumps
+    q0 = g.standard_normal((n_rows, dqk))
+    q_bits = orc.f64_to_bf16_bits(q0[:, None, :] + 0.1 * g.standard_normal((n_rows, H, dqk)))
+    kv_bits = orc.f64_to_bf16_bits(0.5 * g.standard_normal((n_kv, dqk)))
+    qf = orc.bf16_bits_to_f64(q_bits)
+    idx = np.full((n_rows, k_cap), -1, np.int32)
+    cnt = np.zeros(n_rows, np.int32)
+    to_log2 = w.sm_scale / np.log(2.0)
+    for i, (n, spikes) in enumerate(_SPIKE_ROWS):
+        bg = g.choice(n_bg, n - len(spikes), replace=False)
+        bgmax = (qf[i] @ orc.bf16_bits_to_f64(kv_bits[bg]).T).max(axis=1) * to_log2  # per head
+        u = q0[i] / np.linalg.norm(q0[i])
+        d = (qf[i] @ u) * to_log2  # per head, per unit of c
+        lst = [int(r) for r in bg]
+        for j, (pos, margin) in enumerate(spikes):
+            r = n_bg + 2 * i + j
+            kv_bits[r] = orc.f64_to_bf16_bits(np.max((bgmax + margin) / d) * u)
+            lst.insert(pos, r)
+        idx[i, :n] = lst
+        cnt[i] = n
+    return q_bits, kv_bits, idx, cnt
+
+
+@pytest.mark.parametrize("copies", [1, 32], ids=["8_rows_split", "256_rows_one_pass"])
+def test_softmax_reference_jumps(copies):
+    """Scores that jump by more than 2^8 mid-list, in either token half of a tile, in both, twice,
+    at the first entry and in the last partial tile: the lazy reference maxima of the two token
+    halves then differ for a tile (or to the end), and the output must still equal Eq. 3 (oracle).
+    8 rows are planned as 32-entry pieces merged by log-sum-exp; 256 rows (each row 32 times) as
+    one pass per row, where the halves' maxima are reconciled across the tiles of the row."""
+    from dataclasses import replace
+    w = replace(W.SMALL_MLA, seq_len=2048)
+    H, dqk, dv = w.attn_dims
+    q_bits, kv_bits, idx, cnt = _spike_inputs(w)
+    n = len(cnt)
+    a = dict(q=np.tile(q_bits, (copies, 1, 1)), kv=kv_bits, v=None)
+    idx_c, cnt_c = np.tile(idx, (copies, 1)), np.tile(cnt, copies)
+    o, l = _gpu_attn(w, a, list(range(n * copies)), idx_c, cnt_c)
+    for i in range(n):
+        oref, lref = orc.attention_for_set(q_bits[i], kv_bits, None, idx[i, :cnt[i]], dv, w.sm_scale)
+        P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({_SPIKE_ROWS[i]})")
+        for c in range(1, copies):  # same row, same result
+            assert np.array_equal(o[c * n + i], o[i]) and np.array_equal(l[c * n + i], l[i]), f"row {i} copy {c}"
+
+
 def test_long_lists_beyond_one_staging_pass():
     """MLA index lists longer than the 8192 entries the kernel stages in LDS at a time: the list is
     walked in several passes (8192 = exactly one pass, 8193 = one entry into the second, and two
