@@ -79,6 +79,51 @@ constexpr int kMlaPSlot = 64 * kMlaPHead + 2 * 64 * 4;  // per tile parity: P of
 __device__ __forceinline__ int mla_swz(int o, int j) { return ((j & 2) << 1) | ((j & 4) >> 1) | (o & 1); }
 constexpr int kMlaHalf = 18 * 1024;  // the second 16 tokens of a tile start 18 blocks later
 constexpr int kMlaIdCap = 8192;      // index-list entries staged in LDS at a time
+// Nine direct loads of one 1152-byte row piece per lane: load k reads the 16 bytes at src + 128 k
+// and writes LDS bytes [lds + 1024 k + 16 lane, +16). The loads share one address and carry
+// 128 k as their immediate offset, which these loads add to the LDS address as well, so M0 steps
+// by 1024 - 128 per load. Written as one asm block so that the compiler does not see LDS being
+// written by vector-memory loads: it would otherwise drain every such load in flight before any
+// later LDS read it cannot prove disjoint; callers order the loads with explicit vmcnt waits and
+// barriers. M0, which holds the LDS address of the loads, is saved and restored; the s_nop after
+// each write of M0 is the wait state before a load may read it.
+__device__ __forceinline__ void lds_dma_row9(const uint8_t* src, uint32_t lds) {
+  uint32_t save;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:128\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:256\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:384\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:512\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:640\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:768\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:896\n\t"
+      "s_add_u32 m0, m0, 0x380\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off offset:1024\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(save)
+      : "v"(src), "s"(lds)
+      : "memory", "scc");
+}
+
 // eight bf16 scaled by f (rounded to nearest even again)
 __device__ __forceinline__ u32x4 scale_bf16x8(u32x4 v, float f) {
   u32x4 r;
@@ -448,10 +493,7 @@ void mla_attn_kernel(AttnGeom a) {
   const int dma_tok = 8 * w4 + dj;
   const int64_t dma_col = ((lane & 7) ^ mla_swz(w4, dj)) * 16;
   auto issue = [&](int r, uint32_t buf_off) {
-    const uint8_t* src = kvb + (r >= 0 ? (int64_t)r * 1152 : 0) + dma_col;
-    const uint8_t* const srcs[kMlaLoads] = {src,       src + 128, src + 256, src + 384,  src + 512,
-                                            src + 640, src + 768, src + 896, src + 1024};
-    lds_dma16x9(srcs, lds_addr(lds + buf_off + w4 * (kMlaLoads * 1024)));
+    lds_dma_row9(kvb + (int64_t)(r > 0 ? r : 0) * 1152 + dma_col, lds_addr(lds + buf_off + w4 * (kMlaLoads * 1024)));
   };
   for (int c0 = 0; c0 < n; c0 += kPass) {
     const int nc = n - c0 < kPass ? n - c0 : kPass;

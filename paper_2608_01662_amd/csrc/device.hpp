@@ -103,49 +103,6 @@ __device__ __forceinline__ void lds_done_barrier() {
 __device__ __forceinline__ void block_sync() { __syncthreads(); }
 
 // ---------------------------------------------------------------- direct global -> LDS loads
-// Nine loads of 16 bytes per lane: load k reads 16 bytes at src[k] and writes LDS bytes
-// [lds + 1024k + 16 lane, +16). Written as one asm block so that the compiler does not see LDS
-// being written by vector-memory loads: it would otherwise drain every such load in flight before
-// any later LDS read it cannot prove disjoint. Callers order these loads with explicit vmcnt
-// waits and barriers. M0, which holds the LDS base of the loads, is saved and restored; the
-// s_nop after each write of M0 is the wait state before a load may read it.
-__device__ __forceinline__ void lds_dma16x9(const uint8_t* const (&src)[9], uint32_t lds) {
-  uint32_t save;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %10\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %2, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %3, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %4, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %5, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %6, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %7, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %8, off\n\t"
-      "s_add_u32 m0, m0, 0x400\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %9, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(save)
-      : "v"(src[0]), "v"(src[1]), "v"(src[2]), "v"(src[3]), "v"(src[4]), "v"(src[5]), "v"(src[6]), "v"(src[7]),
-        "v"(src[8]), "s"(lds)
-      : "memory", "scc");
-}
 // LDS byte address of a pointer into __shared__ memory (the low 32 bits of its generic address).
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
