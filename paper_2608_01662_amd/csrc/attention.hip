@@ -124,6 +124,21 @@ __device__ __forceinline__ void lds_dma_row9(const uint8_t* src, uint32_t lds) {
       : "memory", "scc");
 }
 
+// The maxima of x and of y over the four 16-lane rows (lanes l, l ^ 16, l ^ 32, l ^ 48), sharing
+// the lane swaps: the first swap leaves rows (x0, y0, x2, y2) and (x1, y1, x3, y3), the second
+// (row halves) rows x, y, x, y of the full maxima, the last hands each lane both.
+__device__ __forceinline__ void max4_xor16_32_pair(float& x, float& y) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+  const float z = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(z), __float_as_uint(z), false, false);
+  const float w = fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  const auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(w), __float_as_uint(w), false, false);
+  x = __uint_as_float(c[0]);
+  y = __uint_as_float(c[1]);
+}
+constexpr float kNoRef = -3.40282347e38f;  // reference maximum before a head's first score (finite, so
+                                           // exp2(s - m) needs no guard: masked scores are -inf)
+
 // eight bf16 scaled by f (rounded to nearest even again)
 __device__ __forceinline__ u32x4 scale_bf16x8(u32x4 v, float f) {
   u32x4 r;
@@ -358,7 +373,7 @@ void mla_attn_kernel(AttnGeom a) {
     const int k_row = th * kMlaHalf + 9 * (i16 >> 3) * 1024 + 8 * (i16 & 7) * 16;
     const int k_even = k_row + ((0 + g) ^ ksw) * 16, k_odd = k_row + ((4 + g) ^ ksw) * 16;
     const int lj = lane & 31;  // token of this lane's validity bit in the softmax mask
-    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+    float m[2] = {kNoRef, kNoRef}, l[2] = {0.f, 0.f};
     for (int c0 = 0; c0 < n; c0 += kPass) {
       const int nc = n - c0 < kPass ? n - c0 : kPass;
       const int ntiles = (nc + kMlaT - 1) / kMlaT;
@@ -422,24 +437,26 @@ void mla_attn_kernel(AttnGeom a) {
             for (int r = 0; r < 4; ++r) sacc[nb][r] = ((hmask >> (4 * g + r)) & 1u) ? sacc[nb][r] : -INFINITY;
         }
         uint8_t* slot = pslots + (it & 1) * kMlaPSlot;
+        float smx[2];
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) smx[nb] = fmaxf(fmaxf(sacc[nb][0], sacc[nb][1]), fmaxf(sacc[nb][2], sacc[nb][3]));
+        max4_xor16_32_pair(smx[0], smx[1]);
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
-          float smax = fmaxf(fmaxf(sacc[nb][0], sacc[nb][1]), fmaxf(sacc[nb][2], sacc[nb][3]));
-          smax = max4_xor16_32(smax);
-          const float mx = smax * a.scale_log2;  // scale > 0: max commutes with scaling
+          const float mx = smx[nb] * a.scale_log2;  // scale > 0: max commutes with scaling
           // the reference maximum moves when a head's maximum grows by more than 2^8, or to the
           // other half's reference when that is larger; the value wave reconciles the two halves
           float tgt = mx > m[nb] + kLazy ? mx : m[nb];
           tgt = fmaxf(tgt, mp[nb]);
-          if (tgt > m[nb]) {
-            l[nb] *= fast_exp2(m[nb] - tgt);
-            m[nb] = tgt;
+          const bool up = tgt > m[nb];
+          if (__ballot(up)) {  // rare once a row's scores have settled
+            l[nb] = up ? l[nb] * fast_exp2(m[nb] - tgt) : l[nb];
+            m[nb] = up ? tgt : m[nb];
           }
-          const float mb = m[nb] == -INFINITY ? 0.f : m[nb];  // m = -inf only while every score is -inf
           float p[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            p[r] = fast_exp2(fmaf(sacc[nb][r], a.scale_log2, -mb));  // -inf -> 0
+            p[r] = fast_exp2(fmaf(sacc[nb][r], a.scale_log2, -m[nb]));  // -inf -> 0
             l[nb] += p[r];
           }
           // P of tokens 16 th + 4g .. + 3, bf16, into the head's row of the slot
