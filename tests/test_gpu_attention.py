@@ -217,6 +217,35 @@ def test_long_lists_beyond_one_staging_pass():
         P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({cnt[i]} entries)")
 
 
+def test_many_rows_mixed_lists():
+    """Calls of 256 rows or more run one pass over each row's whole list (no split into pieces):
+    259 rows mixing short lists, empty lists, one exact tile and lists longer than one staging pass
+    (8192 entries, so the list is staged in two passes), against the oracle."""
+    from dataclasses import replace
+    w = replace(W.SMALL_MLA, seq_len=12000)
+    n_kv, n_rows, k_cap = w.seq_len, 259, 9000
+    H, dqk, dv = w.attn_dims
+    a = _attn_inputs(w, 0, n_rows, n_kv)
+    g = np.random.default_rng(7)
+    counts = g.integers(1, 400, n_rows)
+    for i in (0, 5, 6, 11, 255, 258):
+        counts[i] = 0                       # empty lists, also first and last of a group
+    for i in (1, 4, 7, 12, 257):
+        counts[i] = 8193 if i % 2 else 9000  # two staging passes
+    counts[2] = 32                           # exactly one tile
+    idx = np.full((n_rows, k_cap), -1, np.int32)
+    for i, c in enumerate(counts):
+        idx[i, :c] = g.choice(n_kv, c, replace=False)
+    cnt = counts.astype(np.int32)
+    o, l = _gpu_attn(w, a, list(range(n_rows)), idx, cnt)
+    for i in range(n_rows):
+        if cnt[i] == 0:
+            assert np.all(o[i] == 0) and np.all(np.isneginf(l[i])), f"row {i}"
+            continue
+        oref, lref = orc.attention_for_set(a["q"][i], a["kv"], a["v"], idx[i, :cnt[i]], dv, w.sm_scale)
+        P.check_attention_row(o[i], l[i], oref, lref, f"row {i} ({cnt[i]} entries)")
+
+
 def test_mqa_long_lists():
     """MQA (16 x 128, separate K and V) over lists far longer than the L = 2048 workload's (1, 31,
     32, 33, 4097 and 9000 entries, the last tile partial), against the oracle."""
