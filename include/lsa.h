@@ -276,7 +276,7 @@ lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const 
  *              n_kv_rows
  *   k_swa      the indexer's window size: idx must end with the whole window of each row, as
  *              lsa_index_prefill writes it (rows shorter than the window hold [0, t])
- *   workspace  >= lsa_hfa_attn_workspace_size(p, n_rows) bytes, 256-byte aligned (fp32 partials)
+ *   workspace  >= lsa_hfa_attn_workspace_size(p, n_rows) bytes, 256-byte aligned (the partials)
  * Other arguments as lsa_sparse_attn. Calls on one device share the side stream and its two
  * events; the library enqueues one call's whole sequence under a lock, so concurrent calls from
  * several host threads are correct (their work on the side stream runs one call after the other).

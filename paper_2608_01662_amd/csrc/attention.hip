@@ -606,55 +606,53 @@ void mla_attn_kernel(AttnGeom a) {
     mfin[hb] = fmaxf(ma, mb);
     lt[hb] = (ma == mfin[hb] ? la : la * fast_exp2(ma - mfin[hb])) + (mb == mfin[hb] ? lb : lb * fast_exp2(mb - mfin[hb]));
   }
-  if (!SPLIT) {
-    // the normalised O of this wave (64 heads x 128 value columns, bf16) is staged head-major in
-    // the tile buffers, idle since the barrier above (272 bytes per head: 256 + 16 of padding),
-    // and written as 256-byte pieces of the head rows, four per store instruction
-    uint8_t* ost = lds + w4 * (64 * 272);
+  // The normalised O of this wave (64 heads x 128 value columns, bf16) is staged head-major in the
+  // tile buffers, idle since the barrier above (272 bytes per head: 256 + 16 of padding), and
+  // written as 256-byte pieces of the head rows, four per store instruction: to the output, or
+  // (SPLIT) to this split's partial, normalised by its own sum, which the merge weights back.
+  uint8_t* ost = lds + w4 * (64 * 272);
 #pragma unroll
-    for (int hb = 0; hb < 2; ++hb) {
-      const float inv = lt[hb] > 0.f ? 1.f / lt[hb] : 0.f;
+  for (int hb = 0; hb < 2; ++hb) {
+    const float inv = lt[hb] > 0.f ? 1.f / lt[hb] : 0.f;
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x16& ob = o[4 * hb + c];
-          const u32x2 v = {pack_bf16x2(ob[4 * q] * inv, ob[4 * q + 1] * inv),
-                           pack_bf16x2(ob[4 * q + 2] * inv, ob[4 * q + 3] * inv)};
-          *reinterpret_cast<u32x2*>(ost + (32 * hb + oj) * 272 + (32 * c + 8 * q + 4 * (lane >> 5)) * 2) = v;
-        }
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // (this wave's staging writes are done)
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& ob = o[4 * hb + c];
+        const u32x2 v = {pack_bf16x2(ob[4 * q] * inv, ob[4 * q + 1] * inv),
+                         pack_bf16x2(ob[4 * q + 2] * inv, ob[4 * q + 3] * inv)};
+        *reinterpret_cast<u32x2*>(ost + (32 * hb + oj) * 272 + (32 * c + 8 * q + 4 * (lane >> 5)) * 2) = v;
+      }
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // (this wave's staging writes are done)
+  // local head hh = 32 hb + h: head hh of the row, or (WIN) head 32 blockIdx.y + h of row 2 item + hb
+  auto split_index = [&](int hb, int h, int64_t& pi) {
+    const int64_t orow = WIN ? 2 * item + hb : row;
+    pi = (orow * a.n_split + split) * 64 + (WIN ? 32 * (int)blockIdx.y : 32 * hb) + h;
+    return orow < a.n_rows;  // WIN: the second row of an odd count is not written
+  };
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int hh = 4 * k + (lane >> 4);
-      const u32x4 v = *reinterpret_cast<const u32x4*>(ost + hh * 272 + 16 * (lane & 15));
+  for (int k = 0; k < 16; ++k) {
+    const int hh = 4 * k + (lane >> 4);
+    const u32x4 v = *reinterpret_cast<const u32x4*>(ost + hh * 272 + 16 * (lane & 15));
+    if (!SPLIT) {
       *reinterpret_cast<u32x4*>(a.out + (row * 64 + hh) * 512 + 128 * w4 + 8 * (lane & 15)) = v;
+    } else {
+      int64_t pi;
+      if (split_index(hh >> 5, hh & 31, pi)) *reinterpret_cast<u32x4*>(a.part_o + pi * 512 + 128 * w4 + 8 * (lane & 15)) = v;
     }
-    if (a.lse && w4 == 0 && lane < 32) {
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
-        a.lse[row * 64 + 32 * hb + oj] = lt[hb] > 0.f ? (mfin[hb] + __log2f(lt[hb])) * kLn2 : -INFINITY;
-    }
-  } else {
-    const int dv0 = 128 * w4 + 4 * (lane >> 5);
+  }
+  if (w4 == 0 && lane < 32) {
 #pragma unroll
     for (int hb = 0; hb < 2; ++hb) {
-      const int64_t orow = WIN ? 2 * item + hb : row;
-      if (orow >= a.n_rows) continue;  // WIN: the second row of an odd count
-      const int ohead = (WIN ? 32 * (int)blockIdx.y : 32 * hb) + oj;
-      const int64_t pi = (orow * a.n_split + split) * 64 + ohead;
-      float* po = a.part_o + pi * 512 + dv0;
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x16& ob = o[4 * hb + c];
-          *reinterpret_cast<f32x4*>(po + 32 * c + 8 * q) = f32x4{ob[4 * q], ob[4 * q + 1], ob[4 * q + 2], ob[4 * q + 3]};
+      if (!SPLIT) {
+        if (a.lse) a.lse[row * 64 + 32 * hb + oj] = lt[hb] > 0.f ? (mfin[hb] + __log2f(lt[hb])) * kLn2 : -INFINITY;
+      } else {
+        int64_t pi;
+        if (split_index(hb, oj, pi)) {
+          a.part_ml[pi * 2] = mfin[hb];
+          a.part_ml[pi * 2 + 1] = lt[hb];
         }
-      if (w4 == 0 && lane < 32) {
-        a.part_ml[pi * 2] = mfin[hb];
-        a.part_ml[pi * 2 + 1] = lt[hb];
       }
     }
   }
@@ -771,7 +769,8 @@ __global__ __launch_bounds__(64) void mqa_attn_kernel(AttnGeom a) {
 
 // ============================================================================ split combine
 // Log-sum-exp merge of the per-split partial results (the same rescaling the paper uses to
-// merge partial attentions, Sec. 4.1.1 and App. B). Grid (n_rows, H), block 128.
+// merge partial attentions, Sec. 4.1.1 and App. B): each partial is stored in bf16, normalised by
+// its own sum l_s, and weighted by l_s 2^(m_s - M) / sum_s l_s 2^(m_s - M). Grid (n_rows, H), block 128.
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnGeom a, int H, int d_v) {
   const int64_t row = blockIdx.x;
   const int head = blockIdx.y;
@@ -790,8 +789,11 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnGeom a, int H, in
       const int64_t pi = (row * a.n_split + s) * H + head;
       const float ls = a.part_ml[pi * 2 + 1];
       if (!(ls > 0.f)) continue;
-      const float wgt = fast_exp2(a.part_ml[pi * 2] - M);
-      acc += wgt * *reinterpret_cast<const f32x4*>(a.part_o + pi * d_v + d);
+      // the partial is normalised by its own sum ls: weight it back by ls 2^(m_s - M)
+      const float wgt = ls * fast_exp2(a.part_ml[pi * 2] - M);
+      const u32x2 pv = *reinterpret_cast<const u32x2*>(a.part_o + pi * d_v + d);
+      acc += wgt * f32x4{__uint_as_float(pv.x << 16), __uint_as_float(pv.x & 0xFFFF0000u),
+                         __uint_as_float(pv.y << 16), __uint_as_float(pv.y & 0xFFFF0000u)};
     }
     const u32x2 v = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
     *reinterpret_cast<u32x2*>(a.out + (row * H + head) * d_v + d) = v;

@@ -62,7 +62,7 @@ struct AttnGeom {
   int k_cap;
   uint16_t* out;           // [n_rows, H, d_v]
   float* lse;              // [n_rows, H] or nullptr
-  float* part_o;           // split partials [n_rows, n_split, H, d_v]
+  uint16_t* part_o;        // split partials, each normalised by its own sum, bf16 [n_rows, n_split, H, d_v]
   float* part_ml;          // [n_rows, n_split, H, 2]
   int64_t n_rows;
   int n_split, split_len;  // slots per split (multiple of the tile)

@@ -231,7 +231,7 @@ AttnPlan plan_attn(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int3
   pl.off_rows = off;
   if (paged) off += round_up((size_t)n_rows * k_cap * 4, 256);
   pl.off_po = off;
-  if (pl.n_split > 1) off += round_up((size_t)n_rows * pl.n_split * p->n_heads * p->d_v * 4, 256);
+  if (pl.n_split > 1) off += round_up((size_t)n_rows * pl.n_split * p->n_heads * p->d_v * 2, 256);
   pl.off_ml = off;
   if (pl.n_split > 1) off += round_up((size_t)n_rows * pl.n_split * p->n_heads * 2 * 4, 256);
   pl.total = off;
@@ -560,7 +560,7 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
     a.rows = rows;
   }
   if (pl.n_split > 1) {
-    a.part_o = reinterpret_cast<float*>(ws + pl.off_po);
+    a.part_o = reinterpret_cast<uint16_t*>(ws + pl.off_po);
     a.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   }
   hipError_t e = mla ? lsa::launch_mla_attn(a, st) : lsa::launch_mqa_attn(a, st);
@@ -640,7 +640,7 @@ lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const 
   a.scale_log2 = p->sm_scale * 1.4426950408889634f;
   a.part = -1;
   if (pl.n_split > 1) {
-    a.part_o = reinterpret_cast<float*>(ws + pl.off_po);
+    a.part_o = reinterpret_cast<uint16_t*>(ws + pl.off_po);
     a.part_ml = reinterpret_cast<float*>(ws + pl.off_ml);
   }
   const hipError_t e = lsa::launch_mla_attn(a, st);
@@ -649,16 +649,16 @@ lsa_status lsa_sparse_attn_runs(const lsa_attn_params* p, int64_t n_rows, const 
 }
 
 // ---------------------------------------------------------------- split attention (HFA)
-// Rows per pass of lsa_hfa_attn: the two fp32 partials of a row take 2 * 64 * (512 + 2) * 4 bytes.
+// Rows per pass of lsa_hfa_attn: the two partials of a row (bf16 values, fp32 maximum and sum per
+// head) take 2 * 64 * (512 * 2 + 2 * 4) bytes.
 constexpr int64_t kHfaRowsPerPass = 16384;
-constexpr size_t kHfaRowBytes = size_t(2) * 64 * (512 + 2) * 4;
 
 static int64_t hfa_rows_per_pass(int64_t n_rows) { return n_rows < kHfaRowsPerPass ? n_rows : kHfaRowsPerPass; }
 
 size_t lsa_hfa_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows) {
   if (check_attn_params(p) != LSA_OK || n_rows < 0 || p->latent == 0) return 0;
   const size_t r = (size_t)hfa_rows_per_pass(n_rows);
-  return round_up(r * 2 * 64 * 512 * 4, 256) + round_up(r * 2 * 64 * 2 * 4, 256);
+  return round_up(r * 2 * 64 * 512 * 2, 256) + round_up(r * 2 * 64 * 2 * 4, 256);
 }
 
 namespace {
@@ -733,8 +733,8 @@ lsa_status lsa_hfa_attn(const lsa_attn_params* p, int64_t n_rows, const void* q,
   std::lock_guard<std::mutex> call_lock(g_hfa_call_mu);
   const int64_t rpp = hfa_rows_per_pass(n_rows);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  float* part_o = reinterpret_cast<float*>(ws);
-  float* part_ml = reinterpret_cast<float*>(ws + round_up((size_t)rpp * 2 * 64 * 512 * 4, 256));
+  uint16_t* part_o = reinterpret_cast<uint16_t*>(ws);
+  float* part_ml = reinterpret_cast<float*>(ws + round_up((size_t)rpp * 2 * 64 * 512 * 2, 256));
   for (int64_t r0 = 0; r0 < n_rows; r0 += rpp) {
     const int64_t nr = n_rows - r0 < rpp ? n_rows - r0 : rpp;
     lsa::AttnGeom a{};

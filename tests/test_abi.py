@@ -234,9 +234,10 @@ def test_bad_split_attention_arguments():
     assert hfa(ws=None) == WORKSPACE
     assert hfa(wsb=16) == WORKSPACE
     assert hfa(n_rows=0, q=None, idx=None, cnt=None, out=None, ws=None, wsb=0) == OK
-    # two fp32 partials (O and (m, l)) per row and head, for at most 16384 rows per pass
-    assert L.lsa_hfa_attn_workspace_size(ctypes.byref(mla.c()), 100) == 100 * 2 * 64 * (512 + 2) * 4
-    assert L.lsa_hfa_attn_workspace_size(ctypes.byref(mla.c()), 131072) == 16384 * 2 * 64 * (512 + 2) * 4
+    # two partials per row and head (O normalised, in bf16, and (m, l) in fp32), for at most 16384
+    # rows per pass
+    assert L.lsa_hfa_attn_workspace_size(ctypes.byref(mla.c()), 100) == 100 * 2 * 64 * (512 * 2 + 2 * 4)
+    assert L.lsa_hfa_attn_workspace_size(ctypes.byref(mla.c()), 131072) == 16384 * 2 * 64 * (512 * 2 + 2 * 4)
 
 
 def test_workspace_sizes():
