@@ -360,6 +360,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   const int64_t row0 = (int64_t)(STAGED ? gridDim.x - 1 - blockIdx.x : blockIdx.x) * R;
   const int nsub = g.P / g.B;
 
+  if constexpr (PAGED) {
+    // Decode: one row, chunks of 8 tiles, wave wv scoring tiles wv and wv + 4 of its chunk. The
+    // page-table entries of both tiles and the query are requested before the context length is
+    // known (any page below max_pages lies inside the sequence's table row), and both tiles' block
+    // keys together, so the scores wait for two round trips instead of four. Pages past the
+    // row's eligible range are scored but not stored.
+    static_assert(R == 1 && !STAGED, "paged scoring takes one row per workgroup");
+    const int64_t row = row0, p_base = g.k_sink / g.P;  // first eligible page (k_sink only)
+    const int64_t tile_beg = (int64_t)blockIdx.y * tiles_per_chunk;
+    int64_t pp[2], ph[2];
+    int sub[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t sb = (tile_beg + wv + 4 * u) * 32 + j;  // sub-block counted from the first eligible page
+      pp[u] = p_base + sb / nsub;
+      sub[u] = (int)(sb % nsub);
+      ph[u] = phys_page(g, row, pp[u]);
+    }
+    u32x4 a[KS];
+    float wr[16];
+    if constexpr (MINMAX) load_query_minmax<D>(q, g.H, row, lane, a);
+    else load_query_operand<D>(q, g.H, row, lane, a);
+    load_head_weights(w, g.H, row, lane, wr);
+    const RowInfo ri = row_info(g, row);
+    if (!ri.valid || ri.p_hi < ri.p_lo) return;
+    const int64_t n_tiles = ((ri.p_hi - ri.p_lo + 1) * nsub + 31) / 32;
+    u32x4 b[2][KS];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t mrow = ph[u] >= 0 ? ph[u] * nsub + sub[u] : 0;
+      const u32x4* pk = reinterpret_cast<const u32x4*>(kmean + mrow * DK + (DK / 2) * (lane >> 5));
+#pragma unroll
+      for (int s = 0; s < KS; ++s) b[u][s] = pk[s];
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t tile = tile_beg + wv + 4 * u;
+      if (4 * u + wv >= tiles_per_chunk || tile >= n_tiles) break;  // (wave-uniform)
+      f32x16 acc = {};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) acc = mfma32(a[s], b[u][s], acc);
+      float v = head_reduce(acc, wr);
+      for (int o = 1; o < nsub; o <<= 1) v += __shfl_xor(v, o);  // sum the sub-blocks of a page
+      if (lane < 32 && sub[u] == 0 && pp[u] <= ri.p_hi) page_keys[row * ld + pp[u]] = ph[u] >= 0 ? score_key(v) : 0u;
+    }
+    return;
+  }
+
   RowInfo ri[R];
   int64_t max_tiles = 0;
 #pragma unroll
@@ -448,14 +496,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     const int sub_in_page = (int)(sb % nsub);
     int64_t mrow = 0;
     bool okp = true;
-    if (PAGED) {
-      const int64_t ph = (R == 1 && p <= ri[0].p_hi) ? phys_page(g, row0, p) : -1;
-      okp = ph >= 0;
-      mrow = okp ? ph * nsub + sub_in_page : 0;
-    } else {
-      okp = p * nsub + sub_in_page < g.n_sub;
-      mrow = okp ? p * nsub + sub_in_page : 0;
-    }
+    okp = p * nsub + sub_in_page < g.n_sub;
+    mrow = okp ? p * nsub + sub_in_page : 0;
     u32x4 b[KS];
     {
       const u32x4* pk = reinterpret_cast<const u32x4*>(kmean + mrow * DK + (DK / 2) * (lane >> 5));
@@ -798,9 +840,15 @@ __device__ __forceinline__ void range_threshold(Each&& each, uint32_t lo, uint32
 // ============================================================================ Stage 1: page top-M
 // Eq. (10): P_t = the M eligible pages of largest coarse score (ties to the smaller page),
 // written in ascending page order and padded with -1. All eligible pages when there are <= M.
+// Decode (paged cache) also writes, for the k-th recalled page, its physical page (-1 when the
+// page-table entry is out of range) to phys[row * ld + k], in the row's own page-key area: the
+// fine stage then reads page and physical page side by side instead of a page-table lookup that
+// waits for the page. The page-table entries of every eligible page are read into LDS together
+// with the page keys, so the lookup adds no round trip here either. (phys aliases page_keys: each
+// workgroup reads its row's keys into LDS before its first barrier and writes phys after it.)
 template <int NT>
-__global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* __restrict__ page_keys,
-                                                         int64_t ld, int32_t* __restrict__ pages) {
+__global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_rows, const uint32_t* page_keys,
+                                                         int64_t ld, int32_t* __restrict__ pages, int32_t* phys) {
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t hist[2 * kRangeBins];
   __shared__ __align__(16) uint32_t cand[64];
@@ -811,16 +859,23 @@ __global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_
   const int64_t row = blockIdx.x;
   const RowInfo ri = row_info(g, row);
   int32_t* out = pages + row * g.M;
+  int32_t* pout = phys ? phys + row * ld : nullptr;
   const int64_t n_elig = (ri.valid && ri.p_hi >= ri.p_lo) ? ri.p_hi - ri.p_lo + 1 : 0;
   if (n_elig <= g.M) {
     for (int i = threadIdx.x; i < g.M; i += NT) out[i] = i < n_elig ? (int32_t)(ri.p_lo + i) : -1;
+    if (pout)
+      for (int i = threadIdx.x; i < n_elig; i += NT) pout[i] = (int32_t)phys_page(g, row, ri.p_lo + i);
     return;
   }
   const int n = (int)n_elig;
   uint32_t* keys = smem;
+  int32_t* ptab = reinterpret_cast<int32_t*>(smem + n);  // decode: physical pages of the eligible pages
   for (int i = threadIdx.x; i < 2 * kRangeBins; i += NT) hist[i] = 0u;
   if (threadIdx.x < kRangeAux) aux[threadIdx.x] = (threadIdx.x == 6 || threadIdx.x == 8) ? ~0u : 0u;
-  for (int i = threadIdx.x; i < n; i += NT) keys[i] = page_keys[row * ld + ri.p_lo + i];
+  for (int i = threadIdx.x; i < n; i += NT) {
+    keys[i] = page_keys[row * ld + ri.p_lo + i];
+    if (pout) ptab[i] = (int32_t)phys_page(g, row, ri.p_lo + i);
+  }
   __syncthreads();
   // thread x holds the contiguous slice [x E, x E + E) of the row's page keys
   const int E = (n + NT - 1) / NT;
@@ -849,37 +904,62 @@ __global__ __launch_bounds__(NT) void page_select_kernel(IndexGeom g, int64_t n_
   for (int i = b; i < e; ++i) {
     const uint32_t key = keys[i];
     const bool is_eq = key == T;
-    if (key > T || (is_eq && eqr < take)) out[rank++] = (int32_t)(ri.p_lo + i);
+    if (key > T || (is_eq && eqr < take)) {
+      if (pout) pout[rank] = ptab[i];
+      out[rank++] = (int32_t)(ri.p_lo + i);
+    }
     eqr += is_eq;
   }
 }
 
 // ============================================================================ Stage 2: fine token scores
-// Eq. (11) over the recalled pages (Eq. 1 over E_t in flat mode). Grid: (n_rows, chunks of
-// pages_per_wg pages); each wave scores whole pages in 32-token MFMA tiles. Output:
-// fine_keys[row * ldf + k * P + offset] = order key of the score of position page_k * P +
-// offset, or 0 for positions outside E_t.
-template <int D, bool FP8, bool PAGED>
+// Eq. (11) over the recalled pages (Eq. 1 over E_t in flat mode), decode variant (paged cache).
+// Grid: (n_rows, chunks of pages_per_wg pages); each wave scores whole pages in 32-token MFMA
+// tiles. Output: fine_keys[row * ldf + k * P + offset] = order key of the score of position
+// page_k * P + offset, or 0 for positions outside E_t.
+// Hierarchical mode reads the k-th recalled page from pages[row * M + k] and its physical page
+// from phys[row * ldp + k] (written by the page selection); flat mode (phys == nullptr) takes the
+// eligible pages in order and looks their physical pages up in the page table. The page ids, the
+// physical pages and the query are requested before the row's context length is known (every
+// such read stays inside its array), so that the first key tile waits for one round trip after
+// them, not for a chain of context length, page, page-table entry and keys.
+template <int D, bool FP8>
 __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, const uint16_t* __restrict__ q,
                                                    const float* __restrict__ w, const void* __restrict__ k,
                                                    const float* __restrict__ kscale, const int32_t* __restrict__ pages,
+                                                   const int32_t* __restrict__ phys, int64_t ldp,
                                                    uint32_t* __restrict__ fine_keys, int64_t ldf, int pages_per_wg) {
   constexpr int KS = D / 16;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, j = lane & 31;
   const int64_t row = blockIdx.x;
-  const RowInfo ri = row_info(g, row);
-  if (!ri.valid || ri.p_hi < ri.p_lo) return;
-  const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
   const bool flat = g.M <= 0;
-  const int64_t n_sel = flat ? n_elig : (n_elig < g.M ? n_elig : g.M);
   const int64_t k0 = (int64_t)blockIdx.y * pages_per_wg;
-  const int64_t k1 = k0 + pages_per_wg < n_sel ? k0 + pages_per_wg : n_sel;
-  if (k0 >= k1) return;
-
+  // this wave's first two pages (every fourth of the chunk, two at a time; see below): ids and
+  // physical pages requested up front (slots below min(M, ldp) are inside the row's arrays)
+  int32_t pg_pre[2] = {-1, -1}, ph_pre[2] = {-1, -1};
+  if (!flat) {
+    const int64_t lim = g.M < ldp ? g.M : ldp;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t kk = k0 + wv + 4 * u;
+      if (kk < lim) {
+        pg_pre[u] = pages[row * g.M + kk];
+        ph_pre[u] = phys[row * ldp + kk];
+      }
+    }
+  }
   u32x4 a[KS];
   float wr[16];
   load_query_operand<D>(q, g.H, row, lane, a);
   load_head_weights(w, g.H, row, lane, wr);
+
+  const RowInfo ri = row_info(g, row);
+  if (!ri.valid || ri.p_hi < ri.p_lo) return;
+  const int64_t n_elig = ri.p_hi - ri.p_lo + 1;
+  const int64_t n_sel = flat ? n_elig : (n_elig < g.M ? n_elig : g.M);
+  const int64_t k1 = k0 + pages_per_wg < n_sel ? k0 + pages_per_wg : n_sel;
+  if (k0 >= k1) return;
+
   i32x8 qh[D / 64], ql[D / 64];
   if constexpr (FP8) query_fp8<D>(a, lane, qh, ql, wr);
 
@@ -900,18 +980,23 @@ __global__ __launch_bounds__(256) void fine_kernel(IndexGeom g, int64_t n_rows, 
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int64_t kk = kk0 + 4 * u;
-      pg[u] = kk < k1 ? (flat ? ri.p_lo + kk : (int64_t)pages[row * g.M + kk]) : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
+      int64_t ph = -1;
+      pg[u] = -1;
+      if (kk < k1) {
+        if (flat) {
+          pg[u] = ri.p_lo + kk;
+        } else if (kk0 == k0 + wv) {  // the pair requested up front
+          pg[u] = pg_pre[u];
+          ph = ph_pre[u];
+        } else {
+          pg[u] = pages[row * g.M + kk];
+          ph = phys[row * ldp + kk];
+        }
+      }
       kb[u] = -1;  // key row of the page's first token
       if (pg[u] >= ri.p_lo && pg[u] <= ri.p_hi) {
-        if (PAGED) {
-          const int64_t ph = phys_page(g, row, pg[u]);
-          kb[u] = ph >= 0 ? ph * g.kv_page : -1;
-        } else {
-          kb[u] = pg[u] * g.P;  // positions checked below stay <= hi < n_kv
-        }
+        if (flat) ph = phys_page(g, row, pg[u]);
+        kb[u] = ph >= 0 ? ph * g.kv_page : -1;
       }
     }
     const int n_items = (kk0 + 4 < k1 ? 2 : 1) * tpp;
@@ -1749,25 +1834,27 @@ hipError_t launch_coarse(const IndexGeom& g, int64_t n_rows, const uint16_t* q, 
 }
 
 hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t* page_keys, int64_t ld,
-                              int32_t* pages, int64_t max_elig, hipStream_t st) {
+                              int32_t* pages, int32_t* phys, int64_t max_elig, hipStream_t st) {
   if (n_rows == 0) return hipSuccess;
-  const size_t lds = (size_t)(max_elig > 0 ? max_elig : 1) * 4;
+  const size_t lds = page_select_lds_bytes(max_elig, phys != nullptr);
   if (n_rows <= kSelectFewRows)  // few rows (decode): more threads per row
-    hipLaunchKernelGGL(page_select_kernel<1024>, dim3((unsigned)n_rows), dim3(1024), lds, st, g, n_rows, page_keys, ld, pages);
+    hipLaunchKernelGGL(page_select_kernel<1024>, dim3((unsigned)n_rows), dim3(1024), lds, st, g, n_rows, page_keys, ld,
+                       pages, phys);
   else
-    hipLaunchKernelGGL(page_select_kernel<256>, dim3((unsigned)n_rows), dim3(256), lds, st, g, n_rows, page_keys, ld, pages);
+    hipLaunchKernelGGL(page_select_kernel<256>, dim3((unsigned)n_rows), dim3(256), lds, st, g, n_rows, page_keys, ld,
+                       pages, phys);
   return hipGetLastError();
 }
 
-template <int D, bool FP8, bool PAGED>
+template <int D, bool FP8>
 static hipError_t launch_fine_t(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
-                                const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf,
-                                int64_t max_sel, hipStream_t st) {
-  const int ppw = PAGED ? 8 : (int)(max_sel > 0 ? max_sel : 1);
+                                const float* ks, const int32_t* pages, const int32_t* phys, int64_t ldp,
+                                uint32_t* fine_keys, int64_t ldf, int64_t max_sel, hipStream_t st) {
+  constexpr int ppw = 8;  // recalled pages per workgroup (two per wave)
   const int64_t chunks = (max_sel + ppw - 1) / ppw;
   if (chunks == 0 || n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL((fine_kernel<D, FP8, PAGED>), dim3((unsigned)n_rows, (unsigned)chunks), dim3(256), 0, st, g, n_rows,
-                     q, w, k, ks, pages, fine_keys, ldf, ppw);
+  hipLaunchKernelGGL((fine_kernel<D, FP8>), dim3((unsigned)n_rows, (unsigned)chunks), dim3(256), 0, st, g, n_rows, q, w,
+                     k, ks, pages, phys, ldp, fine_keys, ldf, ppw);
   return hipGetLastError();
 }
 
@@ -1792,8 +1879,8 @@ static hipError_t launch_flat_dense_t(const IndexGeom& g, int64_t n_rows, const 
 }
 
 hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
-                       const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
-                       hipStream_t st) {
+                       const float* ks, const int32_t* pages, const int32_t* phys, int64_t ldp, uint32_t* fine_keys,
+                       int64_t ldf, int64_t max_sel, hipStream_t st) {
   const bool paged = g.ctx_len != nullptr, fp8 = g.fp8 != 0;
   if (!paged && g.M <= 0) {  // flat prefill: dense causal scoring
     if (max_sel <= 0) return hipSuccess;
@@ -1810,10 +1897,11 @@ hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, co
                : launch_fine_xcd_t<64, false>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, st);
   }
   // paged decode: per (sequence, page) through the page table
-  if (g.D == 128) return fp8 ? launch_fine_t<128, true, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
-                             : launch_fine_t<128, false, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st);
-  return fp8 ? launch_fine_t<64, true, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st)
-             : launch_fine_t<64, false, true>(g, n_rows, q, w, k, ks, pages, fine_keys, ldf, max_sel, st);
+  if (g.D == 128)
+    return fp8 ? launch_fine_t<128, true>(g, n_rows, q, w, k, ks, pages, phys, ldp, fine_keys, ldf, max_sel, st)
+               : launch_fine_t<128, false>(g, n_rows, q, w, k, ks, pages, phys, ldp, fine_keys, ldf, max_sel, st);
+  return fp8 ? launch_fine_t<64, true>(g, n_rows, q, w, k, ks, pages, phys, ldp, fine_keys, ldf, max_sel, st)
+             : launch_fine_t<64, false>(g, n_rows, q, w, k, ks, pages, phys, ldp, fine_keys, ldf, max_sel, st);
 }
 
 // Which selection kernel serves rows of slots_cap candidates: keys in registers, staged in LDS,

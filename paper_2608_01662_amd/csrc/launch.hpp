@@ -27,11 +27,19 @@ hipError_t launch_block_keys(int64_t n_items, const int64_t* rows, int64_t n_tok
                              const void* k, const float* ks, uint16_t* out, hipStream_t st);
 hipError_t launch_coarse(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const uint16_t* kmean,
                          uint32_t* page_keys, int64_t ld, int64_t max_tiles, hipStream_t st);
+// Page selection; with phys != nullptr (paged decode) it also writes each recalled page's physical
+// page to phys[row * ld + k], which may alias page_keys (the row's keys are read first).
 hipError_t launch_page_select(const IndexGeom& g, int64_t n_rows, const uint32_t* page_keys, int64_t ld,
-                              int32_t* pages, int64_t max_elig, hipStream_t st);
+                              int32_t* pages, int32_t* phys, int64_t max_elig, hipStream_t st);
+// Dynamic LDS bytes of the page selection over rows of up to max_elig eligible pages.
+inline size_t page_select_lds_bytes(int64_t max_elig, bool with_phys) {
+  return (size_t)(max_elig > 0 ? max_elig : 1) * (with_phys ? 8 : 4);
+}
+// Fine scoring; paged decode reads the recalled pages' physical pages from phys (row stride ldp)
+// as the page selection wrote them (nullptr in flat mode: looked up in the page table).
 hipError_t launch_fine(const IndexGeom& g, int64_t n_rows, const uint16_t* q, const float* w, const void* k,
-                       const float* ks, const int32_t* pages, uint32_t* fine_keys, int64_t ldf, int64_t max_sel,
-                       hipStream_t st);
+                       const float* ks, const int32_t* pages, const int32_t* phys, int64_t ldp, uint32_t* fine_keys,
+                       int64_t ldf, int64_t max_sel, hipStream_t st);
 // Dynamic LDS bytes of the token selection; rows of up to kSelectRegMax candidates keep their keys
 // in registers (20 KB of static LDS), larger ones stage them in LDS (4 KB of static LDS).
 constexpr int64_t kSelectRegMax = 512 * 64;

@@ -124,7 +124,8 @@ IndexPlan plan_index(const lsa_index_params* p, int64_t n_rows, int64_t max_kv, 
   return pl;
 }
 
-lsa_status check_lds(const lsa_index_params* p, const IndexPlan& pl) {
+// paged: decode (the page selection also stages the page-table entries of the eligible pages)
+lsa_status check_lds(const lsa_index_params* p, const IndexPlan& pl, bool paged) {
   const int k_cap = p->k_sink + p->k_swa + p->k_sparse;
   const size_t ts = lsa::token_select_lds_bytes(pl.slots, k_cap, p->keep_pages);
   LSA_REQUIRE(ts + lsa::token_select_static_lds(pl.slots) <= kMaxLds, LSA_ERR_UNSUPPORTED,
@@ -132,7 +133,7 @@ lsa_status check_lds(const lsa_index_params* p, const IndexPlan& pl) {
               "lower k_sparse + k_sink + k_swa or keep_pages",
               (long long)pl.slots, k_cap);
   if (p->keep_pages > 0)
-    LSA_REQUIRE((size_t)pl.n_pages * 4 + kSelectStaticLds <= kMaxLds, LSA_ERR_UNSUPPORTED,
+    LSA_REQUIRE(lsa::page_select_lds_bytes(pl.n_pages, paged) + kSelectStaticLds <= kMaxLds, LSA_ERR_UNSUPPORTED,
                 "%lld pages per row exceed the LDS of the page selection", (long long)pl.n_pages);
   return LSA_OK;
 }
@@ -181,15 +182,18 @@ lsa_status run_index(const lsa_index_params* p, const lsa::IndexGeom& g, int64_t
     const auto* q16 = static_cast<const uint16_t*>(q) + r0 * g.H * g.D;
     const float* wp = w + r0 * g.H;
     int32_t* pages = pages_out ? pages_out + r0 * g.M : reinterpret_cast<int32_t*>(ws + pl.off_pages);
+    int32_t* phys = (g.ctx_len && g.M > 0) ? reinterpret_cast<int32_t*>(page_keys) : nullptr;
     if (g.M > 0) {
       const int64_t max_tiles = cdiv(max_elig * (g.P / g.B), 32);
       e = lsa::launch_coarse(gp, nr, q16, wp, static_cast<const uint16_t*>(block_keys), page_keys, pl.n_pages,
                              max_tiles, st);
       if (e != hipSuccess) return hip_fail(e, "coarse page scoring");
-      e = lsa::launch_page_select(gp, nr, page_keys, pl.n_pages, pages, max_elig, st);
+      // decode: the physical pages of the recalled ones go to the row's page-key area, which the
+      // page selection has read by then
+      e = lsa::launch_page_select(gp, nr, page_keys, pl.n_pages, pages, phys, max_elig, st);
       if (e != hipSuccess) return hip_fail(e, "page selection");
     }
-    e = lsa::launch_fine(gp, nr, q16, wp, k, k_scale, pages, fine, pl.slots, max_sel, st);
+    e = lsa::launch_fine(gp, nr, q16, wp, k, k_scale, pages, phys, pl.n_pages, fine, pl.slots, max_sel, st);
     if (e != hipSuccess) return hip_fail(e, "fine token scoring");
     e = lsa::launch_token_select(gp, nr, fine, pl.slots, g.M > 0 ? pages : nullptr, idx + r0 * k_cap, count + r0,
                                  runs ? reinterpret_cast<int32_t*>(runs + r0 * k_cap) : nullptr,
@@ -358,7 +362,7 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
   LSA_REQUIRE(aligned(pages_out, 4), LSA_ERR_INVALID_ARG, "pages_out must be 4-byte aligned");
   const lsa_index_params e = effective_params(p, n_kv);
   const IndexPlan pl = plan_index(&e, n_q, n_kv);
-  s = check_lds(&e, pl);
+  s = check_lds(&e, pl, false);
   if (s != LSA_OK) return s;
   if (n_q == 0) return LSA_OK;  // nothing to read or write
   s = check_index_io(&e, q, w, k, k_scale, block_keys, n_kv / p->sub_block, idx, count, runs, run_count, workspace,
@@ -398,7 +402,7 @@ static lsa_status decode_setup(const lsa_index_params* p, int32_t batch, const i
   const int64_t max_kv = (int64_t)max_pages * kv_page_size;
   const lsa_index_params e = effective_params(p, max_kv);
   const IndexPlan pl = plan_index(&e, batch, max_kv, budget);
-  s = check_lds(&e, pl);
+  s = check_lds(&e, pl, true);
   if (s != LSA_OK) return s;
   if (budget != 0) {
     const size_t row = index_row_bytes(&e, max_kv);
