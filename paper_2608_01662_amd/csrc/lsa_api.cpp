@@ -454,8 +454,10 @@ lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int3
 // fine-score keys) of one row pass lives in this fixed device array instead of a caller-owned
 // workspace. Each device holds its own copy until the process ends. Host code must not use the
 // array's name as an address: its device address is looked up once per device (first call there)
-// and only that pointer is passed to kernels. Nothing in it needs to start at zero (every entry a
-// kernel reads is written earlier in the same call), and it keeps the last call's contents.
+// and only that pointer is passed to kernels. Nothing in it needs to start at zero: every entry a
+// kernel uses is written earlier in the same call (the paged fine kernel requests the page slots
+// of its chunk before it knows how many of them the row has, and ignores the others), and it
+// keeps the last call's contents.
 static __device__ __align__(256) uint8_t scratch[LSA_STATIC_SCRATCH_BYTES];
 
 namespace {
