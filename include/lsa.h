@@ -214,7 +214,7 @@ typedef struct lsa_attn_params {
   float sm_scale;  /* softmax scale applied to q . k                                           */
 } lsa_attn_params;
 
-/* Workspace bytes for lsa_sparse_attn (non-zero only for paged / split calls). */
+/* Workspace bytes for lsa_sparse_attn (non-zero only for split calls and paged MQA calls). */
 size_t lsa_sparse_attn_workspace_size(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap,
                                       int32_t paged);
 

@@ -335,6 +335,22 @@ void mla_attn_kernel(AttnGeom a) {
         const int i = (int)threadIdx.x + 512 * u;
         v[u] = i < nc ? (win0 >= 0 ? (int)(win0 + c0 + i) : slots[c0 + i]) : -1;
       }
+      if (a.page_table) {  // paged cache: position -> cache row through the sequence's page table
+        const int32_t* tab = a.page_table + (row / a.rows_per_seq) * a.max_pages;
+        const int kvp = a.kv_page;
+        const bool p2 = (kvp & (kvp - 1)) == 0;
+        const int lg = __ffs(kvp) - 1;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int pos = v[u];
+          if (pos >= 0) {
+            const int pg = p2 ? pos >> lg : pos / kvp;
+            const int64_t ph = pg < a.max_pages ? tab[pg] : -1;
+            const int64_t cr = ph * kvp + (pos - pg * kvp);
+            v[u] = (ph >= 0 && cr < a.n_kv_rows) ? (int)cr : -1;
+          }
+        }
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int i = (int)threadIdx.x + 512 * u;

@@ -85,6 +85,11 @@ struct AttnGeom {
   // of the runs (start, length) runs[r, 0..run_count[r]), int32 pairs with row stride k_cap.
   const int32_t* runs;
   const int32_t* run_count;
+  // Paged cache (MLA list form; nullptr = rows are cache rows): rows holds positions, and position
+  // s of query row r is cache row page_table[(r / rows_per_seq) * max_pages + s / kv_page] *
+  // kv_page + s % kv_page, translated while the list is staged.
+  const int32_t* page_table;
+  int max_pages, kv_page, rows_per_seq;
 };
 
 hipError_t launch_mla_attn(const AttnGeom& a, hipStream_t st);

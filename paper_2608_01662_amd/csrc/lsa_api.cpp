@@ -232,8 +232,8 @@ AttnPlan plan_attn(const lsa_attn_params* p, int64_t n_rows, int32_t k_cap, int3
     }
   }
   size_t off = 0;
-  pl.off_rows = off;
-  if (paged) off += round_up((size_t)n_rows * k_cap * 4, 256);
+  pl.off_rows = off;  // translated cache rows (paged MQA; the MLA kernel translates as it stages)
+  if (paged && !mla) off += round_up((size_t)n_rows * k_cap * 4, 256);
   pl.off_po = off;
   if (pl.n_split > 1) off += round_up((size_t)n_rows * pl.n_split * p->n_heads * p->d_v * 2, 256);
   pl.off_ml = off;
@@ -558,7 +558,12 @@ lsa_status lsa_sparse_attn(const lsa_attn_params* p, int64_t n_rows, const void*
   a.split_len = pl.split_len;
   a.scale_log2 = p->sm_scale * 1.4426950408889634f;
   a.part = -1;  // the whole index list
-  if (paged) {
+  if (paged && mla) {  // the MLA kernel translates positions while it stages each list
+    a.page_table = page_table;
+    a.max_pages = max_pages;
+    a.kv_page = kv_page_size;
+    a.rows_per_seq = rows_per_seq;
+  } else if (paged) {
     int32_t* rows = reinterpret_cast<int32_t*>(ws + pl.off_rows);
     hipError_t e = lsa::launch_translate_rows(idx, count, n_rows, k_cap, page_table, max_pages, kv_page_size,
                                               rows_per_seq, n_kv_rows, rows, st);
