@@ -787,22 +787,62 @@ __global__ __launch_bounds__(64) void mqa_attn_kernel(AttnGeom a) {
 // Log-sum-exp merge of the per-split partial results (the same rescaling the paper uses to
 // merge partial attentions, Sec. 4.1.1 and App. B): each partial is stored in bf16, normalised by
 // its own sum l_s, and weighted by l_s 2^(m_s - M) / sum_s l_s 2^(m_s - M). Grid (n_rows, H), block 128.
+constexpr int kCombineRegs = 8;  // splits whose partials a thread holds at once
 __global__ __launch_bounds__(128) void attn_combine_kernel(AttnGeom a, int H, int d_v) {
   const int64_t row = blockIdx.x;
   const int head = blockIdx.y;
+  const int ns = a.n_split;
+  auto pidx = [&](int s) { return (row * ns + s) * H + head; };
+  if (ns <= kCombineRegs && d_v == 512) {
+    // every split's maximum, sum and four values of this thread requested together (one round trip)
+    const int d = (int)threadIdx.x * 4;
+    float ms[kCombineRegs], ls[kCombineRegs];
+    u32x2 pv[kCombineRegs];
+#pragma unroll
+    for (int s = 0; s < kCombineRegs; ++s) {
+      ms[s] = -INFINITY;
+      ls[s] = 0.f;
+      pv[s] = u32x2{0u, 0u};
+      if (s < ns) {
+        const int64_t pi = pidx(s);
+        ms[s] = a.part_ml[pi * 2];
+        ls[s] = a.part_ml[pi * 2 + 1];
+        pv[s] = *reinterpret_cast<const u32x2*>(a.part_o + pi * d_v + d);
+      }
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kCombineRegs; ++s) M = fmaxf(M, ms[s]);
+    float L = 0.f;
+    f32x4 acc = {};
+#pragma unroll
+    for (int s = 0; s < kCombineRegs; ++s) {
+      if (!(ls[s] > 0.f)) continue;
+      // the partial is normalised by its own sum ls: weight it back by ls 2^(m_s - M)
+      const float wgt = ls[s] * fast_exp2(ms[s] - M);
+      L += wgt;
+      acc += wgt * f32x4{__uint_as_float(pv[s].x << 16), __uint_as_float(pv[s].x & 0xFFFF0000u),
+                         __uint_as_float(pv[s].y << 16), __uint_as_float(pv[s].y & 0xFFFF0000u)};
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    const u32x2 v = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
+    *reinterpret_cast<u32x2*>(a.out + (row * H + head) * d_v + d) = v;
+    if (a.lse && threadIdx.x == 0) a.lse[row * H + head] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
+    return;
+  }
   float M = -INFINITY;
-  for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, a.part_ml[((row * a.n_split + s) * H + head) * 2]);
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.part_ml[pidx(s) * 2]);
   float L = 0.f;
-  for (int s = 0; s < a.n_split; ++s) {
-    const int64_t pi = (row * a.n_split + s) * H + head;
+  for (int s = 0; s < ns; ++s) {
+    const int64_t pi = pidx(s);
     const float ms = a.part_ml[pi * 2], ls = a.part_ml[pi * 2 + 1];
     L += ls > 0.f ? ls * fast_exp2(ms - M) : 0.f;
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
   for (int d = threadIdx.x * 4; d < d_v; d += 128 * 4) {
     f32x4 acc = {};
-    for (int s = 0; s < a.n_split; ++s) {
-      const int64_t pi = (row * a.n_split + s) * H + head;
+    for (int s = 0; s < ns; ++s) {
+      const int64_t pi = pidx(s);
       const float ls = a.part_ml[pi * 2 + 1];
       if (!(ls > 0.f)) continue;
       // the partial is normalised by its own sum ls: weight it back by ls 2^(m_s - M)
