@@ -173,8 +173,10 @@ lsa_status lsa_index_prefill(const lsa_index_params* p, int64_t q_start, int64_t
  *   k, k_scale  [n_phys * kv_page_size, d_I] keys (+ scales) of the page pool
  *   block_keys  [n_phys * kv_page_size / B, d_I] bf16 mean keys of the page pool
  *               ([.., 2 d_I] extrema with LSA_POOL_MINMAX)
- * Outputs as in lsa_index_prefill with n_q = batch. Rows whose ctx_len or page-table entries
- * are out of range get count = 0.
+ * Outputs as in lsa_index_prefill with n_q = batch. Rows whose ctx_len is out of range get
+ * count = 0. A page whose page-table entry lies outside [0, n_phys) is scored 0 and gives no token
+ * to the sparse part (its keys are never read); the row's sink and window positions are listed
+ * whatever the table holds (lsa_sparse_attn skips the positions it cannot map).
  */
 lsa_status lsa_index_decode(const lsa_index_params* p, int32_t batch, const int32_t* ctx_len,
                             const int32_t* page_table, int32_t max_pages, int32_t kv_page_size,

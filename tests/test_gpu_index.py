@@ -514,6 +514,48 @@ def test_decode_bad_rows_are_skipped():
     assert out["count"][2].item() > 0
 
 
+def test_decode_bad_page_table_entries():
+    """Page-table entries outside [0, n_phys) (here -1 and n_phys) in one sequence's eligible range:
+    the pages they name are scored 0 and never give a token to the sparse part (their key rows are
+    never read), the row keeps its sink, its window and a full sparse part from its other pages,
+    and every other sequence's output is unchanged. The paged attention over the result reads only
+    mapped rows (finite output for the row)."""
+    w = W.SMALL_DECODE
+    ctx, table, n_phys, inp = _decode_case(w)
+    prm = w.index_params()
+    q, wt, k, ks = P.gpu_index_inputs(inp, w)
+    bk = lsa.block_keys(prm, k, ks)
+    good = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk)
+    r = 3
+    t = int(ctx[r]) - 1
+    hi_page = (t - w.k_swa) // w.kv_page
+    bad = [hi_page // 3, (2 * hi_page) // 3]
+    assert 0 < bad[0] < bad[1] < hi_page
+    tab = table.copy()
+    tab[r, bad[0]] = -1
+    tab[r, bad[1]] = n_phys
+    dtab = P.to_dev(tab)
+    out = lsa.index_decode(prm, P.to_dev(ctx), dtab, w.kv_page, n_phys, q, wt, k, ks, bk)
+    torch.cuda.synchronize()
+    gi, gc = good["idx"].cpu().numpy(), good["count"].cpu().numpy()
+    idx, cnt = out["idx"].cpu().numpy(), out["count"].cpu().numpy()
+    for b in range(w.batch):
+        if b != r:
+            assert cnt[b] == gc[b] and np.array_equal(idx[b], gi[b]), f"sequence {b} changed"
+    S = idx[r][: cnt[r]]
+    assert cnt[r] == gc[r] == w.k_sink + w.k_swa + w.k_sparse
+    for p in bad:
+        assert not np.any((S >= p * w.kv_page) & (S < (p + 1) * w.kv_page)), f"token of unmapped page {p} selected"
+    assert set(range(w.k_sink)) <= set(S.tolist()) and set(range(t - w.k_swa + 1, t + 1)) <= set(S.tolist())
+    H, dqk, dv = w.attn_dims
+    a = synth.attention_inputs(w.seed, 0, w.batch, n_phys * w.kv_page, H, dqk, dv, latent=True)
+    qa, kv = P.bf16_dev(a["q"]), P.bf16_dev(a["kv"]).view(n_phys, w.kv_page, dqk)
+    o, l = lsa.sparse_attn(w.attn_params(), qa, kv, None, out["idx"], out["count"], page_table=dtab,
+                           kv_page_size=w.kv_page)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o[r].float()).all() and torch.isfinite(l[r]).all()
+
+
 @pytest.mark.parametrize("w", [W.SMALL_DECODE, W.SMALL_DECODE_MINMAX], ids=lambda w: w.name)
 def test_decode_short_contexts(w):
     """Paged decode at the context lengths where the streaming split changes shape: one token,
