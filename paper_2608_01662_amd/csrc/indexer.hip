@@ -16,6 +16,8 @@
 // half h supply dims (d_I/2)*h + 8*s .. +7 of both operands. Any permutation applied to both
 // operands leaves the dot product unchanged, and this one lets every lane read one contiguous
 // run of key bytes.
+#include <atomic>
+
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -2050,11 +2052,11 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t st) {
 // Lets the two select kernels use up to 156 KB of dynamic LDS (gfx950 has 160 KB per
 // workgroup); done once per device.
 hipError_t prepare_index_kernels() {
-  static bool done[64] = {};
+  static std::atomic<bool> done[64] = {};  // per device; repeated setup by racing threads is harmless
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev >= 0 && dev < 64 && done[dev]) return hipSuccess;
+  if (dev >= 0 && dev < 64 && done[dev].load(std::memory_order_acquire)) return hipSuccess;
   const int lim = (int)kSelectLdsLimit;
   const void* sel[] = {(const void*)token_select_kernel<512, false>, (const void*)token_select_kernel<1024, true>,
                        (const void*)token_select_reg_kernel<512, 16>, (const void*)token_select_reg_kernel<512, 32>,
@@ -2070,7 +2072,7 @@ hipError_t prepare_index_kernels() {
   e = hipFuncSetAttribute((const void*)page_select_kernel<1024>, hipFuncAttributeMaxDynamicSharedMemorySize, lim - 4096);
   if (e != hipSuccess) return e;
 
-  if (dev >= 0 && dev < 64) done[dev] = true;
+  if (dev >= 0 && dev < 64) done[dev].store(true, std::memory_order_release);
   return hipSuccess;
 }
 
