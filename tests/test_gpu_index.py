@@ -468,20 +468,26 @@ def _decode_case(w, signed_weights=False):
 
 _DECODE_D64 = replace(W.SMALL_DECODE, name="small_decode_b8_d64_fp8", head_dim=64)
 _DECODE_D64_MINMAX = replace(W.SMALL_DECODE_MINMAX, name="small_decode_b8_d64_bf16_minmax", head_dim=64, fp8=False)
+_DECODE_BF16 = replace(W.SMALL_DECODE, name="small_decode_b8_bf16", fp8=False)
+_DECODE_FLAT = replace(W.SMALL_DECODE, name="small_decode_b8_flat", keep_pages=0)
 
 
 @pytest.mark.parametrize("w,signed", [(W.SMALL_DECODE, False), (W.SMALL_DECODE_MINMAX, False), (_DECODE_D64, False),
-                                      (_DECODE_D64_MINMAX, False), (W.SMALL_DECODE, True)],
-                         ids=["mean", "minmax", "d64_fp8", "d64_bf16_minmax", "signed_w"])
+                                      (_DECODE_D64_MINMAX, False), (W.SMALL_DECODE, True), (_DECODE_BF16, False),
+                                      (_DECODE_FLAT, False)],
+                         ids=["mean", "minmax", "d64_fp8", "d64_bf16_minmax", "signed_w", "bf16", "flat"])
 def test_index_decode_parity(w, signed):
     """Paged decode indexer against the oracle on every sequence. The d_I = 64 cases run the paged
     coarse instances coarse_kernel<64, 1, true, false / true> and fine_kernel<64, fp8 / bf16>;
-    signed_w draws head weights of either sign (two of the eight sequences with all weights <= 0)."""
+    bf16 runs fine_kernel<128, bf16>; flat (keep_pages = 0) runs the fine kernel over every eligible
+    page, looked up in the page table, and the selection over all of them; signed_w draws head
+    weights of either sign (two of the eight sequences with all weights <= 0)."""
     ctx, table, n_phys, inp = _decode_case(w, signed)
     prm = w.index_params()
     q, wt, k, ks = P.gpu_index_inputs(inp, w)
-    bk = lsa.block_keys(prm, k, ks)
-    out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk, pages=True)
+    hier = w.keep_pages > 0
+    bk = lsa.block_keys(prm, k, ks) if hier else None
+    out = lsa.index_decode(prm, P.to_dev(ctx), P.to_dev(table), w.kv_page, n_phys, q, wt, k, ks, bk, pages=hier)
     torch.cuda.synchronize()
     out = {key: v.cpu().numpy() for key, v in out.items()}
     prmo = P.oracle_params(w)
@@ -494,7 +500,7 @@ def test_index_decode_parity(w, signed):
         k_mean = P.oracle_block_cache(w, k_log)
         res.append(P.oracle_index_row(t, qf[b], inp["w"][b], k_log, k_mean, prmo))
         rows_t.append(t)
-    P.check_index_rows(w, rows_t, out["idx"], out["count"], out["pages"], res)
+    P.check_index_rows(w, rows_t, out["idx"], out["count"], out.get("pages"), res)
     P.check_runs(out["runs"], out["run_count"], out["idx"], out["count"], w.run_align)
 
 
